@@ -1,0 +1,130 @@
+/*
+ * bitnet_mi355x.h -- C ABI of the ternary-weight x int8-activation mpGEMM library for AMD MI355X (gfx950).
+ *
+ * The library computes the mixed-precision GEMM/GEMV that Bitnet.cpp (arXiv 2502.11880) identifies as the
+ * bulk of ternary-LLM inference time (abstract; Sec. 1), in three calls that follow the phases of the
+ * paper's algorithms (Algorithm "MAD-based mpGEMM", Algorithm "ELUT mpGEMM", Algorithms TL1/TL2):
+ *
+ *   bitnet_pack_weights   offline weight preprocessing: absmean ternarisation + packing (Sec. 2.1, Table 1)
+ *   bitnet_quantize_act   per-call activation preprocessing: per-token absmax int8 (Sec. 2.1, Sec. 3.2.2)
+ *   bitnet_mpgemm         accumulation + dequantisation: y[m, n] = beta / s_m * sum_k xq[m, k] * t[n, k]
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is a DEVICE pointer (hipMalloc or equivalent) to contiguous row-major memory
+ *     owned by the caller.  The library never allocates, frees or copies between host and device.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).  All work is enqueued on it;
+ *     no call synchronises.  Results are ready when the stream reaches them.
+ *   - Arguments are validated on the host before anything is enqueued; a non-OK status means nothing was
+ *     enqueued (except BITNET_E_HIP, which reports a failed launch).  No call aborts or throws.
+ *   - Calls are thread-safe.  Two calls that run concurrently must not share a workspace.
+ *   - Naming: M = tokens (activation rows), N = output features (weight rows), K = reduction length.
+ */
+#ifndef BITNET_MI355X_H
+#define BITNET_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BITNET_OK = 0,
+    BITNET_E_INVALID = 1,    /* null pointer, unknown option, or a buffer smaller than required      */
+    BITNET_E_SHAPE = 2,      /* a size outside the supported range (see each call)                   */
+    BITNET_E_ALIGN = 3,      /* a device pointer not aligned to 16 bytes                             */
+    BITNET_E_LAYOUT = 4,     /* unknown weight layout                                                */
+    BITNET_E_WORKSPACE = 5,  /* workspace missing or smaller than the matching *_workspace_bytes     */
+    BITNET_E_HIP = 6         /* the HIP runtime reported an error; see bitnet_last_error()          */
+} bitnet_status;
+
+/*
+ * Weight layouts.  Both need N % 16 == 0 and K % 64 == 0 (rows are tiled by 16, K by 64).
+ *
+ * BITNET_LAYOUT_I2S ("Int2 with a Scale", Table 1, Sec. 3.2.2): 2 bits per weight, code = t + 1.
+ *   16-row groups; K in blocks of up to 256 (four 64-k sub-tiles; only the last block may be shorter).
+ *   In a block of T sub-tiles the group's 64 lanes l = 16*q + r (r = row in group, q = 0..3) own 4*T
+ *   contiguous bytes each; word j of lane (r, q) holds k = 64*(4*s + j) + 16*q + 4*f + b in byte b,
+ *   bits [2f, 2f+1].  Size N*K/4 bytes.
+ *
+ * BITNET_LAYOUT_TL2 (Sec. 3.1, Table 5, Table 6): ~1.67 bits per weight.  K splits into
+ *   ThreeK = floor(K/384)*384 and TwoK = K - ThreeK (block-fitting weight splitting, Sec. 3.1.2).
+ *   Each triple of the ThreeK part becomes a 4-bit index |9 t0 + 3 t1 + t2| and a 1-bit sign [value < 0]
+ *   (Table 6, mirror consolidation Sec. 3.1.1), stored in separate planes (signed-unsigned weight
+ *   splitting, Sec. 3.1.2); each pair of the TwoK part becomes the 4-bit TL1 code 3(t0+1) + (t1+1)
+ *   (Table 5).  Planes in order: index [N*ThreeK/6 B], sign [N*ThreeK/24 B], tail [N*TwoK/4 B].
+ *   In a 384-k block, lane l = 16*q + r owns 16 index bytes (triples 32q..32q+31 of the block, triple i
+ *   in byte i/2, low nibble first) and 4 sign bytes (triple i at bit i%8 of byte i/8).  The tail is cut
+ *   into 64-k units; lane (r, q) owns one 32-bit word per unit holding pairs 32u + 8q + i (byte i/2, low
+ *   nibble first), with each lane's words contiguous.
+ */
+typedef enum {
+    BITNET_LAYOUT_I2S = 0,
+    BITNET_LAYOUT_TL2 = 1
+} bitnet_layout;
+
+/* Bytes of the packed buffer for an N x K weight in `layout`; 0 if the shape or layout is unsupported. */
+size_t bitnet_packed_bytes(int layout, int64_t N, int64_t K);
+
+/* Workspace bytes bitnet_pack_weights needs for an N x K weight (independent of the layout). */
+size_t bitnet_pack_workspace_bytes(int64_t N, int64_t K);
+
+/*
+ * bitnet_pack_weights -- ternarise and pack one weight tensor (Sec. 2.1; Algorithm TL1/TL2 weight
+ * preprocessing; Table 1 for I2_S).
+ *   W          device fp32 [N, K], finite values.
+ *   packed     device buffer of at least bitnet_packed_bytes(layout, N, K) bytes; fully overwritten.
+ *   w_scale    device fp32 [1]; receives beta = the fp32 value nearest (ties to even) to the exact mean
+ *              of |W| over all N*K entries, so it does not depend on any summation order.
+ *   t = clamp(rint(fp32(W / beta)), -1, 1) with IEEE division and ties-to-even; beta == 0 gives t = 0.
+ *   ws         device workspace of bitnet_pack_workspace_bytes(N, K) bytes (any contents).
+ *   Shapes: N % 16 == 0, K % 64 == 0, N*K < 2^32.  Pointers 16-byte aligned.
+ */
+bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t K,
+                                  void* packed, size_t packed_bytes, float* w_scale,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * bitnet_quantize_act -- per-token absmax int8 quantisation (Sec. 2.1, Sec. 3.2.2).
+ *   x        device fp32 [M, K], finite values.
+ *   xq       device int8 [M, K]:  xq = clamp(rint(fp32(x * s_m)), -128, 127)  (ties to even).
+ *   x_scale  device fp32 [M]:     s_m = fp32(127 / max(max_k |x[m, k]|, 1e-5)).
+ *   Shapes: M >= 1, 1 <= K <= 1048576.  Pointers 16-byte aligned.
+ */
+bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
+                                  void* stream);
+
+/* Workspace bytes bitnet_mpgemm needs for this problem (0 is a valid answer). */
+size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K);
+
+/*
+ * bitnet_mpgemm -- ternary x int8 accumulation with the dequantisation epilogue (Eq. 1 / Eq. 3).
+ *   packed, packed_bytes, w_scale   as written by bitnet_pack_weights for an N x K weight in `layout`.
+ *   xq, x_scale                     as written by bitnet_quantize_act for an M x K activation.
+ *   y      device fp32 [M, N]: y[m, n] = fp32(acc[m, n]) * fp32(w_scale / x_scale[m]).
+ *   acc    device int32 [M, N] or NULL: when given, also receives acc[m, n] = sum_k xq[m, k] * t[n, k]
+ *          exactly (the same integers for every tiling and launch shape).
+ *   ws     device workspace of at least bitnet_mpgemm_workspace_bytes(layout, M, N, K) bytes, or NULL
+ *          when that is 0.  It holds split-K partial sums and per-tile completion counters.  It must be
+ *          zero-filled before its first use; every call resets the counters it used to zero when its
+ *          kernels finish, so one workspace serves any number of calls on one stream (not concurrent
+ *          calls on several streams).
+ *   Shapes: M >= 1, N % 16 == 0, K % 64 == 0, K <= 132096 (127 * K < 2^24 keeps acc exact in fp32).
+ *   M <= 16 runs the decode GEMV; larger M runs the prefill GEMM.
+ */
+bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale,
+                            int64_t N, int64_t K, const int8_t* xq, const float* x_scale, int64_t M,
+                            float* y, int32_t* acc, void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* bitnet_status_string(int status);
+
+/* Detail text of the last non-OK status returned on the calling thread ("" if none). */
+const char* bitnet_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BITNET_MI355X_H */

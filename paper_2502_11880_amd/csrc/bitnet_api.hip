@@ -1,0 +1,143 @@
+// C ABI of the library: argument validation, layout arithmetic and dispatch to the HIP kernels.
+// Every check runs on the host before anything is enqueued; no entry point allocates, frees, copies
+// between host and device or synchronises.
+#include "bitnet_mi355x.h"
+#include "bitnet_internal.hpp"
+
+#include <cstdarg>
+#include <cstdio>
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+bitnet_status fail(bitnet_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+bitnet_status ok() {
+    g_last_error[0] = '\0';
+    return BITNET_OK;
+}
+
+bitnet_status hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(BITNET_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+constexpr int64_t kMaxK = 132096;   // 127 * K < 2^24: accumulators stay exact in fp32
+
+bool weight_shape_ok(int64_t N, int64_t K) {
+    return N > 0 && K > 0 && N % bitnet::kRowsPerGroup == 0 && K % bitnet::kSubK == 0 && K <= kMaxK &&
+           N <= (int64_t)1 << 30;
+}
+
+bool layout_ok(int layout) { return layout == BITNET_LAYOUT_I2S || layout == BITNET_LAYOUT_TL2; }
+
+size_t packed_bytes_of(int layout, int64_t N, int64_t K) {
+    if (layout == BITNET_LAYOUT_I2S) return (size_t)N * (size_t)K / 4;
+    const int64_t three = (K / bitnet::kTl2BlockK) * bitnet::kTl2BlockK;
+    const int64_t two = K - three;
+    return (size_t)N * three / 6 + (size_t)N * three / 24 + (size_t)N * two / 4;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t bitnet_packed_bytes(int layout, int64_t N, int64_t K) {
+    if (!layout_ok(layout) || !weight_shape_ok(N, K)) return 0;
+    return packed_bytes_of(layout, N, K);
+}
+
+size_t bitnet_pack_workspace_bytes(int64_t N, int64_t K) {
+    (void)N;
+    (void)K;
+    return bitnet::pack_workspace_bytes();
+}
+
+bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t K, void* packed,
+                                  size_t packed_bytes, float* w_scale, void* ws, size_t ws_bytes, void* stream) {
+    if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
+    if (!W || !packed || !w_scale) return fail(BITNET_E_INVALID, "null pointer argument");
+    if (!weight_shape_ok(N, K)) return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
+                                            (long long)kMaxK, (long long)N, (long long)K);
+    if ((uint64_t)N * (uint64_t)K >= ((uint64_t)1 << 32)) return fail(BITNET_E_SHAPE, "N*K must be below 2^32");
+    if (!aligned(W, 16) || !aligned(packed, 16) || !aligned(ws, 16) || !aligned(w_scale, 4))
+        return fail(BITNET_E_ALIGN, "W, packed and ws need 16-byte alignment, w_scale 4-byte");
+    if (packed_bytes < packed_bytes_of(layout, N, K))
+        return fail(BITNET_E_INVALID, "packed buffer holds %zu bytes, %zu needed", packed_bytes,
+                    packed_bytes_of(layout, N, K));
+    if (!ws || ws_bytes < bitnet::pack_workspace_bytes())
+        return fail(BITNET_E_WORKSPACE, "pack workspace needs %zu bytes", bitnet::pack_workspace_bytes());
+    return hip_status(bitnet::launch_pack(layout, W, N, K, packed, w_scale, ws, (hipStream_t)stream),
+                      "bitnet_pack_weights launch");
+}
+
+bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale, void* stream) {
+    if (!x || !xq || !x_scale) return fail(BITNET_E_INVALID, "null pointer argument");
+    if (M < 1 || M > ((int64_t)1 << 31) - 1 || K < 1 || K > ((int64_t)1 << 20))
+        return fail(BITNET_E_SHAPE, "need M >= 1 and 1 <= K <= 1048576; got M=%lld K=%lld", (long long)M,
+                    (long long)K);
+    if (!aligned(x, 16) || !aligned(xq, 16) || !aligned(x_scale, 4))
+        return fail(BITNET_E_ALIGN, "x and xq need 16-byte alignment, x_scale 4-byte");
+    return hip_status(bitnet::launch_quantize_act(x, M, K, xq, x_scale, (hipStream_t)stream),
+                      "bitnet_quantize_act launch");
+}
+
+size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K) {
+    if (!layout_ok(layout) || !weight_shape_ok(N, K) || M < 1) return 0;
+    if (layout == BITNET_LAYOUT_I2S) return bitnet::i2s_decode_workspace_bytes(M, N, K);
+    return 0;
+}
+
+bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale, int64_t N,
+                            int64_t K, const int8_t* xq, const float* x_scale, int64_t M, float* y, int32_t* acc,
+                            void* ws, size_t ws_bytes, void* stream) {
+    if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
+    if (!packed || !w_scale || !xq || !x_scale || !y) return fail(BITNET_E_INVALID, "null pointer argument");
+    if (!weight_shape_ok(N, K)) return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
+                                            (long long)kMaxK, (long long)N, (long long)K);
+    if (M < 1 || M > ((int64_t)1 << 24)) return fail(BITNET_E_SHAPE, "need 1 <= M <= 2^24; got M=%lld", (long long)M);
+    if (!aligned(packed, 16) || !aligned(xq, 16) || !aligned(y, 16) || (acc && !aligned(acc, 16)) ||
+        !aligned(ws, 16) || !aligned(w_scale, 4) || !aligned(x_scale, 4))
+        return fail(BITNET_E_ALIGN, "packed, xq, y, acc and ws need 16-byte alignment, scales 4-byte");
+    if (packed_bytes < packed_bytes_of(layout, N, K))
+        return fail(BITNET_E_INVALID, "packed buffer holds %zu bytes, %zu needed", packed_bytes,
+                    packed_bytes_of(layout, N, K));
+    const size_t need = bitnet_mpgemm_workspace_bytes(layout, M, N, K);
+    if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
+    if (layout != BITNET_LAYOUT_I2S) return fail(BITNET_E_LAYOUT, "TL2 accumulation is not available in this build");
+
+    hipStream_t s = (hipStream_t)stream;
+    for (int64_t m0 = 0; m0 < M; m0 += 16) {
+        const int mc = (int)((M - m0) < 16 ? (M - m0) : 16);
+        hipError_t e = bitnet::launch_i2s_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
+                                                 y + m0 * N, acc ? acc + m0 * N : nullptr, ws, s);
+        if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
+    }
+    return ok();
+}
+
+const char* bitnet_status_string(int status) {
+    switch (status) {
+        case BITNET_OK: return "ok";
+        case BITNET_E_INVALID: return "invalid argument";
+        case BITNET_E_SHAPE: return "unsupported shape";
+        case BITNET_E_ALIGN: return "misaligned pointer";
+        case BITNET_E_LAYOUT: return "unknown or unavailable layout";
+        case BITNET_E_WORKSPACE: return "workspace missing or too small";
+        case BITNET_E_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+const char* bitnet_last_error(void) { return g_last_error; }
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+"""Host-side checks of the C ABI: every declared symbol is exported, size queries agree with the layout
+definitions, and argument validation returns the documented status before anything touches a GPU."""
+import os
+import re
+
+import pytest
+
+import paper_2502_11880_amd as B
+from oracle import bitnet_oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = []
+    for fn in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names += re.findall(r"\b(bitnet_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    names = _declared_functions()
+    assert len(names) >= 8
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(n for n, _, _ in B._SIGNATURES) == names
+
+
+@pytest.mark.parametrize("N,K", [(16, 64), (32, 448), (4096, 4096), (3200, 8640), (12288, 33024)])
+def test_packed_bytes_match_layout_definitions(N, K):
+    assert B.bitnet_packed_bytes("i2s", N, K) == O.i2s_packed_bytes(N, K)
+    assert B.bitnet_packed_bytes("tl2", N, K) == O.tl2_packed_bytes(N, K)
+
+
+def test_packed_bytes_rejects_bad_shapes():
+    for layout in ("i2s", "tl2"):
+        assert B.bitnet_packed_bytes(layout, 15, 64) == 0
+        assert B.bitnet_packed_bytes(layout, 16, 65) == 0
+        assert B.bitnet_packed_bytes(layout, 0, 64) == 0
+    assert B.bitnet_packed_bytes(7, 16, 64) == 0
+
+
+FAKE = 1 << 20          # aligned, never dereferenced: validation fails before any launch
+
+
+def _mpgemm(**kw):
+    a = dict(layout=0, packed=FAKE, packed_bytes=1 << 30, w_scale=FAKE, N=64, K=256, xq=FAKE, x_scale=FAKE, M=1,
+             y=FAKE, acc=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return B.lib().bitnet_mpgemm(a["layout"], a["packed"], a["packed_bytes"], a["w_scale"], a["N"], a["K"], a["xq"],
+                                 a["x_scale"], a["M"], a["y"], a["acc"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+def test_mpgemm_validation_statuses():
+    assert _mpgemm(layout=5) == 4
+    assert _mpgemm(packed=None) == 1
+    assert _mpgemm(y=None) == 1
+    assert _mpgemm(N=40) == 2
+    assert _mpgemm(K=100) == 2
+    assert _mpgemm(K=132096 + 64) == 2
+    assert _mpgemm(M=0) == 2
+    assert _mpgemm(xq=FAKE + 4) == 3
+    assert _mpgemm(acc=FAKE + 8) == 3
+    assert _mpgemm(packed_bytes=10) == 1
+    need = B.bitnet_mpgemm_workspace_bytes("i2s", 1, 64, 256 * 64)
+    assert need > 0
+    assert _mpgemm(K=256 * 64, ws=None, ws_bytes=0) == 5
+    assert _mpgemm(K=256 * 64, ws_bytes=need - 1) == 5
+    assert "workspace" in B.bitnet_last_error()
+
+
+def test_quantize_and_pack_validation_statuses():
+    lib = B.lib()
+    assert lib.bitnet_quantize_act(None, 1, 64, FAKE, FAKE, None) == 1
+    assert lib.bitnet_quantize_act(FAKE, 0, 64, FAKE, FAKE, None) == 2
+    assert lib.bitnet_quantize_act(FAKE, 1, 0, FAKE, FAKE, None) == 2
+    assert lib.bitnet_quantize_act(FAKE + 4, 1, 64, FAKE, FAKE, None) == 3
+    ws = B.bitnet_pack_workspace_bytes(64, 64)
+    assert lib.bitnet_pack_weights(3, FAKE, 64, 64, FAKE, 1 << 20, FAKE, FAKE, ws, None) == 4
+    assert lib.bitnet_pack_weights(0, FAKE, 60, 64, FAKE, 1 << 20, FAKE, FAKE, ws, None) == 2
+    assert lib.bitnet_pack_weights(0, FAKE, 64, 64, FAKE, 100, FAKE, FAKE, ws, None) == 1
+    assert lib.bitnet_pack_weights(0, FAKE, 64, 64, FAKE, 1 << 20, FAKE, FAKE, ws - 8, None) == 5
+    assert lib.bitnet_pack_weights(0, FAKE, 64, 64, FAKE + 2, 1 << 20, FAKE, FAKE, ws, None) == 3
+
+
+def test_status_strings():
+    for st in range(7):
+        assert B.bitnet_status_string(st)
+    assert B.bitnet_status_string(99) == "unknown status"
