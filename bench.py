@@ -7,8 +7,8 @@ timing (offline preprocessing); the packed copies rotate so that every step stre
 HBM rather than from the 256 MB Infinity Cache.
 
 Prints one JSON line.  `value` is the packed-weight bandwidth of the step (GB/s); `roofline` describes
-the dominant kernel (the mpGEMM) from HIP events around each of its launches; `cpu_baseline` times the
-CPU oracle on a bounded sample of the same workload.
+the dominant kernel (the mpGEMM) from HIP events around a graph of its launches back to back;
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -85,46 +85,59 @@ def main():
     ys = {n: torch.empty((M, by_name[n][1]), dtype=torch.float32, device=dev) for n in by_name}
     wss = {n: torch.zeros(max(16, B.bitnet_mpgemm_workspace_bytes(layout, M, by_name[n][1], by_name[n][0])),
                           dtype=torch.uint8, device=dev) for n in by_name}
-    stream = torch.cuda.current_stream()
+    stream = torch.cuda.Stream()
     sptr = stream.cuda_stream
 
-    def step(i, events=None):
+    def step(i, quantize=True):
         pk = rot[i % copies]
         for gi, g in enumerate(groups):
-            B.bitnet_quantize_act(xs[gi], xqs[gi], sxs[gi], sptr)
+            if quantize:
+                B.bitnet_quantize_act(xs[gi], xqs[gi], sxs[gi], sptr)
             for n in g:
                 K, N = by_name[n]
-                if events is not None:
-                    events.append((n, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)))
-                    events[-1][1].record(stream)
                 B.bitnet_mpgemm(layout, pk[n], scales[n], N, K, xqs[gi], sxs[gi], ys[n], None, wss[n], sptr)
-                if events is not None:
-                    events[-1][2].record(stream)
 
-    for i in range(args.warmup):
-        step(i)
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            step(i)
     torch.cuda.synchronize()
 
-    # ---- timed region: K steps, HIP events around every mpGEMM launch ----
-    events = []
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    # The K timed steps are captured once as a HIP graph and replayed, so the GPU runs them back to back
+    # (host-side launch overhead would otherwise dominate kernels this short).  A second graph holds only
+    # the mpGEMM launches of the same K steps, back to back: its time per launch is the dominant kernel's
+    # launch duration (including the short gap between graph nodes).
+    g_steps = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_steps, stream=stream):
+        for i in range(args.steps):
+            step(args.warmup + i)
+    g_gemm = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_gemm, stream=stream):
+        for i in range(args.steps):
+            step(args.warmup + i, quantize=False)
+    with torch.cuda.stream(stream):
+        g_steps.replay()
+        g_gemm.replay()
     torch.cuda.synchronize()
+
+    # ---- timed region: one replay of the K-step graph, then one of the mpGEMM-only graph ----
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     w0 = time.perf_counter()
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(args.warmup + i, events)
-    t_end.record(stream)
+    with torch.cuda.stream(stream):
+        ev[0].record(stream)
+        g_steps.replay()
+        ev[1].record(stream)
+        g_gemm.replay()
+        ev[2].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    gpu_ms = t_start.elapsed_time(t_end)
+    gpu_ms = ev[0].elapsed_time(ev[1])
     ms_per_step = gpu_ms / args.steps
+    gemm_total_ms = ev[1].elapsed_time(ev[2])
+    launches = args.steps * len(linears)
 
-    gemm_ms = [s.elapsed_time(e) for _, s, e in events]
     per_launch_bytes = {n: packed[n].numel() + M * by_name[n][0] + 4 * M * by_name[n][1] for n in by_name}
-    total_bytes = sum(per_launch_bytes[n] for n, _, _ in events)
-    avg_launch_ms = sum(gemm_ms) / len(gemm_ms)
-    avg_bytes = total_bytes / len(events)
+    avg_bytes = sum(per_launch_bytes.values()) / len(per_launch_bytes)
+    avg_launch_ms = gemm_total_ms / launches
     achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
 
     value = step_weight_bytes / (ms_per_step * 1e-3) / 1e9
@@ -160,7 +173,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "bitnet_mpgemm (decode GEMV)", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": None, "avg_launch_us": round(avg_launch_ms * 1e3, 3),
-                     "avg_algorithmic_bytes": int(avg_bytes), "launches": len(events)},
+                     "avg_algorithmic_bytes": int(avg_bytes), "launches": launches},
         "cpu_baseline": cpu,
         "parity": parity,
     }

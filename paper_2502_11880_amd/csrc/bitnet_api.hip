@@ -93,7 +93,6 @@ bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* 
 
 size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K) {
     if (!layout_ok(layout) || !weight_shape_ok(N, K) || M < 1) return 0;
-    if (layout == BITNET_LAYOUT_I2S) return bitnet::i2s_decode_workspace_bytes(M, N, K);
     return 0;
 }
 
@@ -119,7 +118,7 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
     for (int64_t m0 = 0; m0 < M; m0 += 16) {
         const int mc = (int)((M - m0) < 16 ? (M - m0) : 16);
         hipError_t e = bitnet::launch_i2s_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
-                                                 y + m0 * N, acc ? acc + m0 * N : nullptr, ws, s);
+                                                 y + m0 * N, acc ? acc + m0 * N : nullptr, s);
         if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
     }
     return ok();

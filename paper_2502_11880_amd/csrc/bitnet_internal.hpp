@@ -44,16 +44,9 @@ size_t pack_workspace_bytes();
 hipError_t launch_pack(int layout, const float* W, int64_t N, int64_t K, void* packed, float* w_scale,
                        void* ws, hipStream_t stream);
 
-struct DecodePlan {
-    int nt;            // row groups per work group
-    int tiles;         // N / (16 * nt)
-    int splits;        // work groups along K per tile
-    int kb_per_split;  // 256-k blocks per split
-};
-DecodePlan plan_i2s_decode(int64_t N, int64_t K);
-size_t i2s_decode_workspace_bytes(int64_t M, int64_t N, int64_t K);
+int i2s_decode_waves(int64_t K);
 hipError_t launch_i2s_decode(const void* packed, const float* w_scale, const int8_t* xq,
                              const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
-                             void* ws, hipStream_t stream);
+                             hipStream_t stream);
 
 }  // namespace bitnet

@@ -9,19 +9,23 @@
 // The codes carry a +1 offset; a second MFMA against an all-ones B gives sum_k xq[m, k] over the same
 // k, which is subtracted (exact integers).
 //
-// Work split: a work group (4 waves) owns NT row groups (16*NT rows) and a range of 256-k blocks;
-// waves take every 4th block.  Waves reduce through LDS; when K is split over several work groups the
-// partial int32 sums go to the workspace and the last group to finish (an atomic ticket per tile) adds
-// them in split order and applies the epilogue.  Ticket counters are reset to zero by that group.
+// Work split: one work group per 16-row group, holding the whole K.  Its 4, 8 or 16 waves take every
+// WAVES-th 256-k block, issue all their weight loads up front (a GEMV of a few MB is latency-bound: one
+// DRAM round trip should cover it) and reduce through LDS; wave 0 applies the epilogue.  No work group
+// depends on another, so no device-wide fence is needed (an agent-scope release writes back the whole
+// L2 of the XCD, which costs more than these GEMVs).
 #include "bitnet_internal.hpp"
 
-#include <algorithm>
+// Tuning constants: 256-k blocks loaded per wave per batch, and the widest work group (in waves).
+#ifndef BITNET_DECODE_U
+#define BITNET_DECODE_U 2
+#endif
+#ifndef BITNET_DECODE_MAX_WAVES
+#define BITNET_DECODE_MAX_WAVES 16
+#endif
 
 namespace bitnet {
 namespace {
-
-constexpr int kWaves = 4;
-constexpr int kBlock = 64 * kWaves;
 
 __device__ __forceinline__ v4i unpack_codes(uint32_t w) {
     v4i b;
@@ -40,44 +44,36 @@ __device__ __forceinline__ v4u load_stream16(const uint8_t* p) {
     return __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p));
 }
 
-template <int NT, int U>
-__global__ __launch_bounds__(kBlock) void i2s_decode_kernel(
+__device__ __forceinline__ uint32_t word_of(const v4u& v, int j) {
+    return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+}
+
+template <int WAVES, int U>
+__global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(
     const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
-    const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out,
-    int32_t* __restrict__ partial, unsigned* __restrict__ tickets, int splits, int kb_per_split) {
-    __shared__ v4i red[kWaves][NT][64];
+    const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out) {
+    __shared__ v4i red[WAVES][64];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int L = xcd_logical_id(blockIdx.x, gridDim.x);
-    const int tile = L / splits, sp = L - tile * splits;
+    const int rg = xcd_logical_id(blockIdx.x, gridDim.x);
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int nfull = K / kI2sBlockK;
-    const int kb0 = sp * kb_per_split;
-    const int kb1 = min(kb0 + kb_per_split, nkb);
     const int q = lane >> 4, r = lane & 15;
     const bool a_on = r < M;                        // A operand: row = token r, 16 k per lane group q
     const int8_t* arow = xq + (size_t)(a_on ? r : 0) * K + 16 * q;
-    const size_t rg_bytes = (size_t)4 * K;
-    const uint8_t* wbase = packed + (size_t)tile * NT * rg_bytes;
+    const uint8_t* wbase = packed + (size_t)rg * 4 * K;
     const v4i ones = {0x01010101, 0x01010101, 0x01010101, 0x01010101};
     const v4i zero = {0, 0, 0, 0};
 
-    v4i acc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = zero;
-    v4i rowsum = zero;
-
-    const int full_end = min(kb1, nfull);
-    for (int kb = kb0 + wave; kb < full_end; kb += kWaves * U) {
-        v4u wv[U][NT];
+    v4i acc = zero, rowsum = zero;
+    for (int kb = wave; kb < nfull; kb += WAVES * U) {
+        v4u wv[U];
         v4i av[U][4];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int kbu = kb + kWaves * u;
-            if (kbu < full_end) {
-#pragma unroll
-                for (int t = 0; t < NT; ++t)
-                    wv[u][t] = load_stream16(wbase + t * rg_bytes + (size_t)kbu * 1024 + 16 * lane);
+            const int kbu = kb + WAVES * u;
+            if (kbu < nfull) {
+                wv[u] = load_stream16(wbase + (size_t)kbu * 1024 + 16 * lane);
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
                     av[u][j] = a_on ? *reinterpret_cast<const v4i*>(arow + kbu * kI2sBlockK + kSubK * j) : zero;
@@ -85,139 +81,74 @@ __global__ __launch_bounds__(kBlock) void i2s_decode_kernel(
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (kb + kWaves * u < full_end) {
+            if (kb + WAVES * u < nfull) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-                        const uint32_t w = j == 0 ? wv[u][t].x : j == 1 ? wv[u][t].y : j == 2 ? wv[u][t].z : wv[u][t].w;
-                        acc[t] = mfma16x16x64(av[u][j], unpack_codes(w), acc[t]);
-                    }
+                    acc = mfma16x16x64(av[u][j], unpack_codes(word_of(wv[u], j)), acc);
                     rowsum = mfma16x16x64(av[u][j], ones, rowsum);
                 }
             }
         }
     }
     // A short last block (K % 256 != 0): T sub-tiles, lane words 4*T bytes apart.
-    if (nfull < nkb && nkb - 1 >= kb0 && nkb - 1 < kb1 && ((nkb - 1 - kb0) % kWaves) == wave) {
-        const int kbu = nkb - 1;
+    if (nfull < nkb && (nfull % WAVES) == wave) {
         const int T = (K - nfull * kI2sBlockK) / kSubK;
         for (int j = 0; j < T; ++j) {
-            const v4i a = a_on ? *reinterpret_cast<const v4i*>(arow + kbu * kI2sBlockK + kSubK * j) : zero;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const uint32_t w = *reinterpret_cast<const uint32_t*>(wbase + t * rg_bytes + (size_t)kbu * 1024 +
-                                                                      4 * T * lane + 4 * j);
-                acc[t] = mfma16x16x64(a, unpack_codes(w), acc[t]);
-            }
+            const v4i a = a_on ? *reinterpret_cast<const v4i*>(arow + nfull * kI2sBlockK + kSubK * j) : zero;
+            const uint32_t w = *reinterpret_cast<const uint32_t*>(wbase + (size_t)nfull * 1024 + 4 * T * lane + 4 * j);
+            acc = mfma16x16x64(a, unpack_codes(w), acc);
             rowsum = mfma16x16x64(a, ones, rowsum);
         }
     }
 
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        acc[t] -= rowsum;
-        red[wave][t][lane] = acc[t];
-    }
+    red[wave][lane] = acc - rowsum;
     __syncthreads();
     if (wave != 0) return;
+    acc = red[0][lane];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = red[0][t][lane] + red[1][t][lane] + red[2][t][lane] + red[3][t][lane];
+    for (int w = 1; w < WAVES; ++w) acc += red[w][lane];
 
     // Output element v of lane l is D[row 4*(l/16) + v][col l%16]: token m = 4q + v, weight row r.
-    if (splits > 1) {
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int n = (tile * NT + t) * kRowsPerGroup + r;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int m = 4 * q + v;
-                if (m < M)
-                    __hip_atomic_store(partial + ((size_t)sp * M + m) * N + n, acc[t][v], __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-        __threadfence();
-        unsigned prev = 0u;
-        if (lane == 0) prev = atomicAdd(tickets + tile, 1u);
-        prev = __shfl(prev, 0, 64);
-        if (prev != (unsigned)(splits - 1)) return;
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int n = (tile * NT + t) * kRowsPerGroup + r;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int m = 4 * q + v;
-                int s = 0;
-                if (m < M)
-                    for (int p = 0; p < splits; ++p)
-                        s += __hip_atomic_load(partial + ((size_t)p * M + m) * N + n, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-                acc[t][v] = s;
-            }
-        }
-        if (lane == 0) tickets[tile] = 0u;
-    }
-
     const float beta = *w_scale;
+    const int n = rg * kRowsPerGroup + r;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        const int n = (tile * NT + t) * kRowsPerGroup + r;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int m = 4 * q + v;
-            if (m < M) {
-                const float sc = beta / x_scale[m];
-                y[(size_t)m * N + n] = (float)acc[t][v] * sc;
-                if (acc_out) acc_out[(size_t)m * N + n] = acc[t][v];
-            }
+    for (int v = 0; v < 4; ++v) {
+        const int m = 4 * q + v;
+        if (m < M) {
+            const float sc = beta / x_scale[m];
+            y[(size_t)m * N + n] = (float)acc[v] * sc;
+            if (acc_out) acc_out[(size_t)m * N + n] = acc[v];
         }
     }
-}
-
-template <int NT>
-hipError_t launch_nt(const DecodePlan& p, const void* packed, const float* w_scale, const int8_t* xq,
-                     const float* x_scale, int M, int N, int K, float* y, int32_t* acc, void* ws,
-                     hipStream_t stream) {
-    int32_t* partial = static_cast<int32_t*>(ws);
-    unsigned* tickets = reinterpret_cast<unsigned*>(static_cast<uint8_t*>(ws) +
-                                                    (size_t)p.splits * 16 * N * sizeof(int32_t));
-    const unsigned grid = (unsigned)(p.tiles * p.splits);
-    hipLaunchKernelGGL((i2s_decode_kernel<NT, 2>), dim3(grid), dim3(kBlock), 0, stream,
-                       static_cast<const uint8_t*>(packed), w_scale, xq, x_scale, M, N, K, y, acc, partial, tickets,
-                       p.splits, p.kb_per_split);
-    return hipGetLastError();
 }
 
 }  // namespace
 
-DecodePlan plan_i2s_decode(int64_t N, int64_t K) {
-    DecodePlan p;
-    const int nrg = (int)(N / kRowsPerGroup);
-    p.nt = (nrg % 2 == 0) ? 2 : 1;
-    p.tiles = nrg / p.nt;
+int i2s_decode_waves(int64_t K) {
     const int nkb = (int)((K + kI2sBlockK - 1) / kI2sBlockK);
-    const int target_groups = 1024;                       // 4 work groups (16 waves) per CU
-    int splits = (target_groups + p.tiles - 1) / p.tiles;
-    splits = std::max(1, std::min(splits, std::max(1, nkb / kWaves)));
-    p.kb_per_split = (nkb + splits - 1) / splits;
-    p.splits = (nkb + p.kb_per_split - 1) / p.kb_per_split;
-    return p;
-}
-
-size_t i2s_decode_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    (void)M;
-    const DecodePlan p = plan_i2s_decode(N, K);
-    if (p.splits <= 1) return 0;
-    return (size_t)p.splits * 16 * (size_t)N * sizeof(int32_t) + (size_t)p.tiles * sizeof(unsigned);
+    const int w = nkb <= 4 ? 4 : nkb <= 8 ? 8 : 16;
+    return w < BITNET_DECODE_MAX_WAVES ? w : BITNET_DECODE_MAX_WAVES;
 }
 
 hipError_t launch_i2s_decode(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                             int M, int N, int K, float* y, int32_t* acc, void* ws, hipStream_t stream) {
-    const DecodePlan p = plan_i2s_decode(N, K);
-    if (p.nt == 2) return launch_nt<2>(p, packed, w_scale, xq, x_scale, M, N, K, y, acc, ws, stream);
-    return launch_nt<1>(p, packed, w_scale, xq, x_scale, M, N, K, y, acc, ws, stream);
+                             int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    const unsigned grid = (unsigned)(N / kRowsPerGroup);
+    const uint8_t* pk = static_cast<const uint8_t*>(packed);
+    switch (i2s_decode_waves(K)) {
+        case 4:
+            hipLaunchKernelGGL((i2s_decode_kernel<4, BITNET_DECODE_U>), dim3(grid), dim3(256), 0, stream, pk, w_scale, xq, x_scale,
+                               M, N, K, y, acc);
+            break;
+        case 8:
+            hipLaunchKernelGGL((i2s_decode_kernel<8, BITNET_DECODE_U>), dim3(grid), dim3(512), 0, stream, pk, w_scale, xq, x_scale,
+                               M, N, K, y, acc);
+            break;
+        default:
+            hipLaunchKernelGGL((i2s_decode_kernel<16, BITNET_DECODE_U>), dim3(grid), dim3(1024), 0, stream, pk, w_scale, xq,
+                               x_scale, M, N, K, y, acc);
+            break;
+    }
+    return hipGetLastError();
 }
 
 }  // namespace bitnet

@@ -5,8 +5,9 @@
 //   s_m     = 127 / gamma_m                       (IEEE fp32 divide, round to nearest even)
 //   xq      = clamp(rint(x * s_m), -128, 127)     (fp32 multiply, ties to even)
 //
-// One work group per token row: a first pass finds the absmax, a second pass (an L2 hit) writes the
-// codes.  HBM-bound: 4 bytes read and 1 byte written per element.
+// One work group per token row.  The row is read once into registers (up to 16 float4 per lane), reduced
+// to its absmax, then quantised from registers; rows too long for that take a second pass over memory.
+// HBM-bound: 4 bytes read and 1 byte written per element.
 #include "bitnet_internal.hpp"
 
 namespace bitnet {
@@ -33,45 +34,68 @@ __device__ __forceinline__ int quant_one(float v, float s) {
     return (int)r;
 }
 
+template <int BLOCK, int VPT>
+__global__ __launch_bounds__(BLOCK) void quantize_rows_reg(const float* __restrict__ x, int K,
+                                                           int8_t* __restrict__ xq, float* __restrict__ x_scale) {
+    __shared__ float red[BLOCK / 64];
+    const size_t m = blockIdx.x;
+    const float4* x4 = reinterpret_cast<const float4*>(x + m * (size_t)K);
+    uint32_t* q4 = reinterpret_cast<uint32_t*>(xq + m * (size_t)K);
+    const int K4 = K >> 2;
+    float4 v[VPT];
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int idx = threadIdx.x + i * BLOCK;
+        v[i] = idx < K4 ? x4[idx] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[i].x), fabsf(v[i].y)), fmaxf(fabsf(v[i].z), fabsf(v[i].w))));
+    }
+    amax = block_max<BLOCK>(amax, red);
+    const float s = 127.0f / fmaxf(amax, 1e-5f);
+    if (threadIdx.x == 0) x_scale[m] = s;
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int idx = threadIdx.x + i * BLOCK;
+        if (idx < K4)
+            q4[idx] = (uint32_t)(quant_one(v[i].x, s) & 0xFF) | ((uint32_t)(quant_one(v[i].y, s) & 0xFF) << 8) |
+                      ((uint32_t)(quant_one(v[i].z, s) & 0xFF) << 16) | ((uint32_t)(quant_one(v[i].w, s) & 0xFF) << 24);
+    }
+}
+
+// Any K: two passes over the row.
 template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void quantize_rows(const float* __restrict__ x, int K,
-                                                       int8_t* __restrict__ xq, float* __restrict__ x_scale) {
+__global__ __launch_bounds__(BLOCK) void quantize_rows_2pass(const float* __restrict__ x, int K,
+                                                             int8_t* __restrict__ xq, float* __restrict__ x_scale) {
     __shared__ float red[BLOCK / 64];
     const size_t m = blockIdx.x;
     const float* xr = x + m * (size_t)K;
     int8_t* qr = xq + m * (size_t)K;
-    const bool vec = (K & 3) == 0;
-    const int K4 = vec ? K >> 2 : 0;
-
     float amax = 0.0f;
-    if (vec) {
-        const float4* x4 = reinterpret_cast<const float4*>(xr);
-        for (int i = threadIdx.x; i < K4; i += BLOCK) {
-            const float4 v = x4[i];
-            amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
-        }
-    } else {
-        for (int i = threadIdx.x; i < K; i += BLOCK) amax = fmaxf(amax, fabsf(xr[i]));
-    }
+    for (int i = threadIdx.x; i < K; i += BLOCK) amax = fmaxf(amax, fabsf(xr[i]));
     amax = block_max<BLOCK>(amax, red);
-    const float gamma = fmaxf(amax, 1e-5f);
-    const float s = 127.0f / gamma;
+    const float s = 127.0f / fmaxf(amax, 1e-5f);
     if (threadIdx.x == 0) x_scale[m] = s;
+    for (int i = threadIdx.x; i < K; i += BLOCK) qr[i] = (int8_t)quant_one(xr[i], s);
+}
 
-    if (vec) {
-        const float4* x4 = reinterpret_cast<const float4*>(xr);
-        uint32_t* q4 = reinterpret_cast<uint32_t*>(qr);
-        for (int i = threadIdx.x; i < K4; i += BLOCK) {
-            const float4 v = x4[i];
-            const uint32_t w = (uint32_t)(quant_one(v.x, s) & 0xFF) |
-                               ((uint32_t)(quant_one(v.y, s) & 0xFF) << 8) |
-                               ((uint32_t)(quant_one(v.z, s) & 0xFF) << 16) |
-                               ((uint32_t)(quant_one(v.w, s) & 0xFF) << 24);
-            q4[i] = w;
-        }
+template <int BLOCK>
+hipError_t launch_block(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale, hipStream_t stream) {
+    const dim3 grid((unsigned)M), block(BLOCK);
+    const int64_t K4 = K / 4;
+    if (K % 4 != 0 || K4 > 16 * BLOCK) {
+        hipLaunchKernelGGL(quantize_rows_2pass<BLOCK>, grid, block, 0, stream, x, (int)K, xq, x_scale);
+    } else if (K4 <= BLOCK) {
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 1>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+    } else if (K4 <= 2 * BLOCK) {
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 2>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+    } else if (K4 <= 4 * BLOCK) {
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 4>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+    } else if (K4 <= 8 * BLOCK) {
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 8>), grid, block, 0, stream, x, (int)K, xq, x_scale);
     } else {
-        for (int i = threadIdx.x; i < K; i += BLOCK) qr[i] = (int8_t)quant_one(xr[i], s);
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 16>), grid, block, 0, stream, x, (int)K, xq, x_scale);
     }
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -79,14 +103,8 @@ __global__ __launch_bounds__(BLOCK) void quantize_rows(const float* __restrict__
 hipError_t launch_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
                                hipStream_t stream) {
     // Few rows: wide groups so one row is spread over many lanes.  Many rows: one 256-lane group each.
-    if (M <= 64) {
-        hipLaunchKernelGGL(quantize_rows<1024>, dim3((unsigned)M), dim3(1024), 0, stream, x, (int)K, xq,
-                           x_scale);
-    } else {
-        hipLaunchKernelGGL(quantize_rows<256>, dim3((unsigned)M), dim3(256), 0, stream, x, (int)K, xq,
-                           x_scale);
-    }
-    return hipGetLastError();
+    if (M <= 64) return launch_block<1024>(x, M, K, xq, x_scale, stream);
+    return launch_block<256>(x, M, K, xq, x_scale, stream);
 }
 
 }  // namespace bitnet

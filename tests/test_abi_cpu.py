@@ -66,11 +66,12 @@ def test_mpgemm_validation_statuses():
     assert _mpgemm(xq=FAKE + 4) == 3
     assert _mpgemm(acc=FAKE + 8) == 3
     assert _mpgemm(packed_bytes=10) == 1
-    need = B.bitnet_mpgemm_workspace_bytes("i2s", 1, 64, 256 * 64)
-    assert need > 0
-    assert _mpgemm(K=256 * 64, ws=None, ws_bytes=0) == 5
-    assert _mpgemm(K=256 * 64, ws_bytes=need - 1) == 5
-    assert "workspace" in B.bitnet_last_error()
+    for layout, M, N, K in ((0, 1, 64, 256 * 64), (1, 1, 64, 4096), (0, 512, 4096, 4096), (1, 512, 4096, 4096)):
+        need = B.bitnet_mpgemm_workspace_bytes(layout, M, N, K)
+        if need:
+            assert _mpgemm(layout=layout, M=M, N=N, K=K, ws=None, ws_bytes=0) == 5
+            assert _mpgemm(layout=layout, M=M, N=N, K=K, ws_bytes=need - 1) == 5
+            assert "workspace" in B.bitnet_last_error()
 
 
 def test_quantize_and_pack_validation_statuses():
