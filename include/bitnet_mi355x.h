@@ -117,6 +117,21 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
                             int64_t N, int64_t K, const int8_t* xq, const float* x_scale, int64_t M,
                             float* y, int32_t* acc, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * bitnet_elut_tables -- the activation tables of the TL2 path, written out (Eq. 3; mirror consolidation,
+ * Sec. 3.1.1; the Table-setup step of Algorithm "ELUT mpGEMM" and PreCompute of Algorithms TL1/TL2).
+ * bitnet_mpgemm builds the same tables in LDS for the TL2 layout; this call exposes them.
+ *   xq    device int8 [M, K] (from bitnet_quantize_act).
+ *   lut   device int16 [M, ThreeK/3, 16]: for triple g (k = 3g..3g+2) entry i < 14 is
+ *         d0(i)*xq[3g] + d1(i)*xq[3g+1] + d2(i)*xq[3g+2] where i = 9*d0 + 3*d1 + d2 with digits in {-1,0,1}
+ *         and a non-negative leading digit; entries 14 and 15 are 0.
+ *   lut1  device int16 [M, TwoK/2, 16]: for tail pair p (k = ThreeK + 2p, +1) entry i < 9 is
+ *         (i/3 - 1)*xq[k] + (i%3 - 1)*xq[k+1] (Table 5 order); entries 9..15 are 0.  May be NULL when TwoK == 0.
+ *   Shapes: K % 64 == 0, 384 <= K <= 132096, ThreeK = floor(K/384)*384, TwoK = K - ThreeK.
+ */
+bitnet_status bitnet_elut_tables(const int8_t* xq, int64_t M, int64_t K, int16_t* lut, int16_t* lut1,
+                                 void* stream);
+
 /* Static description of a status code. */
 const char* bitnet_status_string(int status);
 

@@ -36,6 +36,8 @@ _SIGNATURES = [
      [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
       ctypes.c_size_t, ctypes.c_void_p]),
+    ("bitnet_elut_tables", ctypes.c_int,
+     [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     ("bitnet_status_string", ctypes.c_char_p, [ctypes.c_int]),
     ("bitnet_last_error", ctypes.c_char_p, []),
 ]
@@ -149,6 +151,15 @@ def bitnet_mpgemm(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=N
                              _ptr(x_scale, "x_scale", torch.float32), M, _ptr(y, "y", torch.float32),
                              _ptr(acc, "acc", torch.int32), ws_ptr, ws_bytes, _stream(stream))
     _check("bitnet_mpgemm", st)
+
+
+def bitnet_elut_tables(xq, lut, lut1=None, stream=None) -> None:
+    """TL2 activation tables of xq (int8 [M, K], device) into lut (int16 [M, ThreeK/3, 16]) and lut1."""
+    import torch
+    M, K = xq.shape
+    st = lib().bitnet_elut_tables(_ptr(xq, "xq", torch.int8), M, K, _ptr(lut, "lut", torch.int16),
+                                  _ptr(lut1, "lut1", torch.int16), _stream(stream))
+    _check("bitnet_elut_tables", st)
 
 
 def bitnet_status_string(status: int) -> str:

@@ -112,16 +112,35 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
                     packed_bytes_of(layout, N, K));
     const size_t need = bitnet_mpgemm_workspace_bytes(layout, M, N, K);
     if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
-    if (layout != BITNET_LAYOUT_I2S) return fail(BITNET_E_LAYOUT, "TL2 accumulation is not available in this build");
 
     hipStream_t s = (hipStream_t)stream;
-    for (int64_t m0 = 0; m0 < M; m0 += 16) {
-        const int mc = (int)((M - m0) < 16 ? (M - m0) : 16);
-        hipError_t e = bitnet::launch_i2s_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
-                                                 y + m0 * N, acc ? acc + m0 * N : nullptr, s);
+    const int64_t slice = layout == BITNET_LAYOUT_I2S ? 16 : bitnet::kElutMaxTokens;
+    for (int64_t m0 = 0; m0 < M; m0 += slice) {
+        const int mc = (int)((M - m0) < slice ? (M - m0) : slice);
+        hipError_t e;
+        if (layout == BITNET_LAYOUT_I2S)
+            e = bitnet::launch_i2s_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K, y + m0 * N,
+                                          acc ? acc + m0 * N : nullptr, s);
+        else
+            e = bitnet::launch_tl2_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
+                                               y + m0 * N, acc ? acc + m0 * N : nullptr, s);
         if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
     }
     return ok();
+}
+
+bitnet_status bitnet_elut_tables(const int8_t* xq, int64_t M, int64_t K, int16_t* lut, int16_t* lut1, void* stream) {
+    if (!xq || !lut) return fail(BITNET_E_INVALID, "null pointer argument");
+    if (M < 1 || M > ((int64_t)1 << 24) || K <= 0 || K % bitnet::kSubK != 0 || K > kMaxK)
+        return fail(BITNET_E_SHAPE, "need M >= 1 and K %% 64 == 0, 0 < K <= %lld; got M=%lld K=%lld", (long long)kMaxK,
+                    (long long)M, (long long)K);
+    const int64_t three = (K / bitnet::kTl2BlockK) * bitnet::kTl2BlockK;
+    if (three == 0) return fail(BITNET_E_SHAPE, "K = %lld has no 384-weight TL2 block", (long long)K);
+    if (K != three && !lut1) return fail(BITNET_E_INVALID, "lut1 is required when K %% 384 != 0");
+    if (!aligned(xq, 16) || !aligned(lut, 16) || (lut1 && !aligned(lut1, 16)))
+        return fail(BITNET_E_ALIGN, "xq, lut and lut1 need 16-byte alignment");
+    return hip_status(bitnet::launch_elut_tables(xq, (int)M, (int)K, lut, lut1, (hipStream_t)stream),
+                      "bitnet_elut_tables launch");
 }
 
 const char* bitnet_status_string(int status) {

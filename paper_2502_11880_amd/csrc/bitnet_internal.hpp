@@ -49,4 +49,12 @@ hipError_t launch_i2s_decode(const void* packed, const float* w_scale, const int
                              const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
                              hipStream_t stream);
 
+constexpr int kElutMaxTokens = 8;     // tokens per ELUT launch
+int tl2_elut_waves(int M);
+size_t tl2_elut_lds_bytes(int M);
+hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, const int8_t* xq,
+                                  const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
+                                  hipStream_t stream);
+hipError_t launch_elut_tables(const int8_t* xq, int M, int K, int16_t* lut, int16_t* lut1, hipStream_t stream);
+
 }  // namespace bitnet

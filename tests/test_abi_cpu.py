@@ -88,6 +88,15 @@ def test_quantize_and_pack_validation_statuses():
     assert lib.bitnet_pack_weights(0, FAKE, 64, 64, FAKE + 2, 1 << 20, FAKE, FAKE, ws, None) == 3
 
 
+def test_elut_tables_validation_statuses():
+    lib = B.lib()
+    assert lib.bitnet_elut_tables(None, 1, 384, FAKE, FAKE, None) == 1
+    assert lib.bitnet_elut_tables(FAKE, 1, 320, FAKE, FAKE, None) == 2      # no TL2 block
+    assert lib.bitnet_elut_tables(FAKE, 1, 400, FAKE, FAKE, None) == 2      # K % 64
+    assert lib.bitnet_elut_tables(FAKE, 1, 448, FAKE, None, None) == 1      # tail needs lut1
+    assert lib.bitnet_elut_tables(FAKE + 2, 1, 384, FAKE, None, None) == 3
+
+
 def test_status_strings():
     for st in range(7):
         assert B.bitnet_status_string(st)

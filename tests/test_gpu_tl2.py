@@ -1,0 +1,110 @@
+"""GPU parity of the TL2 path (packing, the ELUT tables and the table-lookup accumulation) against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bitnet_oracle as O
+from paper_2502_11880_amd import inputs
+import paper_2502_11880_amd as B
+from tests import hip_runner as H
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(*what):
+    print("case:", *what, flush=True)
+
+
+@pytest.mark.parametrize("N,K", [(16, 64), (16, 384), (32, 448), (48, 832), (64, 1600), (208, 3200), (64, 4096),
+                                 (32, 8640), (16, 14336)])
+def test_pack_tl2_bit_exact(N, K):
+    _announce("pack tl2", N, K)
+    W = inputs.weight_f32(N, K, seed=inputs.seed_for(8, 3 * N + K))
+    packed, w_scale = H.pack(W, "tl2")
+    t_ref, beta_ref = O.ternarize(W.numpy())
+    assert H.to_np(w_scale)[0] == beta_ref
+    got = H.to_np(packed)
+    ref = O.pack_tl2(t_ref)
+    assert got.size == ref.size
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("M,K", [(1, 384), (2, 448), (3, 4096), (1, 8640), (5, 14336)])
+def test_elut_tables_bit_exact(M, K):
+    _announce("elut tables", M, K)
+    x = inputs.activation_f32(M, K, seed=inputs.seed_for(6, M + K))
+    xq, _ = H.quantize(x)
+    three, two = O.tl2_split(K)
+    lut = torch.empty((M, three // 3, 16), dtype=torch.int16, device=H.DEV)
+    lut1 = torch.empty((M, max(two // 2, 1), 16), dtype=torch.int16, device=H.DEV)
+    B.bitnet_elut_tables(xq, lut, lut1 if two else None)
+    ref, ref1 = O.elut_tables(H.to_np(xq))
+    got = H.to_np(lut).astype(np.int64)
+    assert np.array_equal(got[..., :14], ref)
+    assert not got[..., 14:].any()
+    if two:
+        got1 = H.to_np(lut1).astype(np.int64)
+        assert np.array_equal(got1[..., :9], ref1)
+        assert not got1[..., 9:].any()
+
+
+def _tl2_vs_oracle(M, N, K, seed, repeat=True):
+    W = inputs.weight_f32(N, K, seed=seed)
+    x = inputs.activation_f32(M, K, seed=seed + 500)
+    packed, w_scale = H.pack(W, "tl2")
+    xq, s = H.quantize(x)
+    y, acc = H.mpgemm("tl2", packed, w_scale, N, K, xq, s)
+    y_ref, acc_ref, *_ = O.mpgemm_reference(x.numpy(), W.numpy())
+    acc_np = H.to_np(acc)
+    assert np.array_equal(acc_np, acc_ref)
+    H.check_y(H.to_np(y), y_ref, acc_ref)
+    if repeat:
+        y2, acc2 = H.mpgemm("tl2", packed, w_scale, N, K, xq, s)
+        assert np.array_equal(H.to_np(acc2), acc_np)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 16, 64), (1, 16, 384), (1, 32, 448), (2, 48, 832), (3, 64, 1600),
+                                   (4, 208, 3200), (5, 16, 4096), (8, 96, 1536), (9, 32, 8640), (16, 16, 768),
+                                   (17, 48, 448), (1, 1024, 4096)])
+def test_tl2_mpgemm_parity(M, N, K):
+    _announce("tl2 mpgemm", M, N, K)
+    _tl2_vs_oracle(M, N, K, seed=inputs.seed_for(5, M * 131 + N * 7 + K))
+
+
+def test_tl2_elut_matches_i2s_on_same_weights():
+    _announce("tl2 == i2s")
+    M, N, K = 3, 64, 3200
+    W = inputs.weight_f32(N, K, seed=44)
+    x = inputs.activation_f32(M, K, seed=45)
+    xq, s = H.quantize(x)
+    p1, b1 = H.pack(W, "i2s")
+    p2, b2 = H.pack(W, "tl2")
+    y1, a1 = H.mpgemm("i2s", p1, b1, N, K, xq, s)
+    y2, a2 = H.mpgemm("tl2", p2, b2, N, K, xq, s)
+    assert np.array_equal(H.to_np(a1), H.to_np(a2))
+    assert np.array_equal(H.to_np(y1), H.to_np(y2))
+
+
+def test_tl2_extreme_values():
+    _announce("tl2 extremes")
+    N, K = 32, 832
+    W = torch.full((N, K), 0.02)
+    W[1::2] *= -1
+    W[:, 5::7] = 0.0
+    x = torch.full((2, K), 5.0)
+    x[1] = -5.0
+    packed, w_scale = H.pack(W, "tl2")
+    xq, s = H.quantize(x)
+    y, acc = H.mpgemm("tl2", packed, w_scale, N, K, xq, s)
+    y_ref, acc_ref, *_ = O.mpgemm_reference(x.numpy(), W.numpy())
+    assert np.array_equal(H.to_np(acc), acc_ref)
+    H.check_y(H.to_np(y), y_ref, acc_ref)
+
+
+@pytest.mark.parametrize("workload", [0, 1, 2])
+def test_tl2_workload_shapes(workload):
+    spec = inputs.WORKLOADS[workload]
+    for i, (name, K, N, _) in enumerate(spec["linears"]):
+        for M in spec["tokens"]:
+            _announce("tl2 workload", workload, name, M, N, K)
+            _tl2_vs_oracle(M, N, K, seed=inputs.seed_for(workload, i), repeat=False)
