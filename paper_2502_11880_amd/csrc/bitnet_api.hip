@@ -31,7 +31,8 @@ bitnet_status hip_status(hipError_t e, const char* what) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-constexpr int64_t kMaxK = 132096;   // 127 * K < 2^24: accumulators stay exact in fp32
+constexpr int64_t kMaxK = 132096;
+constexpr int64_t kDecodeMaxTokens = 16;   // up to 16 tokens fill the rows of one 16x16x64 MFMA   // 127 * K < 2^24: accumulators stay exact in fp32
 
 bool weight_shape_ok(int64_t N, int64_t K) {
     return N > 0 && K > 0 && N % bitnet::kRowsPerGroup == 0 && K % bitnet::kSubK == 0 && K <= kMaxK &&
@@ -114,6 +115,9 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
     if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
 
     hipStream_t s = (hipStream_t)stream;
+    if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens)
+        return hip_status(bitnet::launch_i2s_prefill(packed, w_scale, xq, x_scale, (int)M, (int)N, (int)K, y, acc, s),
+                          "bitnet_mpgemm launch");
     const int64_t slice = layout == BITNET_LAYOUT_I2S ? 16 : bitnet::kElutMaxTokens;
     for (int64_t m0 = 0; m0 < M; m0 += slice) {
         const int mc = (int)((M - m0) < slice ? (M - m0) : slice);

@@ -49,6 +49,9 @@ hipError_t launch_i2s_decode(const void* packed, const float* w_scale, const int
                              const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
                              hipStream_t stream);
 
+hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
+                              int M, int N, int K, float* y, int32_t* acc, hipStream_t stream);
+
 constexpr int kElutMaxTokens = 8;     // tokens per ELUT launch
 int tl2_elut_waves(int M);
 size_t tl2_elut_lds_bytes(int M);
