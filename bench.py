@@ -1,13 +1,17 @@
 """Benchmark of the ternary x int8 mpGEMM hot path on one MI355X.
 
-One step = one pass of the hot path over one batch of synthetic input for every linear of the workload:
-per-token int8 quantisation of each activation group (q/k/v share one input, gate/up share one) and the
-ternary mpGEMM with its fused epilogue for each linear.  Weights are ternarised and packed once before
-timing (offline preprocessing); the packed copies rotate so that every step streams its weights from
-HBM rather than from the 256 MB Infinity Cache.
+One step = one pass of the hot path over one batch of synthetic input through every linear of the
+workload, in layer order: the q/k/v group, o, the gate/up group, down.  Each group quantises its input
+activation per token (int8, absmax) and multiplies it by the group's packed ternary weights with the fused
+dequantisation epilogue.  Decode (M <= 16) runs each group as one fused launch (bitnet_mpgemm_fused); the
+separate-call path (bitnet_quantize_act + one bitnet_mpgemm per weight) is timed too and reported beside
+it.  Prefill (M > 16) runs the quantiser and the MFMA GEMM per weight.  Weights are ternarised and packed
+once before timing (offline preprocessing); packed copies rotate so every step streams its weights from HBM
+rather than from the 256 MB Infinity Cache.
 
-Prints one JSON line.  `value` is the packed-weight bandwidth of the step (GB/s); `roofline` describes
-the dominant kernel (the mpGEMM) from HIP events around a graph of its launches back to back;
+The K timed steps are captured once in a HIP graph and replayed, so the GPU runs them back to back.
+Prints one JSON line.  Decode: `value` = packed weight bytes per step / step time (GB/s), `roofline` bound
+"hbm".  Prefill: `value` = int8 TOP/s of the step (2*M*N*K per linear), `roofline` bound "mfma".
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -15,13 +19,14 @@ from __future__ import annotations
 import argparse
 import json
 import math
-import os
 import sys
 import time
 
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 MFMA, TOP/s
 ROT_BYTES = 512 << 20            # rotate through at least 2x the Infinity Cache
+DECODE_MAX_TOKENS = 16
+METRIC = "decode GEMV weight GB/s (% HBM peak) + tokens/s; prefill int8 TOPS (% MFMA peak)"
 
 
 def parse():
@@ -38,6 +43,14 @@ def parse():
     return p.parse_args()
 
 
+def activation_groups(by_name, inputs):
+    """Linears that read the same input, in layer order; any linear not in a listed group stands alone."""
+    groups = [[n for n in g if n in by_name] for g in inputs.ACTIVATION_GROUPS]
+    groups = [g for g in groups if g]
+    listed = {n for g in groups for n in g}
+    return groups + [[n] for n in by_name if n not in listed]
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -45,7 +58,6 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     import paper_2502_11880_amd as B
@@ -55,9 +67,13 @@ def main():
     torch.cuda.set_device(dev)
     spec = inputs.WORKLOADS[args.workload]
     M = args.tokens if args.tokens is not None else spec["tokens"][0]
+    decode = M <= DECODE_MAX_TOKENS
     layout = args.layout
     linears = [(name, K, N) for name, K, N, _ in spec["linears"]]
     by_name = {name: (K, N) for name, K, N in linears}
+    if not decode:
+        args.steps = max(1, min(args.steps, 20))
+        args.warmup = max(1, min(args.warmup, 3))
 
     # ---- offline: generate, ternarise and pack every weight on the GPU ----
     packed, scales = {}, {}
@@ -71,90 +87,118 @@ def main():
         del W
     torch.cuda.synchronize()
     step_weight_bytes = sum(p.numel() for p in packed.values())
-    copies = max(1, math.ceil(ROT_BYTES / step_weight_bytes))
+    copies = max(1, math.ceil(ROT_BYTES / step_weight_bytes)) if decode else 1
     rot = [packed] + [{k: v.clone() for k, v in packed.items()} for _ in range(copies - 1)]
 
-    groups = [[n for n in g if n in by_name] for g in inputs.ACTIVATION_GROUPS]
-    groups = [g for g in groups if g]
-    xs, xqs, sxs = [], [], []
+    groups = activation_groups(by_name, inputs)
+    xs, xqs, sxs, rss = [], [], [], []
     for gi, g in enumerate(groups):
         K = by_name[g[0]][0]
         xs.append(inputs.activation_f32(M, K, seed=inputs.seed_for(args.workload, 100 + gi)).to(dev))
         xqs.append(torch.empty((M, K), dtype=torch.int8, device=dev))
         sxs.append(torch.empty(M, dtype=torch.float32, device=dev))
+        rss.append(torch.empty(M, dtype=torch.int32, device=dev))
     ys = {n: torch.empty((M, by_name[n][1]), dtype=torch.float32, device=dev) for n in by_name}
-    wss = {n: torch.zeros(max(16, B.bitnet_mpgemm_workspace_bytes(layout, M, by_name[n][1], by_name[n][0])),
-                          dtype=torch.uint8, device=dev) for n in by_name}
+    ws_bytes = max(B.bitnet_mpgemm_workspace_bytes(layout, M, N, K) for _, K, N in linears)
+    ws = torch.zeros(max(16, ws_bytes), dtype=torch.uint8, device=dev)
+    fargs = [[B.FusedArgs([rot[c][n] for n in g], [scales[n] for n in g], [ys[n] for n in g]) for g in groups]
+             for c in range(copies)] if decode else None
     stream = torch.cuda.Stream()
     sptr = stream.cuda_stream
 
-    def step(i, quantize=True):
-        pk = rot[i % copies]
+    def step(i, path, quantize=True):
+        c = i % copies
         for gi, g in enumerate(groups):
+            if path == "fused":
+                B.bitnet_mpgemm_fused(layout, None, None, xs[gi], xqs[gi], sxs[gi], rss[gi], None, ws, sptr,
+                                      args=fargs[c][gi])
+                continue
             if quantize:
-                B.bitnet_quantize_act(xs[gi], xqs[gi], sxs[gi], sptr)
+                B.bitnet_quantize_act(xs[gi], xqs[gi], sxs[gi], rss[gi], sptr)
             for n in g:
                 K, N = by_name[n]
-                B.bitnet_mpgemm(layout, pk[n], scales[n], N, K, xqs[gi], sxs[gi], ys[n], None, wss[n], sptr)
+                B.bitnet_mpgemm(layout, rot[c][n], scales[n], N, K, xqs[gi], sxs[gi], ys[n], None, ws, sptr,
+                                x_rowsum=rss[gi])
 
+    def capture(fn):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(args.steps):
+                fn(args.warmup + i)
+        return g
+
+    main_path = "fused" if decode else "separate"
     with torch.cuda.stream(stream):
         for i in range(args.warmup):
-            step(i)
+            step(i, main_path)
+            if decode:
+                step(i, "separate")
     torch.cuda.synchronize()
 
-    # The K timed steps are captured once as a HIP graph and replayed, so the GPU runs them back to back
-    # (host-side launch overhead would otherwise dominate kernels this short).  A second graph holds only
-    # the mpGEMM launches of the same K steps, back to back: its time per launch is the dominant kernel's
-    # launch duration (including the short gap between graph nodes).
-    g_steps = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g_steps, stream=stream):
-        for i in range(args.steps):
-            step(args.warmup + i)
-    g_gemm = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g_gemm, stream=stream):
-        for i in range(args.steps):
-            step(args.warmup + i, quantize=False)
+    # Graphs: the K steps on the main path, the same steps on the separate-call path (decode), or the
+    # mpGEMM launches alone (prefill: the dominant kernel).
+    g_main = capture(lambda i: step(i, main_path))
+    g_second = capture(lambda i: step(i, "separate")) if decode else \
+        capture(lambda i: step(i, "separate", quantize=False))
     with torch.cuda.stream(stream):
-        g_steps.replay()
-        g_gemm.replay()
+        g_main.replay()
+        g_second.replay()
     torch.cuda.synchronize()
 
-    # ---- timed region: one replay of the K-step graph, then one of the mpGEMM-only graph ----
+    # ---- timed region ----
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     w0 = time.perf_counter()
     with torch.cuda.stream(stream):
         ev[0].record(stream)
-        g_steps.replay()
+        g_main.replay()
         ev[1].record(stream)
-        g_gemm.replay()
+        g_second.replay()
         ev[2].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    gpu_ms = ev[0].elapsed_time(ev[1])
-    ms_per_step = gpu_ms / args.steps
-    gemm_total_ms = ev[1].elapsed_time(ev[2])
-    launches = args.steps * len(linears)
+    ms_per_step = ev[0].elapsed_time(ev[1]) / args.steps
+    second_ms = ev[1].elapsed_time(ev[2]) / args.steps
 
-    per_launch_bytes = {n: packed[n].numel() + M * by_name[n][0] + 4 * M * by_name[n][1] for n in by_name}
-    avg_bytes = sum(per_launch_bytes.values()) / len(per_launch_bytes)
-    avg_launch_ms = gemm_total_ms / launches
-    achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
-
-    value = step_weight_bytes / (ms_per_step * 1e-3) / 1e9
+    flops = sum(2.0 * M * N * K for _, K, N in linears)
+    if decode:
+        value = step_weight_bytes / (ms_per_step * 1e-3) / 1e9
+        unit = "GB/s"
+        launches = len(groups)
+        grp_bytes = [sum(packed[n].numel() + 4 * M * by_name[n][1] for n in g) + 5 * M * by_name[g[0]][0] + 8 * M
+                     for g in groups]
+        avg_bytes = sum(grp_bytes) / launches
+        avg_launch_ms = ms_per_step / launches
+        achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
+        kernel = ("i2s_decode_fused_kernel (bitnet_mpgemm_fused)" if layout == "i2s"
+                  else "bitnet_mpgemm_fused on TL2: quantiser + one ELUT launch per weight")
+        roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_bytes": int(avg_bytes),
+                    "launches_per_step": launches}
+    else:
+        value = flops / (ms_per_step * 1e-3) / 1e12
+        unit = "TOP/s"
+        launches = len(linears)
+        avg_launch_ms = second_ms / launches
+        achieved = (flops / launches) / (avg_launch_ms * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "kernel": "i2s_prefill_kernel (bitnet_mpgemm, M > 16)",
+                    "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": None,
+                    "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_ops": int(flops / launches),
+                    "launches_per_step": launches}
     tokens_per_s = M / (ms_per_step * 1e-3)
 
     parity = None
     if not args.no_parity:
-        parity = parity_spot_check(args, layout, M, linears, packed, scales, xs, groups, by_name, dev)
-
+        parity = parity_spot_check(args, layout, M, linears, packed, scales, xs, dev)
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes)
+        cpu = cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, decode)
 
     out = {
-        "metric": "decode GEMV weight GB/s (% HBM peak) + tokens/s; prefill int8 TOPS (% MFMA peak)",
+        "metric": METRIC,
         "value": round(value, 2),
-        "unit": "GB/s",
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -164,24 +208,23 @@ def main():
         "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic",
-        "config": {"workload": spec["name"], "tokens": M, "layout": layout,
+        "config": {"workload": spec["name"], "tokens": M, "layout": layout, "path": main_path,
                    "linears": [f"{n}:{K}x{N}" for n, K, N in linears],
                    "packed_weight_bytes_per_step": step_weight_bytes, "rotating_copies": copies},
         "tokens_per_s": round(tokens_per_s, 1),
-        "hbm_frac_step": round(value / HBM_PEAK_GBS, 4),
+        "hbm_frac_step": round(step_weight_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "mfma_frac_step": round(flops / (ms_per_step * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+        ("separate_path_ms_per_step" if decode else "gemm_only_ms_per_step"): round(second_ms, 5),
         "wall_s": round(wall, 3),
-        "roofline": {"bound": "hbm", "kernel": "bitnet_mpgemm (decode GEMV)", "achieved": round(achieved, 2),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "avg_launch_us": round(avg_launch_ms * 1e3, 3),
-                     "avg_algorithmic_bytes": int(avg_bytes), "launches": launches},
+        "roofline": roofline,
         "cpu_baseline": cpu,
         "parity": parity,
     }
     print(json.dumps(out), flush=True)
 
 
-def parity_spot_check(args, layout, M, linears, packed, scales, xs, groups, by_name, dev):
-    """Bit-exact check of the benchmark's own first linear against the oracle."""
+def parity_spot_check(args, layout, M, linears, packed, scales, xs, dev):
+    """Bit-exact check of the benchmark's own first linear against the oracle (sampled rows for prefill)."""
     import numpy as np
     import torch
 
@@ -194,21 +237,27 @@ def parity_spot_check(args, layout, M, linears, packed, scales, xs, groups, by_n
     x = xs[0].cpu()
     xq = torch.empty((M, K), dtype=torch.int8, device=dev)
     s = torch.empty(M, dtype=torch.float32, device=dev)
-    B.bitnet_quantize_act(xs[0], xq, s)
+    rs = torch.empty(M, dtype=torch.int32, device=dev)
+    B.bitnet_quantize_act(xs[0], xq, s, rs)
     y = torch.empty((M, N), dtype=torch.float32, device=dev)
     acc = torch.empty((M, N), dtype=torch.int32, device=dev)
     ws = torch.zeros(max(16, B.bitnet_mpgemm_workspace_bytes(layout, M, N, K)), dtype=torch.uint8, device=dev)
-    B.bitnet_mpgemm(layout, packed[name], scales[name], N, K, xq, s, y, acc, ws)
+    B.bitnet_mpgemm(layout, packed[name], scales[name], N, K, xq, s, y, acc, ws, x_rowsum=rs)
     torch.cuda.synchronize()
-    y_ref, acc_ref, *_ = O.mpgemm_reference(x.numpy(), W.numpy())
-    exact = bool(np.array_equal(acc.cpu().numpy(), acc_ref))
-    rel = float(np.max(np.abs(y.cpu().numpy().astype(np.float64) - y_ref) / np.maximum(np.abs(y_ref), 1e-30)))
-    return {"linear": f"{name}:{K}x{N}", "acc_bit_exact": exact, "y_max_rel_err": rel}
+    rows = np.arange(M) if M <= 16 else np.unique(np.r_[0, M - 1, np.random.default_rng(0).choice(M, 6, False)])
+    xq_ref, s_ref = O.quantize_act(x.numpy())
+    t_ref, beta = O.ternarize(W.numpy())
+    acc_ref = O.mad_gemm(xq_ref[rows], t_ref)
+    y_ref = O.epilogue(acc_ref, beta, s_ref[rows])
+    exact = bool(np.array_equal(acc.cpu().numpy()[rows], acc_ref))
+    yg = y.cpu().numpy()[rows].astype(np.float64)
+    rel = float(np.max(np.abs(yg - y_ref) / np.maximum(np.abs(y_ref), 1e-30)))
+    return {"linear": f"{name}:{K}x{N}", "rows_checked": int(len(rows)), "acc_bit_exact": exact,
+            "y_max_rel_err": rel}
 
 
-def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes):
+def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, decode):
     """Time the oracle (quantise + exact integer accumulation + epilogue) on the host for ~cpu_seconds."""
-    import numpy as np
     import torch
 
     from oracle import bitnet_oracle as O
@@ -219,7 +268,9 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes):
     for i, (name, K, N) in enumerate(linears):
         W = inputs.weight_f32(N, K, seed=inputs.seed_for(args.workload, i)).numpy()
         ts[name], betas[name] = O.ternarize(W)
-    xs = [inputs.activation_f32(M, by_name[g[0]][0], seed=inputs.seed_for(args.workload, 100 + gi)).numpy()
+    # prefill: a bounded sample of token rows stands in for the full M
+    Mc = M if decode else min(M, 4)
+    xs = [inputs.activation_f32(M, by_name[g[0]][0], seed=inputs.seed_for(args.workload, 100 + gi)).numpy()[:Mc]
           for gi, g in enumerate(groups)]
     t0 = time.perf_counter()
     steps = 0
@@ -233,10 +284,13 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes):
         if el >= args.cpu_seconds:
             break
     per_step = el / steps
-    return {"value": round(step_weight_bytes / per_step / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} full steps of the same workload (all {len(linears)} linears, M={M}) in {el:.1f} s; "
-                      "numpy int64 matmul, single thread",
-            "tokens_per_s": round(M / per_step, 3)}
+    if decode:
+        return {"value": round(step_weight_bytes / per_step / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": f"{steps} full steps of the same workload (all {len(linears)} linears, M={M}) in {el:.1f} s; "
+                          "numpy int64 matmul, one thread", "tokens_per_s": round(M / per_step, 3)}
+    return {"value": round(flops * Mc / M / per_step / 1e12, 6), "unit": "TOP/s", "cores": 1, "kind": "oracle",
+            "sample": f"{steps} steps of the same linears on {Mc} of the {M} token rows in {el:.1f} s; "
+                      "numpy int64 matmul, one thread", "tokens_per_s": round(Mc / per_step, 3)}
 
 
 if __name__ == "__main__":

@@ -87,13 +87,15 @@ bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t
 
 /*
  * bitnet_quantize_act -- per-token absmax int8 quantisation (Sec. 2.1, Sec. 3.2.2).
- *   x        device fp32 [M, K], finite values.
- *   xq       device int8 [M, K]:  xq = clamp(rint(fp32(x * s_m)), -128, 127)  (ties to even).
- *   x_scale  device fp32 [M]:     s_m = fp32(127 / max(max_k |x[m, k]|, 1e-5)).
- *   Shapes: M >= 1, 1 <= K <= 1048576.  Pointers 16-byte aligned.
+ *   x         device fp32 [M, K], finite values.
+ *   xq        device int8 [M, K]:  xq = clamp(rint(fp32(x * s_m)), -128, 127)  (ties to even).
+ *   x_scale   device fp32 [M]:     s_m = fp32(127 / max(max_k |x[m, k]|, 1e-5)).
+ *   x_rowsum  device int32 [M] or NULL: sum_k xq[m, k].  Passing it on to bitnet_mpgemm saves the I2_S
+ *             kernels the work of forming it (their codes are t + 1, so they subtract this sum).
+ *   Shapes: M >= 1, 1 <= K <= 1048576.  x and xq 16-byte aligned, x_scale and x_rowsum 4-byte.
  */
 bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
-                                  void* stream);
+                                  int32_t* x_rowsum, void* stream);
 
 /* Workspace bytes bitnet_mpgemm needs for this problem (0 is a valid answer). */
 size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K);
@@ -102,6 +104,7 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  * bitnet_mpgemm -- ternary x int8 accumulation with the dequantisation epilogue (Eq. 1 / Eq. 3).
  *   packed, packed_bytes, w_scale   as written by bitnet_pack_weights for an N x K weight in `layout`.
  *   xq, x_scale                     as written by bitnet_quantize_act for an M x K activation.
+ *   x_rowsum                        as written by bitnet_quantize_act, or NULL (then computed here).
  *   y      device fp32 [M, N]: y[m, n] = fp32(acc[m, n]) * fp32(w_scale / x_scale[m]).
  *   acc    device int32 [M, N] or NULL: when given, also receives acc[m, n] = sum_k xq[m, k] * t[n, k]
  *          exactly (the same integers for every tiling and launch shape).
@@ -114,8 +117,29 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *   M <= 16 runs the decode GEMV; larger M runs the prefill GEMM.
  */
 bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale,
-                            int64_t N, int64_t K, const int8_t* xq, const float* x_scale, int64_t M,
-                            float* y, int32_t* acc, void* ws, size_t ws_bytes, void* stream);
+                            int64_t N, int64_t K, const int8_t* xq, const float* x_scale,
+                            const int32_t* x_rowsum, int64_t M, float* y, int32_t* acc, void* ws,
+                            size_t ws_bytes, void* stream);
+
+/*
+ * bitnet_mpgemm_fused -- one activation, several weights: bitnet_quantize_act followed by bitnet_mpgemm for
+ * each weight, as one launch where possible (the decode step of the linears that read the same input, such
+ * as q/k/v or gate/up).  Results are identical to those separate calls.
+ *   n_linears                   1..8.
+ *   packed, packed_bytes, w_scale, N, y
+ *                               HOST arrays of n_linears entries: device packed buffer, its size, device beta,
+ *                               rows of that weight, device fp32 output [M, N[i]].
+ *   K, x, M                     the shared reduction length and the device fp32 activation [M, K].
+ *   xq, x_scale, x_rowsum       device outputs as in bitnet_quantize_act (all three required).
+ *   ws                          as for bitnet_mpgemm, at least the largest workspace of the n products.
+ *   Shapes: 1 <= M <= 16; each weight as in bitnet_mpgemm.  I2_S with M == 1 and K <= 61440 runs as one launch
+ *   (every work group quantises the row itself, keeping the codes in LDS); other I2_S cases run the quantiser
+ *   and then all products in one launch; TL2 runs the quantiser and one launch per weight.
+ */
+bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* packed, const size_t* packed_bytes,
+                                  const float* const* w_scale, const int64_t* N, int64_t K, const float* x,
+                                  int64_t M, int8_t* xq, float* x_scale, int32_t* x_rowsum, float* const* y,
+                                  void* ws, size_t ws_bytes, void* stream);
 
 /*
  * bitnet_elut_tables -- the activation tables of the TL2 path, written out (Eq. 3; mirror consolidation,

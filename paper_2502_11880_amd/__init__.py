@@ -30,12 +30,17 @@ _SIGNATURES = [
      [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t,
       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     ("bitnet_quantize_act", ctypes.c_int,
-     [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+     [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+      ctypes.c_void_p]),
     ("bitnet_mpgemm_workspace_bytes", ctypes.c_size_t, [ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]),
     ("bitnet_mpgemm", ctypes.c_int,
      [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
-      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-      ctypes.c_size_t, ctypes.c_void_p]),
+      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    ("bitnet_mpgemm_fused", ctypes.c_int,
+     [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+      ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     ("bitnet_elut_tables", ctypes.c_int,
      [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     ("bitnet_status_string", ctypes.c_char_p, [ctypes.c_int]),
@@ -131,16 +136,19 @@ def bitnet_pack_weights(layout, W, packed, w_scale, ws, stream=None) -> None:
     _check("bitnet_pack_weights", st)
 
 
-def bitnet_quantize_act(x, xq, x_scale, stream=None) -> None:
-    """Per-token absmax int8 quantisation of x (fp32 [M, K], device) into xq (int8) and x_scale (fp32 [M])."""
+def bitnet_quantize_act(x, xq, x_scale, x_rowsum=None, stream=None) -> None:
+    """Per-token absmax int8 quantisation of x (fp32 [M, K], device) into xq (int8), x_scale (fp32 [M]) and,
+    optionally, x_rowsum (int32 [M])."""
     import torch
     M, K = x.shape
     st = lib().bitnet_quantize_act(_ptr(x, "x", torch.float32), M, K, _ptr(xq, "xq", torch.int8),
-                                   _ptr(x_scale, "x_scale", torch.float32), _stream(stream))
+                                   _ptr(x_scale, "x_scale", torch.float32), _ptr(x_rowsum, "x_rowsum", torch.int32),
+                                   _stream(stream))
     _check("bitnet_quantize_act", st)
 
 
-def bitnet_mpgemm(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=None, ws=None, stream=None) -> None:
+def bitnet_mpgemm(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=None, ws=None, stream=None,
+                  x_rowsum=None) -> None:
     """y = dequant(xq @ t^T) for the packed ternary weight; optionally the exact int32 accumulators."""
     import torch
     M = xq.shape[0]
@@ -148,9 +156,42 @@ def bitnet_mpgemm(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=N
     ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
     st = lib().bitnet_mpgemm(_layout(layout), _ptr(packed, "packed", torch.uint8), packed.numel(),
                              _ptr(w_scale, "w_scale", torch.float32), N, K, _ptr(xq, "xq", torch.int8),
-                             _ptr(x_scale, "x_scale", torch.float32), M, _ptr(y, "y", torch.float32),
+                             _ptr(x_scale, "x_scale", torch.float32), _ptr(x_rowsum, "x_rowsum", torch.int32), M,
+                             _ptr(y, "y", torch.float32),
                              _ptr(acc, "acc", torch.int32), ws_ptr, ws_bytes, _stream(stream))
     _check("bitnet_mpgemm", st)
+
+
+class FusedArgs:
+    """Host arrays for bitnet_mpgemm_fused, built once so repeated calls only pass pointers."""
+
+    def __init__(self, packed, w_scales, ys):
+        import torch
+        n = len(packed)
+        self.n = n
+        self.packed = (ctypes.c_void_p * n)(*[_ptr(p, "packed", torch.uint8) for p in packed])
+        self.packed_bytes = (ctypes.c_size_t * n)(*[p.numel() for p in packed])
+        self.w_scale = (ctypes.c_void_p * n)(*[_ptr(w, "w_scale", torch.float32) for w in w_scales])
+        self.N = (ctypes.c_int64 * n)(*[y.shape[1] for y in ys])
+        self.y = (ctypes.c_void_p * n)(*[_ptr(y, "y", torch.float32) for y in ys])
+        self._keep = (list(packed), list(w_scales), list(ys))
+
+
+def bitnet_mpgemm_fused(layout, packed, w_scales, x, xq, x_scale, x_rowsum, ys, ws=None, stream=None,
+                        args: FusedArgs = None) -> None:
+    """Quantise x (fp32 [M, K]) and multiply it by every packed weight (lists of equal length) in one call."""
+    import torch
+    M, K = x.shape
+    a = args if args is not None else FusedArgs(packed, w_scales, ys)
+    if a.n < 1:
+        raise ValueError("bitnet_mpgemm_fused needs at least one weight")
+    ws_ptr = _ptr(ws, "ws") if ws is not None else None
+    ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    st = lib().bitnet_mpgemm_fused(_layout(layout), a.n, a.packed, a.packed_bytes, a.w_scale, a.N, K,
+                                   _ptr(x, "x", torch.float32), M, _ptr(xq, "xq", torch.int8),
+                                   _ptr(x_scale, "x_scale", torch.float32), _ptr(x_rowsum, "x_rowsum", torch.int32),
+                                   a.y, ws_ptr, ws_bytes, _stream(stream))
+    _check("bitnet_mpgemm_fused", st)
 
 
 def bitnet_elut_tables(xq, lut, lut1=None, stream=None) -> None:

@@ -81,14 +81,15 @@ bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t
                       "bitnet_pack_weights launch");
 }
 
-bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale, void* stream) {
+bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
+                                  int32_t* x_rowsum, void* stream) {
     if (!x || !xq || !x_scale) return fail(BITNET_E_INVALID, "null pointer argument");
     if (M < 1 || M > ((int64_t)1 << 31) - 1 || K < 1 || K > ((int64_t)1 << 20))
         return fail(BITNET_E_SHAPE, "need M >= 1 and 1 <= K <= 1048576; got M=%lld K=%lld", (long long)M,
                     (long long)K);
-    if (!aligned(x, 16) || !aligned(xq, 16) || !aligned(x_scale, 4))
-        return fail(BITNET_E_ALIGN, "x and xq need 16-byte alignment, x_scale 4-byte");
-    return hip_status(bitnet::launch_quantize_act(x, M, K, xq, x_scale, (hipStream_t)stream),
+    if (!aligned(x, 16) || !aligned(xq, 16) || !aligned(x_scale, 4) || !aligned(x_rowsum, 4))
+        return fail(BITNET_E_ALIGN, "x and xq need 16-byte alignment, x_scale and x_rowsum 4-byte");
+    return hip_status(bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, (hipStream_t)stream),
                       "bitnet_quantize_act launch");
 }
 
@@ -98,16 +99,16 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
 }
 
 bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale, int64_t N,
-                            int64_t K, const int8_t* xq, const float* x_scale, int64_t M, float* y, int32_t* acc,
-                            void* ws, size_t ws_bytes, void* stream) {
+                            int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
+                            float* y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
     if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
     if (!packed || !w_scale || !xq || !x_scale || !y) return fail(BITNET_E_INVALID, "null pointer argument");
     if (!weight_shape_ok(N, K)) return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
                                             (long long)kMaxK, (long long)N, (long long)K);
     if (M < 1 || M > ((int64_t)1 << 24)) return fail(BITNET_E_SHAPE, "need 1 <= M <= 2^24; got M=%lld", (long long)M);
     if (!aligned(packed, 16) || !aligned(xq, 16) || !aligned(y, 16) || (acc && !aligned(acc, 16)) ||
-        !aligned(ws, 16) || !aligned(w_scale, 4) || !aligned(x_scale, 4))
-        return fail(BITNET_E_ALIGN, "packed, xq, y, acc and ws need 16-byte alignment, scales 4-byte");
+        !aligned(ws, 16) || !aligned(w_scale, 4) || !aligned(x_scale, 4) || !aligned(x_rowsum, 4))
+        return fail(BITNET_E_ALIGN, "packed, xq, y, acc and ws need 16-byte alignment, scales and x_rowsum 4-byte");
     if (packed_bytes < packed_bytes_of(layout, N, K))
         return fail(BITNET_E_INVALID, "packed buffer holds %zu bytes, %zu needed", packed_bytes,
                     packed_bytes_of(layout, N, K));
@@ -115,20 +116,90 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
     if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
 
     hipStream_t s = (hipStream_t)stream;
-    if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens)
-        return hip_status(bitnet::launch_i2s_prefill(packed, w_scale, xq, x_scale, (int)M, (int)N, (int)K, y, acc, s),
+    if (layout == BITNET_LAYOUT_I2S && M <= kDecodeMaxTokens) {
+        bitnet::FusedLinears L{};
+        L.count = 1;
+        L.packed[0] = static_cast<const uint8_t*>(packed);
+        L.w_scale[0] = w_scale;
+        L.y[0] = y;
+        L.acc[0] = acc;
+        L.N[0] = (int)N;
+        L.rg_start[0] = 0;
+        L.rg_start[1] = (int)(N / bitnet::kRowsPerGroup);
+        return hip_status(bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s), "bitnet_mpgemm launch");
+    }
+    if (layout == BITNET_LAYOUT_I2S)
+        return hip_status(bitnet::launch_i2s_prefill(packed, w_scale, xq, x_scale, x_rowsum, (int)M, (int)N, (int)K, y,
+                                                     acc, s),
                           "bitnet_mpgemm launch");
-    const int64_t slice = layout == BITNET_LAYOUT_I2S ? 16 : bitnet::kElutMaxTokens;
+    const int64_t slice = bitnet::kElutMaxTokens;
     for (int64_t m0 = 0; m0 < M; m0 += slice) {
         const int mc = (int)((M - m0) < slice ? (M - m0) : slice);
-        hipError_t e;
-        if (layout == BITNET_LAYOUT_I2S)
-            e = bitnet::launch_i2s_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K, y + m0 * N,
-                                          acc ? acc + m0 * N : nullptr, s);
-        else
-            e = bitnet::launch_tl2_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
-                                               y + m0 * N, acc ? acc + m0 * N : nullptr, s);
+        hipError_t e = bitnet::launch_tl2_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
+                                                      y + m0 * N, acc ? acc + m0 * N : nullptr, s);
         if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
+    }
+    return ok();
+}
+
+bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* packed, const size_t* packed_bytes,
+                                  const float* const* w_scale, const int64_t* N, int64_t K, const float* x, int64_t M,
+                                  int8_t* xq, float* x_scale, int32_t* x_rowsum, float* const* y, void* ws,
+                                  size_t ws_bytes, void* stream) {
+    if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
+    if (n_linears < 1 || n_linears > bitnet::kMaxFused)
+        return fail(BITNET_E_INVALID, "n_linears must be 1..%d; got %d", bitnet::kMaxFused, n_linears);
+    if (!packed || !packed_bytes || !w_scale || !N || !y || !x || !xq || !x_scale || !x_rowsum)
+        return fail(BITNET_E_INVALID, "null pointer argument");
+    if (M < 1 || M > kDecodeMaxTokens) return fail(BITNET_E_SHAPE, "fused decode needs 1 <= M <= 16; got %lld", (long long)M);
+    if (!aligned(x, 16) || !aligned(xq, 16) || !aligned(x_scale, 4) || !aligned(x_rowsum, 4))
+        return fail(BITNET_E_ALIGN, "x and xq need 16-byte alignment, x_scale and x_rowsum 4-byte");
+    size_t need = 0;
+    for (int i = 0; i < n_linears; ++i) {
+        if (!packed[i] || !w_scale[i] || !y[i]) return fail(BITNET_E_INVALID, "null pointer for weight %d", i);
+        if (!weight_shape_ok(N[i], K)) return fail(BITNET_E_SHAPE, "weight %d: need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
+                                                   i, (long long)kMaxK, (long long)N[i], (long long)K);
+        if (!aligned(packed[i], 16) || !aligned(y[i], 16) || !aligned(w_scale[i], 4))
+            return fail(BITNET_E_ALIGN, "weight %d: packed and y need 16-byte alignment, w_scale 4-byte", i);
+        if (packed_bytes[i] < packed_bytes_of(layout, N[i], K))
+            return fail(BITNET_E_INVALID, "weight %d: packed buffer holds %zu bytes, %zu needed", i, packed_bytes[i],
+                        packed_bytes_of(layout, N[i], K));
+        const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
+        need = w > need ? w : need;
+    }
+    if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "workspace needs %zu bytes", need);
+    if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
+
+    hipStream_t s = (hipStream_t)stream;
+    if (layout == BITNET_LAYOUT_I2S) {
+        bitnet::FusedLinears L{};
+        L.count = n_linears;
+        int64_t rgs = 0;
+        for (int i = 0; i < n_linears; ++i) {
+            L.packed[i] = static_cast<const uint8_t*>(packed[i]);
+            L.w_scale[i] = w_scale[i];
+            L.y[i] = y[i];
+            L.acc[i] = nullptr;
+            L.N[i] = (int)N[i];
+            L.rg_start[i] = (int)rgs;
+            rgs += N[i] / bitnet::kRowsPerGroup;
+        }
+        if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
+        L.rg_start[n_linears] = (int)rgs;
+        if (M == 1 && K <= bitnet::kFusedMaxK)      // one launch: quantise inside every work group
+            return hip_status(bitnet::launch_i2s_decode_quant(L, x, (int)K, xq, x_scale, x_rowsum, s),
+                              "bitnet_mpgemm_fused launch");
+        hipError_t e = bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s);
+        if (e == hipSuccess) e = bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s);
+        return hip_status(e, "bitnet_mpgemm_fused launch");
+    }
+    // TL2: the quantiser once, then one table-lookup launch per weight.
+    hipError_t e = bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s);
+    if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm_fused launch");
+    for (int i = 0; i < n_linears; ++i) {
+        const bitnet_status st = bitnet_mpgemm(layout, packed[i], packed_bytes[i], w_scale[i], N[i], K, xq, x_scale,
+                                               x_rowsum, M, y[i], nullptr, ws, ws_bytes, stream);
+        if (st != BITNET_OK) return st;
     }
     return ok();
 }

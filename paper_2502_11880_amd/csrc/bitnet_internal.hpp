@@ -34,23 +34,59 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
+// The four int8 codes of k = 4f .. 4f+3 sit in field f (bits 2f, 2f+1) of the four bytes of an I2_S word.
+__device__ __forceinline__ v4i unpack_codes(uint32_t w) {
+    v4i b;
+    b.x = (int)(w & 0x03030303u);
+    b.y = (int)((w >> 2) & 0x03030303u);
+    b.z = (int)((w >> 4) & 0x03030303u);
+    b.w = (int)((w >> 6) & 0x03030303u);
+    return b;
+}
+
+__device__ __forceinline__ uint32_t word_of(const v4u& v, int j) {
+    return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+}
+
+__device__ __forceinline__ v4u load_stream16(const uint8_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p));
+}
+
+__device__ __forceinline__ v4i mfma16x16x64(v4i a, v4i b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
 // ------------------------------------------------------------------------------------------------
 // Host launchers (each returns the launch status; shapes were validated by the caller)
 // ------------------------------------------------------------------------------------------------
 hipError_t launch_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
-                               hipStream_t stream);
+                               int32_t* x_rowsum, hipStream_t stream);
 
 size_t pack_workspace_bytes();
 hipError_t launch_pack(int layout, const float* W, int64_t N, int64_t K, void* packed, float* w_scale,
                        void* ws, hipStream_t stream);
 
-int i2s_decode_waves(int64_t K);
-hipError_t launch_i2s_decode(const void* packed, const float* w_scale, const int8_t* xq,
-                             const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
-                             hipStream_t stream);
-
 hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                              int M, int N, int K, float* y, int32_t* acc, hipStream_t stream);
+                              const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc,
+                              hipStream_t stream);
+
+// Up to kMaxFused weights that read the same activation, served by one decode launch.
+constexpr int kMaxFused = 8;
+struct FusedLinears {
+    const uint8_t* packed[kMaxFused];
+    const float* w_scale[kMaxFused];
+    float* y[kMaxFused];
+    int32_t* acc[kMaxFused];       // optional exact accumulators (NULL entries allowed)
+    int N[kMaxFused];
+    int rg_start[kMaxFused + 1];   // first 16-row group of each weight in the launch grid
+    int count;
+};
+constexpr int64_t kFusedMaxK = 61440;   // single-token fused quantise+GEMV keeps the K codes in LDS
+size_t i2s_decode_quant_lds_bytes(int64_t K, int waves);
+hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
+                             int M, int K, hipStream_t stream);
+hipError_t launch_i2s_decode_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                                   int32_t* x_rowsum, hipStream_t stream);
 
 constexpr int kElutMaxTokens = 8;     // tokens per ELUT launch
 int tl2_elut_waves(int M);

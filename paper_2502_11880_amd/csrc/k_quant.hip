@@ -4,6 +4,7 @@
 //   gamma_m = max_k |x[m, k]|, floored at 1e-5
 //   s_m     = 127 / gamma_m                       (IEEE fp32 divide, round to nearest even)
 //   xq      = clamp(rint(x * s_m), -128, 127)     (fp32 multiply, ties to even)
+//   rowsum  = sum_k xq[m, k]                      (optional; exact int32)
 //
 // One work group per token row.  The row is read once into registers (up to 16 float4 per lane), reduced
 // to its absmax, then quantised from registers; rows too long for that take a second pass over memory.
@@ -28,6 +29,19 @@ __device__ float block_max(float v, float* red) {
     return red[0];
 }
 
+template <int BLOCK>
+__device__ int block_sum(int v, int* red) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    int t = 0;
+    for (int w = 0; w < BLOCK / 64; ++w) t += red[w];
+    return t;
+}
+
 __device__ __forceinline__ int quant_one(float v, float s) {
     float r = rintf(v * s);
     r = fminf(fmaxf(r, -128.0f), 127.0f);
@@ -36,8 +50,10 @@ __device__ __forceinline__ int quant_one(float v, float s) {
 
 template <int BLOCK, int VPT>
 __global__ __launch_bounds__(BLOCK) void quantize_rows_reg(const float* __restrict__ x, int K,
-                                                           int8_t* __restrict__ xq, float* __restrict__ x_scale) {
+                                                           int8_t* __restrict__ xq, float* __restrict__ x_scale,
+                                                           int32_t* __restrict__ x_rowsum) {
     __shared__ float red[BLOCK / 64];
+    __shared__ int redi[BLOCK / 64];
     const size_t m = blockIdx.x;
     const float4* x4 = reinterpret_cast<const float4*>(x + m * (size_t)K);
     uint32_t* q4 = reinterpret_cast<uint32_t*>(xq + m * (size_t)K);
@@ -53,20 +69,31 @@ __global__ __launch_bounds__(BLOCK) void quantize_rows_reg(const float* __restri
     amax = block_max<BLOCK>(amax, red);
     const float s = 127.0f / fmaxf(amax, 1e-5f);
     if (threadIdx.x == 0) x_scale[m] = s;
+    int sum = 0;
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
         const int idx = threadIdx.x + i * BLOCK;
-        if (idx < K4)
-            q4[idx] = (uint32_t)(quant_one(v[i].x, s) & 0xFF) | ((uint32_t)(quant_one(v[i].y, s) & 0xFF) << 8) |
-                      ((uint32_t)(quant_one(v[i].z, s) & 0xFF) << 16) | ((uint32_t)(quant_one(v[i].w, s) & 0xFF) << 24);
+        if (idx < K4) {
+            const int c0 = quant_one(v[i].x, s), c1 = quant_one(v[i].y, s), c2 = quant_one(v[i].z, s),
+                      c3 = quant_one(v[i].w, s);
+            sum += c0 + c1 + c2 + c3;
+            q4[idx] = (uint32_t)(c0 & 0xFF) | ((uint32_t)(c1 & 0xFF) << 8) | ((uint32_t)(c2 & 0xFF) << 16) |
+                      ((uint32_t)(c3 & 0xFF) << 24);
+        }
+    }
+    if (x_rowsum) {
+        sum = block_sum<BLOCK>(sum, redi);
+        if (threadIdx.x == 0) x_rowsum[m] = sum;
     }
 }
 
 // Any K: two passes over the row.
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void quantize_rows_2pass(const float* __restrict__ x, int K,
-                                                             int8_t* __restrict__ xq, float* __restrict__ x_scale) {
+                                                             int8_t* __restrict__ xq, float* __restrict__ x_scale,
+                                                             int32_t* __restrict__ x_rowsum) {
     __shared__ float red[BLOCK / 64];
+    __shared__ int redi[BLOCK / 64];
     const size_t m = blockIdx.x;
     const float* xr = x + m * (size_t)K;
     int8_t* qr = xq + m * (size_t)K;
@@ -75,25 +102,35 @@ __global__ __launch_bounds__(BLOCK) void quantize_rows_2pass(const float* __rest
     amax = block_max<BLOCK>(amax, red);
     const float s = 127.0f / fmaxf(amax, 1e-5f);
     if (threadIdx.x == 0) x_scale[m] = s;
-    for (int i = threadIdx.x; i < K; i += BLOCK) qr[i] = (int8_t)quant_one(xr[i], s);
+    int sum = 0;
+    for (int i = threadIdx.x; i < K; i += BLOCK) {
+        const int c = quant_one(xr[i], s);
+        sum += c;
+        qr[i] = (int8_t)c;
+    }
+    if (x_rowsum) {
+        sum = block_sum<BLOCK>(sum, redi);
+        if (threadIdx.x == 0) x_rowsum[m] = sum;
+    }
 }
 
 template <int BLOCK>
-hipError_t launch_block(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale, hipStream_t stream) {
+hipError_t launch_block(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale, int32_t* x_rowsum,
+                        hipStream_t stream) {
     const dim3 grid((unsigned)M), block(BLOCK);
     const int64_t K4 = K / 4;
     if (K % 4 != 0 || K4 > 16 * BLOCK) {
-        hipLaunchKernelGGL(quantize_rows_2pass<BLOCK>, grid, block, 0, stream, x, (int)K, xq, x_scale);
+        hipLaunchKernelGGL(quantize_rows_2pass<BLOCK>, grid, block, 0, stream, x, (int)K, xq, x_scale, x_rowsum);
     } else if (K4 <= BLOCK) {
-        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 1>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 1>), grid, block, 0, stream, x, (int)K, xq, x_scale, x_rowsum);
     } else if (K4 <= 2 * BLOCK) {
-        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 2>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 2>), grid, block, 0, stream, x, (int)K, xq, x_scale, x_rowsum);
     } else if (K4 <= 4 * BLOCK) {
-        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 4>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 4>), grid, block, 0, stream, x, (int)K, xq, x_scale, x_rowsum);
     } else if (K4 <= 8 * BLOCK) {
-        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 8>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 8>), grid, block, 0, stream, x, (int)K, xq, x_scale, x_rowsum);
     } else {
-        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 16>), grid, block, 0, stream, x, (int)K, xq, x_scale);
+        hipLaunchKernelGGL((quantize_rows_reg<BLOCK, 16>), grid, block, 0, stream, x, (int)K, xq, x_scale, x_rowsum);
     }
     return hipGetLastError();
 }
@@ -101,10 +138,10 @@ hipError_t launch_block(const float* x, int64_t M, int64_t K, int8_t* xq, float*
 }  // namespace
 
 hipError_t launch_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
-                               hipStream_t stream) {
+                               int32_t* x_rowsum, hipStream_t stream) {
     // Few rows: wide groups so one row is spread over many lanes.  Many rows: one 256-lane group each.
-    if (M <= 64) return launch_block<1024>(x, M, K, xq, x_scale, stream);
-    return launch_block<256>(x, M, K, xq, x_scale, stream);
+    if (M <= 64) return launch_block<1024>(x, M, K, xq, x_scale, x_rowsum, stream);
+    return launch_block<256>(x, M, K, xq, x_scale, x_rowsum, stream);
 }
 
 }  // namespace bitnet

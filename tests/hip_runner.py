@@ -20,13 +20,14 @@ def pack(W: torch.Tensor, layout="i2s"):
     return packed, w_scale
 
 
-def quantize(x: torch.Tensor):
+def quantize(x: torch.Tensor, with_rowsum=False):
     x = x.to(DEV).contiguous()
     M, K = x.shape
     xq = torch.empty((M, K), dtype=torch.int8, device=DEV)
     s = torch.empty(M, dtype=torch.float32, device=DEV)
-    B.bitnet_quantize_act(x, xq, s)
-    return xq, s
+    rs = torch.empty(M, dtype=torch.int32, device=DEV) if with_rowsum else None
+    B.bitnet_quantize_act(x, xq, s, rs)
+    return (xq, s, rs) if with_rowsum else (xq, s)
 
 
 def workspace(layout, M, N, K):
@@ -34,13 +35,13 @@ def workspace(layout, M, N, K):
     return torch.zeros(max(nbytes, 16), dtype=torch.uint8, device=DEV)
 
 
-def mpgemm(layout, packed, w_scale, N, K, xq, s, ws=None, want_acc=True):
+def mpgemm(layout, packed, w_scale, N, K, xq, s, ws=None, want_acc=True, x_rowsum=None):
     M = xq.shape[0]
     y = torch.empty((M, N), dtype=torch.float32, device=DEV)
     acc = torch.empty((M, N), dtype=torch.int32, device=DEV) if want_acc else None
     if ws is None:
         ws = workspace(layout, M, N, K)
-    B.bitnet_mpgemm(layout, packed, w_scale, N, K, xq, s, y, acc, ws)
+    B.bitnet_mpgemm(layout, packed, w_scale, N, K, xq, s, y, acc, ws, x_rowsum=x_rowsum)
     return y, acc
 
 

@@ -48,11 +48,12 @@ FAKE = 1 << 20          # aligned, never dereferenced: validation fails before a
 
 
 def _mpgemm(**kw):
-    a = dict(layout=0, packed=FAKE, packed_bytes=1 << 30, w_scale=FAKE, N=64, K=256, xq=FAKE, x_scale=FAKE, M=1,
-             y=FAKE, acc=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a = dict(layout=0, packed=FAKE, packed_bytes=1 << 30, w_scale=FAKE, N=64, K=256, xq=FAKE, x_scale=FAKE,
+             x_rowsum=None, M=1, y=FAKE, acc=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
     a.update(kw)
     return B.lib().bitnet_mpgemm(a["layout"], a["packed"], a["packed_bytes"], a["w_scale"], a["N"], a["K"], a["xq"],
-                                 a["x_scale"], a["M"], a["y"], a["acc"], a["ws"], a["ws_bytes"], a["stream"])
+                                 a["x_scale"], a["x_rowsum"], a["M"], a["y"], a["acc"], a["ws"], a["ws_bytes"],
+                                 a["stream"])
 
 
 def test_mpgemm_validation_statuses():
@@ -65,6 +66,7 @@ def test_mpgemm_validation_statuses():
     assert _mpgemm(M=0) == 2
     assert _mpgemm(xq=FAKE + 4) == 3
     assert _mpgemm(acc=FAKE + 8) == 3
+    assert _mpgemm(x_rowsum=FAKE + 2) == 3
     assert _mpgemm(packed_bytes=10) == 1
     for layout, M, N, K in ((0, 1, 64, 256 * 64), (1, 1, 64, 4096), (0, 512, 4096, 4096), (1, 512, 4096, 4096)):
         need = B.bitnet_mpgemm_workspace_bytes(layout, M, N, K)
@@ -76,10 +78,11 @@ def test_mpgemm_validation_statuses():
 
 def test_quantize_and_pack_validation_statuses():
     lib = B.lib()
-    assert lib.bitnet_quantize_act(None, 1, 64, FAKE, FAKE, None) == 1
-    assert lib.bitnet_quantize_act(FAKE, 0, 64, FAKE, FAKE, None) == 2
-    assert lib.bitnet_quantize_act(FAKE, 1, 0, FAKE, FAKE, None) == 2
-    assert lib.bitnet_quantize_act(FAKE + 4, 1, 64, FAKE, FAKE, None) == 3
+    assert lib.bitnet_quantize_act(None, 1, 64, FAKE, FAKE, None, None) == 1
+    assert lib.bitnet_quantize_act(FAKE, 0, 64, FAKE, FAKE, None, None) == 2
+    assert lib.bitnet_quantize_act(FAKE, 1, 0, FAKE, FAKE, None, None) == 2
+    assert lib.bitnet_quantize_act(FAKE + 4, 1, 64, FAKE, FAKE, None, None) == 3
+    assert lib.bitnet_quantize_act(FAKE, 1, 64, FAKE, FAKE, FAKE + 1, None) == 3
     ws = B.bitnet_pack_workspace_bytes(64, 64)
     assert lib.bitnet_pack_weights(3, FAKE, 64, 64, FAKE, 1 << 20, FAKE, FAKE, ws, None) == 4
     assert lib.bitnet_pack_weights(0, FAKE, 60, 64, FAKE, 1 << 20, FAKE, FAKE, ws, None) == 2

@@ -1,0 +1,55 @@
+"""GPU parity of bitnet_mpgemm_fused (quantise once, several products in one launch) against the oracle and
+against the separate quantise + mpGEMM calls."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2502_11880_amd as B
+from oracle import bitnet_oracle as O
+from paper_2502_11880_amd import inputs
+from tests import hip_runner as H
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(*what):
+    print("case:", *what, flush=True)
+
+
+def _fused_case(layout, M, K, Ns, seed):
+    Ws = [inputs.weight_f32(N, K, seed=seed + i) for i, N in enumerate(Ns)]
+    x = inputs.activation_f32(M, K, seed=seed + 100)
+    packs = [H.pack(W, layout) for W in Ws]
+    xd = x.to(H.DEV)
+    xq = torch.empty((M, K), dtype=torch.int8, device=H.DEV)
+    s = torch.empty(M, dtype=torch.float32, device=H.DEV)
+    rs = torch.empty(M, dtype=torch.int32, device=H.DEV)
+    ys = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
+    need = max(B.bitnet_mpgemm_workspace_bytes(layout, M, N, K) for N in Ns)
+    ws = torch.zeros(max(16, need), dtype=torch.uint8, device=H.DEV)
+    B.bitnet_mpgemm_fused(layout, [p for p, _ in packs], [b for _, b in packs], xd, xq, s, rs, ys, ws)
+    xq_ref, s_ref = O.quantize_act(x.numpy())
+    assert np.array_equal(H.to_np(xq), xq_ref)
+    assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
+    for i, (W, (p, b), y) in enumerate(zip(Ws, packs, ys)):
+        t_ref, beta_ref = O.ternarize(W.numpy())
+        acc_ref = O.mad_gemm(xq_ref, t_ref)
+        H.check_y(H.to_np(y), O.epilogue(acc_ref, beta_ref, s_ref), acc_ref)
+        y_sep, _ = H.mpgemm(layout, p, b, Ns[i], K, xq, s, x_rowsum=rs)
+        assert np.array_equal(H.to_np(y), H.to_np(y_sep))      # identical to the separate calls
+
+
+@pytest.mark.parametrize("M,K,Ns", [(1, 64, [16]), (1, 320, [16, 48, 32]), (2, 832, [64, 16]),
+                                    (1, 3200, [3200, 3200, 3200]), (1, 3200, [8640, 8640]), (1, 8640, [3200]),
+                                    (8, 4096, [4096, 1024, 1024]), (5, 1536, [208, 96, 16, 64, 32, 48, 128, 16]),
+                                    (16, 3840, [48]), (8, 14336, [64, 32]), (16, 4096, [32])])
+def test_fused_i2s(M, K, Ns):
+    _announce("fused i2s", M, K, Ns)
+    _fused_case("i2s", M, K, Ns, seed=inputs.seed_for(2, M * 7 + K + len(Ns)))
+
+
+@pytest.mark.parametrize("M,K,Ns", [(1, 448, [16, 32]), (3, 4096, [64, 48])])
+def test_fused_tl2(M, K, Ns):
+    _announce("fused tl2", M, K, Ns)
+    _fused_case("tl2", M, K, Ns, seed=inputs.seed_for(2, 99 + M + K))

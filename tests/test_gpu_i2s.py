@@ -26,10 +26,11 @@ def _announce(*what):
 def test_quantize_act_bit_exact(M, K):
     _announce("quantize", M, K)
     x = inputs.activation_f32(M, K, seed=inputs.seed_for(9, M * 7 + K))
-    xq, s = H.quantize(x)
+    xq, s, rs = H.quantize(x, with_rowsum=True)
     xq_ref, s_ref = O.quantize_act(x.numpy())
     assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
     assert np.array_equal(H.to_np(xq), xq_ref)
+    assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
 
 
 def test_quantize_act_constructed_ties_and_zero_rows():
@@ -81,19 +82,19 @@ def test_pack_beta_constructed():
 # ------------------------------------------------------------------------------------------------
 # a5 + a7: decode accumulation and epilogue
 # ------------------------------------------------------------------------------------------------
-def _path_vs_oracle(M, N, K, seed, layout="i2s", repeat=True):
+def _path_vs_oracle(M, N, K, seed, layout="i2s", repeat=True, rowsum=True):
     W = inputs.weight_f32(N, K, seed=seed)
     x = inputs.activation_f32(M, K, seed=seed + 500)
     packed, w_scale = H.pack(W, layout)
-    xq, s = H.quantize(x)
+    xq, s, rs = H.quantize(x, with_rowsum=True)
     ws = H.workspace(layout, M, N, K)
-    y, acc = H.mpgemm(layout, packed, w_scale, N, K, xq, s, ws)
+    y, acc = H.mpgemm(layout, packed, w_scale, N, K, xq, s, ws, x_rowsum=rs if rowsum else None)
     y_ref, acc_ref, xq_ref, s_ref, t_ref, beta_ref = O.mpgemm_reference(x.numpy(), W.numpy())
     acc_np = H.to_np(acc)
     assert np.array_equal(acc_np, acc_ref)
     H.check_y(H.to_np(y), y_ref, acc_ref)
-    if repeat:   # same workspace again: tickets were reset, results identical
-        y2, acc2 = H.mpgemm(layout, packed, w_scale, N, K, xq, s, ws)
+    if repeat:   # the other way to remove the code offset, same workspace: identical results
+        y2, acc2 = H.mpgemm(layout, packed, w_scale, N, K, xq, s, ws, x_rowsum=None if rowsum else rs)
         assert np.array_equal(H.to_np(acc2), acc_np)
         assert np.array_equal(H.to_np(y2), H.to_np(y))
 
@@ -101,9 +102,10 @@ def _path_vs_oracle(M, N, K, seed, layout="i2s", repeat=True):
 @pytest.mark.parametrize("M,N,K", [(1, 16, 64), (1, 32, 320), (2, 48, 832), (5, 64, 1536), (8, 208, 3200),
                                    (16, 96, 1024), (1, 1024, 4096), (3, 16, 8640), (1, 4096, 1536),
                                    (17, 64, 576), (33, 48, 448)])
-def test_i2s_mpgemm_parity(M, N, K):
-    _announce("i2s mpgemm", M, N, K)
-    _path_vs_oracle(M, N, K, seed=inputs.seed_for(7, M * 131 + N * 7 + K))
+@pytest.mark.parametrize("rowsum", [True, False])
+def test_i2s_mpgemm_parity(M, N, K, rowsum):
+    _announce("i2s mpgemm", M, N, K, rowsum)
+    _path_vs_oracle(M, N, K, seed=inputs.seed_for(7, M * 131 + N * 7 + K), rowsum=rowsum)
 
 
 def test_i2s_mpgemm_extreme_values():

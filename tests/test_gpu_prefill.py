@@ -17,12 +17,12 @@ def _announce(*what):
     print("case:", *what, flush=True)
 
 
-def _prefill_vs_oracle(M, N, K, seed, sample_rows=None, layout="i2s"):
+def _prefill_vs_oracle(M, N, K, seed, sample_rows=None, layout="i2s", rowsum=True):
     W = inputs.weight_f32(N, K, seed=seed)
     x = inputs.activation_f32(M, K, seed=seed + 500)
     packed, w_scale = H.pack(W, layout)
-    xq, s = H.quantize(x)
-    y, acc = H.mpgemm(layout, packed, w_scale, N, K, xq, s)
+    xq, s, rs = H.quantize(x, with_rowsum=True)
+    y, acc = H.mpgemm(layout, packed, w_scale, N, K, xq, s, x_rowsum=rs if rowsum else None)
     xq_ref, s_ref = O.quantize_act(x.numpy())
     t_ref, beta_ref = O.ternarize(W.numpy())
     assert np.array_equal(H.to_np(xq), xq_ref)
@@ -37,9 +37,10 @@ def _prefill_vs_oracle(M, N, K, seed, sample_rows=None, layout="i2s"):
 
 @pytest.mark.parametrize("M,N,K", [(17, 16, 64), (33, 48, 320), (64, 128, 256), (100, 208, 832), (128, 256, 1536),
                                    (129, 1040, 448), (200, 64, 3200), (256, 384, 8640), (300, 512, 4096)])
-def test_i2s_prefill_parity(M, N, K):
-    _announce("i2s prefill", M, N, K)
-    _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(4, M * 131 + N * 7 + K))
+@pytest.mark.parametrize("rowsum", [True, False])
+def test_i2s_prefill_parity(M, N, K, rowsum):
+    _announce("i2s prefill", M, N, K, rowsum)
+    _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(4, M * 131 + N * 7 + K), rowsum=rowsum)
 
 
 def test_i2s_prefill_extreme_values():
