@@ -4,14 +4,19 @@
 // MFMA-bound design for it.  (On gfx950 the 32x32x32 int8 MFMA sustains about twice the rate of the 16x16x64
 // one, so the contraction uses the former.)
 //
-// Tiles: a work group of 4 waves computes a 128-token x 128-row output tile; each wave owns 64 x 64 (2 x 2
-// MFMA tiles of 32 x 32).  K advances in 256-k stages, the I2_S block size, so the packed weights of one row
-// group and stage are one contiguous KiB.  Lane (j, h) of a wave (j = lane % 32, h = lane / 32) needs, for
-// its weight row j, the 16 codes of k-step s at k = 32 s + 16 h: these are word s/2 of the layout's lane chunk
-// q = 2 (s % 2) + h, so each lane loads two 16-byte chunks per 32-row tile per stage straight into registers
-// and unpacks them there; the weights never pass through LDS.  The int8 activation tile (128 x 256) is
-// staged in LDS with rows padded to 272 bytes.  The next stage's global loads are issued before the current
-// stage's MFMAs.
+// Operand reuse decides this kernel: per output tile the int8 activations cost 1 byte per k per token row and
+// the packed weights 1/4 byte per k per weight row, so tiles are wide along N (weights) to reuse each staged
+// activation row many times.  A work group of WM x WN waves computes a 128-token x (128*WN)-row tile; each
+// wave owns (128/WM) x 128 (MT x 4 MFMA tiles of 32 x 32, MT = 4/WM).  The widest tile uses one wave per SIMD
+// with its 256 accumulator registers in AGPRs.  K advances in 256-k stages, the I2_S block size, so the
+// packed weights of one row group and stage are one contiguous KiB.  Lane (j, h) of a wave (j = lane % 32,
+// h = lane / 32) needs, for its weight row j, the 16 codes of k-step s at k = 32 s + 16 h: word s/2 of the
+// layout's lane chunk q = 2 (s % 2) + h; each lane loads those chunks straight into registers and unpacks them
+// there, so the weights never pass through LDS.  The activation tile (128 x 256) is staged in LDS with rows
+// padded to 272 bytes, double-buffered: one barrier per stage.  Activations are loaded into registers one
+// stage ahead of their LDS store, the next stage's weight words at the start of each stage.  Tiles are
+// ordered in groups of 4 token tiles so that the work groups resident on one XCD share activation and weight
+// tiles in its L2.
 //
 // The codes are t + 1: sum_k xq[m, k] is subtracted in the epilogue, either from x_rowsum (written by the
 // quantiser) or accumulated here by the threads that stage the activation rows.
@@ -22,9 +27,9 @@ namespace {
 
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 256;
-constexpr int kThreads = 256;
+constexpr int kBM = 128, kBK = 256;
 constexpr int kARow = kBK + 16;            // padded LDS row of the activation tile
+constexpr int kGroupM = 4;                 // token tiles per scheduling group
 
 __device__ __forceinline__ int byte_sum(const v4i& v) {
     const int ones = 0x01010101;
@@ -34,63 +39,74 @@ __device__ __forceinline__ int byte_sum(const v4i& v) {
     return __builtin_amdgcn_sdot4(v.w, ones, s, false);
 }
 
-template <bool HAS_RS>
-__global__ __launch_bounds__(kThreads) void i2s_prefill_kernel(
+template <int WM, int WN, bool HAS_RS>
+__global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
     const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
     const float* __restrict__ x_scale, const int32_t* __restrict__ x_rowsum, int M, int N, int K,
     float* __restrict__ y, int32_t* __restrict__ acc_out) {
-    __shared__ __align__(16) int8_t As[kBM * kARow];
+    constexpr int kThreads = 64 * WM * WN;
+    constexpr int kBN = 128 * WN;
+    constexpr int MT = 4 / WM;                               // 32-row MFMA tiles per wave along M
+    constexpr int kChunks = kBM * (kBK / 16) / kThreads;     // 16-byte activation chunks per thread per stage
+    __shared__ __align__(16) int8_t As[2][kBM * kARow];       // double-buffered activation tile
     __shared__ int rowsum_s[kBM];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave % WM, wn = wave / WM;
     const int j32 = lane & 31, h = lane >> 5;
     const int tiles_m = (M + kBM - 1) / kBM;
+    const int tiles_n = (N + kBN - 1) / kBN;
     const int L = xcd_logical_id(blockIdx.x, gridDim.x);
-    const int tm = L % tiles_m, tn = L / tiles_m;       // neighbours share a weight tile
+    // grouped order: kGroupM token tiles x all weight tiles per group, token tile fastest
+    const int gsize = kGroupM * tiles_n;
+    const int g = L / gsize, gl = L - g * gsize;
+    const int gm = (tiles_m - g * kGroupM) < kGroupM ? (tiles_m - g * kGroupM) : kGroupM;
+    const int tm = g * kGroupM + gl % gm, tn = gl / gm;
     const int m0 = tm * kBM, n0 = tn * kBN;
     const int nkb = (K + kBK - 1) / kBK;
     const int nfull = K / kBK;
     const int nrg = N / kRowsPerGroup;
     const size_t rg_bytes = (size_t)4 * K;
 
-    // activation staging: thread -> (row, half); 8 x 16 bytes of one row per stage
-    const int a_row = tid >> 1, a_half = tid & 1;
-    const bool a_valid = m0 + a_row < M;
-    const int8_t* a_src = xq + (size_t)(a_valid ? m0 + a_row : 0) * K + 128 * a_half;
-    int8_t* a_dst = As + a_row * kARow + 128 * a_half;
-
     // weight row group and lane chunk of each 32-row tile of this wave
-    int rg[2];
-    bool rg_ok[2];
+    int rg[4];
+    bool rg_ok[4];
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-        rg[ni] = n0 / kRowsPerGroup + 4 * wn + 2 * ni + (j32 >> 4);
+    for (int ni = 0; ni < 4; ++ni) {
+        rg[ni] = n0 / kRowsPerGroup + 8 * wn + 2 * ni + (j32 >> 4);
         rg_ok[ni] = rg[ni] < nrg;
     }
     const int r16 = j32 & 15;
 
     const v4i zero4 = {0, 0, 0, 0};
-    v16i acc[2][2];
+    v16i acc[MT][4];
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < MT; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = v16i{};
-    int rs = 0;
+        for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = v16i{};
+    int rs[kChunks];
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i) rs[i] = 0;
 
-    v4i a_reg[8];
-    v4u b_next[2][2], b_cur[2][2];     // [tile][chunk: q = h, q = 2 + h]
+    v4i a_reg[kChunks];
+    v4u b_cur[4][2], b_next[4][2];     // [tile][chunk: q = h, q = 2 + h]
 
-    auto load_stage = [&](int kb) {
-        const int T = kb < nfull ? 4 : (K - nfull * kBK) / kSubK;   // 64-k sub-tiles in this stage
+    auto stage_T = [&](int kb) { return kb < nfull ? 4 : (K - nfull * kBK) / kSubK; };   // 64-k sub-tiles
+    auto load_a = [&](int kb) {
+        const int T = stage_T(kb);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int koff = 128 * a_half + 16 * i;
-            a_reg[i] = (a_valid && koff < 64 * T) ? *reinterpret_cast<const v4i*>(a_src + (size_t)kb * kBK + 16 * i)
-                                                  : zero4;
+        for (int i = 0; i < kChunks; ++i) {
+            const int c = tid + i * kThreads;
+            const int row = c >> 4, col = (c & 15) * 16;
+            a_reg[i] = (m0 + row < M && col < 64 * T)
+                           ? *reinterpret_cast<const v4i*>(xq + (size_t)(m0 + row) * K + (size_t)kb * kBK + col)
+                           : zero4;
         }
+    };
+    auto load_b = [&](int kb, v4u (&dst)[4][2]) {
+        const int T = stage_T(kb);
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
+        for (int ni = 0; ni < 4; ++ni) {
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
                 v4u w = {0u, 0u, 0u, 0u};
@@ -106,72 +122,86 @@ __global__ __launch_bounds__(kThreads) void i2s_prefill_kernel(
                         if (T > 2) w.z = pw[2];
                     }
                 }
-                b_next[ni][c] = w;
+                dst[ni][c] = w;
             }
         }
     };
-    auto store_stage = [&]() {
+    auto store_a = [&](int buf) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            *reinterpret_cast<v4i*>(a_dst + 16 * i) = a_reg[i];
-            if (!HAS_RS) rs += byte_sum(a_reg[i]);
+        for (int i = 0; i < kChunks; ++i) {
+            const int c = tid + i * kThreads;
+            *reinterpret_cast<v4i*>(As[buf] + (c >> 4) * kARow + (c & 15) * 16) = a_reg[i];
+            if (!HAS_RS) rs[i] += byte_sum(a_reg[i]);
         }
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-            for (int c = 0; c < 2; ++c) b_cur[ni][c] = b_next[ni][c];
     };
 
-    load_stage(0);
-    store_stage();
-    __syncthreads();
+    // prologue: stage 0 in LDS buffer 0 and its weights in registers; stage 1's activations in registers
+    load_a(0);
+    load_b(0, b_cur);
+    store_a(0);
+    if (nkb > 1) load_a(1);
     for (int kb = 0; kb < nkb; ++kb) {
-        const int T = kb < nfull ? 4 : (K - nfull * kBK) / kSubK;
-        if (kb + 1 < nkb) load_stage(kb + 1);
+        const int buf = kb & 1;
+        const int T = stage_T(kb);
+        __syncthreads();                                  // stage kb's tile is in As[buf]; As[buf ^ 1] is free
+        if (kb + 1 < nkb) load_b(kb + 1, b_next);
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
             if (s < 2 * T) {
-                v4i a[2];
+                v4i a[MT];
 #pragma unroll
-                for (int mi = 0; mi < 2; ++mi)
-                    a[mi] = *reinterpret_cast<const v4i*>(As + (64 * wm + 32 * mi + j32) * kARow + 32 * s + 16 * h);
+                for (int mi = 0; mi < MT; ++mi)
+                    a[mi] = *reinterpret_cast<const v4i*>(As[buf] + (32 * MT * wm + 32 * mi + j32) * kARow + 32 * s +
+                                                          16 * h);
 #pragma unroll
-                for (int ni = 0; ni < 2; ++ni) {
+                for (int ni = 0; ni < 4; ++ni) {
                     const v4i b = unpack_codes(word_of(b_cur[ni][s & 1], s >> 1));
 #pragma unroll
-                    for (int mi = 0; mi < 2; ++mi)
+                    for (int mi = 0; mi < MT; ++mi)
                         acc[mi][ni] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[mi], b, acc[mi][ni], 0, 0, 0);
                 }
             }
         }
-        __syncthreads();
         if (kb + 1 < nkb) {
-            store_stage();
-            __syncthreads();
+            store_a(buf ^ 1);                              // stage kb+1 (loaded during stage kb-1)
+            if (kb + 2 < nkb) load_a(kb + 2);
+#pragma unroll
+            for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+                for (int c = 0; c < 2; ++c) b_cur[ni][c] = b_next[ni][c];
         }
     }
 
     if (HAS_RS) {
         if (tid < kBM) rowsum_s[tid] = (m0 + tid < M) ? x_rowsum[m0 + tid] : 0;
     } else {
-        rs += __shfl_xor(rs, 1, 64);                     // the two halves of each row
-        if (a_half == 0) rowsum_s[a_row] = rs;
+        // the 16 threads of one row are 16 consecutive lanes
+#pragma unroll
+        for (int i = 0; i < kChunks; ++i) {
+            int v = rs[i];
+            v += __shfl_xor(v, 1, 64);
+            v += __shfl_xor(v, 2, 64);
+            v += __shfl_xor(v, 4, 64);
+            v += __shfl_xor(v, 8, 64);
+            const int c = tid + i * kThreads;
+            if ((c & 15) == 0) rowsum_s[c >> 4] = v;
+        }
     }
     __syncthreads();
 
     // D element v of lane (j, h): row 8 * (v / 4) + 4 * h + v % 4, column j.
     const float beta = *w_scale;
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
+    for (int mi = 0; mi < MT; ++mi) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            const int ml = 64 * wm + 32 * mi + 8 * (v >> 2) + 4 * h + (v & 3);
+            const int ml = 32 * MT * wm + 32 * mi + 8 * (v >> 2) + 4 * h + (v & 3);
             const int m = m0 + ml;
             if (m >= M) continue;
             const int rsum = rowsum_s[ml];
             const float sc = beta / x_scale[m];
 #pragma unroll
-            for (int ni = 0; ni < 2; ++ni) {
+            for (int ni = 0; ni < 4; ++ni) {
                 if (!rg_ok[ni]) continue;
                 const int n = rg[ni] * kRowsPerGroup + r16;
                 const int val = acc[mi][ni][v] - rsum;
@@ -182,19 +212,32 @@ __global__ __launch_bounds__(kThreads) void i2s_prefill_kernel(
     }
 }
 
+template <int WM, int WN>
+void launch_cfg(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
+                const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    const unsigned tiles = (unsigned)(((M + kBM - 1) / kBM) * ((N + 128 * WN - 1) / (128 * WN)));
+    if (x_rowsum)
+        hipLaunchKernelGGL((i2s_prefill_kernel<WM, WN, true>), dim3(tiles), dim3(64 * WM * WN), 0, stream, pk, w_scale,
+                           xq, x_scale, x_rowsum, M, N, K, y, acc);
+    else
+        hipLaunchKernelGGL((i2s_prefill_kernel<WM, WN, false>), dim3(tiles), dim3(64 * WM * WN), 0, stream, pk,
+                           w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc);
+}
+
 }  // namespace
 
 hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
                               const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc,
                               hipStream_t stream) {
-    const unsigned tiles = (unsigned)(((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN));
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    if (x_rowsum)
-        hipLaunchKernelGGL(i2s_prefill_kernel<true>, dim3(tiles), dim3(kThreads), 0, stream, pk, w_scale, xq, x_scale,
-                           x_rowsum, M, N, K, y, acc);
+    const long tiles_m = (M + kBM - 1) / kBM;
+    // the widest tile that still gives every CU some work
+    if (tiles_m * ((N + 511) / 512) >= 192)
+        launch_cfg<1, 4>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, stream);      // 128 x 512, 4 waves
+    else if (tiles_m * ((N + 255) / 256) >= 96)
+        launch_cfg<2, 2>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, stream);      // 128 x 256, 4 waves
     else
-        hipLaunchKernelGGL(i2s_prefill_kernel<false>, dim3(tiles), dim3(kThreads), 0, stream, pk, w_scale, xq,
-                           x_scale, x_rowsum, M, N, K, y, acc);
+        launch_cfg<2, 1>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, stream);      // 128 x 128, 2 waves
     return hipGetLastError();
 }
 
