@@ -124,8 +124,7 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
         L.y[0] = y;
         L.acc[0] = acc;
         L.N[0] = (int)N;
-        L.rg_start[0] = 0;
-        L.rg_start[1] = (int)(N / bitnet::kRowsPerGroup);
+        bitnet::seal_fused(L);
         return hip_status(bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s), "bitnet_mpgemm launch");
     }
     if (layout == BITNET_LAYOUT_I2S)
@@ -181,13 +180,12 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
             L.y[i] = y[i];
             L.acc[i] = nullptr;
             L.N[i] = (int)N[i];
-            L.rg_start[i] = (int)rgs;
             rgs += N[i] / bitnet::kRowsPerGroup;
         }
         if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
-        L.rg_start[n_linears] = (int)rgs;
+        bitnet::seal_fused(L);
         if (M == 1 && K <= bitnet::kFusedMaxK)      // one launch: quantise inside every work group
-            return hip_status(bitnet::launch_i2s_decode_quant(L, x, (int)K, xq, x_scale, x_rowsum, s),
+            return hip_status(bitnet::launch_i2s_gemv1_stream(L, x, (int)K, xq, x_scale, x_rowsum, s),
                               "bitnet_mpgemm_fused launch");
         hipError_t e = bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s);
         if (e == hipSuccess) e = bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s);

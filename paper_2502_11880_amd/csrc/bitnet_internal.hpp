@@ -78,16 +78,26 @@ struct FusedLinears {
     float* y[kMaxFused];
     int32_t* acc[kMaxFused];       // optional exact accumulators (NULL entries allowed)
     int N[kMaxFused];
-    int rg_start[kMaxFused + 1];   // first 16-row group of each weight in the launch grid
+    int rg_start[kMaxFused + 1];   // first 16-row group of each weight in the launch; INT_MAX past the last
     int count;
+    int total;                     // row groups in the launch
 };
+
+// Fill the launch totals once the first `count` entries are set.
+inline void seal_fused(FusedLinears& L) {
+    int64_t rgs = 0;
+    for (int i = 0; i < L.count; ++i) {
+        L.rg_start[i] = (int)rgs;
+        rgs += L.N[i] / kRowsPerGroup;
+    }
+    L.total = (int)rgs;
+    for (int i = L.count; i <= kMaxFused; ++i) L.rg_start[i] = i == L.count ? L.total : 0x7fffffff;
+}
 constexpr int64_t kFusedMaxK = 61440;   // single-token fused quantise+GEMV keeps the K codes in LDS
-size_t i2s_decode_quant_lds_bytes(int64_t K, int waves);
 hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                              int M, int K, hipStream_t stream);
-hipError_t launch_i2s_decode_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                                    int32_t* x_rowsum, hipStream_t stream);
-
 constexpr int kElutMaxTokens = 8;     // tokens per ELUT launch
 int tl2_elut_waves(int M);
 size_t tl2_elut_lds_bytes(int M);

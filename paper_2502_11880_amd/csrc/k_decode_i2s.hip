@@ -35,38 +35,49 @@ __device__ __forceinline__ int wave_sum(int v) {
     return v;
 }
 
-// Which weight and row group this work group serves.
-__device__ __forceinline__ void locate(const FusedLinears& L, int bid, int& li, int& rg) {
-    li = 0;
-    while (li + 1 < L.count && bid >= L.rg_start[li + 1]) ++li;
-    rg = bid - L.rg_start[li];
-}
-
-// Multiply-accumulate of one 256-k block (T sub-tiles of 64): A from `arow` (global or LDS), B words from `w`.
-template <bool HAS_RS>
-__device__ __forceinline__ void block_mac(const int8_t* arow, int kb, int T, bool a_on, const v4u& w, v4i& acc,
-                                          v4i& rowsum) {
-    const v4i zero = {0, 0, 0, 0};
-    const v4i ones = {0x01010101, 0x01010101, 0x01010101, 0x01010101};
+// Which weight the launch's row group g belongs to, and its row group within that weight.  The bounds are
+// increasing (INT_MAX past the last weight), so a compare-and-select chain over the fixed maximum finds it; for a
+// uniform g it is all scalar.
+__device__ __forceinline__ void locate(const FusedLinears& L, int g, int& li, int& rg) {
+    int l = 0, start = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        if (j < T) {
-            const v4i a = a_on ? *reinterpret_cast<const v4i*>(arow + kb * kI2sBlockK + kSubK * j) : zero;
-            acc = mfma16x16x64(a, unpack_codes(word_of(w, j)), acc);
-            if (!HAS_RS) rowsum = mfma16x16x64(a, ones, rowsum);
-        }
+    for (int i = 1; i < kMaxFused; ++i) {
+        const int st = L.rg_start[i];
+        l = g >= st ? i : l;
+        start = g >= st ? st : start;
     }
+    li = l;
+    rg = g - start;
 }
 
-// The weight words of block kb for this lane (a short last block has T words 4*T bytes apart).
-__device__ __forceinline__ v4u block_words(const uint8_t* wbase, int kb, int nfull, int T, int lane) {
-    if (kb < nfull) return load_stream16(wbase + (size_t)kb * 1024 + 16 * lane);
-    v4u w = {0u, 0u, 0u, 0u};
-    const uint32_t* p = reinterpret_cast<const uint32_t*>(wbase + (size_t)kb * 1024 + 4 * T * lane);
-    w.x = p[0];
-    if (T > 1) w.y = p[1];
-    if (T > 2) w.z = p[2];
-    return w;
+template <typename T>
+__device__ __forceinline__ T pick(const T (&a)[kMaxFused], int li) {
+    T v = a[0];
+#pragma unroll
+    for (int i = 1; i < kMaxFused; ++i) v = li == i ? a[i] : v;
+    return v;
+}
+
+// Words per lane of block kb: 4 for a full 256-k block, (K mod 256) / 64 for a short last one.
+__device__ __forceinline__ int block_T(int kb, int nfull, int Tlast) { return kb < nfull ? 4 : Tlast; }
+
+// The 16 bytes that hold this lane's words of block kb.  A full block gives lane l the words at 16 l; a short
+// block (T words per lane, 256 T bytes) gives them at 4 T l, and lanes near its end read a window moved back to
+// end inside the block, so no lane reads past the row group.  The load is unconditional (the caller clamps kb
+// to a real block), which keeps every weight load of a batch in flight together.
+__device__ __forceinline__ v4u load_block(const uint8_t* wbase, int kb, int T, int lane) {
+    const int want = 4 * T * lane;
+    const int off = want < 256 * T - 16 ? want : 256 * T - 16;
+    return load_stream16(wbase + (size_t)kb * 1024 + off);
+}
+
+// Word j of this lane's block after load_block: words are shifted by the window's move (0 for full blocks).
+__device__ __forceinline__ uint32_t block_word(const v4u& w, int j, int T, int lane) {
+    if (T == 4) return word_of(w, j);
+    const int want = 4 * T * lane;
+    const int sh = want < 256 * T - 16 ? 0 : (want - (256 * T - 16)) >> 2;
+    const int i = j + sh;
+    return i == 0 ? w.x : i == 1 ? w.y : i == 2 ? w.z : w.w;
 }
 
 template <int WAVES, int U, bool HAS_RS>
@@ -78,28 +89,60 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int li, rg;
     locate(L, xcd_logical_id(blockIdx.x, gridDim.x), li, rg);
-    const int N = L.N[li];
+    const int N = pick(L.N, li);
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int nfull = K / kI2sBlockK;
     const int Tlast = nkb > nfull ? (K - nfull * kI2sBlockK) / kSubK : 4;
     const int q = lane >> 4, r = lane & 15;
-    const bool a_on = r < M;                        // A operand: row = token r, 16 k per lane group q
-    const int8_t* arow = xq + (size_t)(a_on ? r : 0) * K + 16 * q;
-    const uint8_t* wbase = L.packed[li] + (size_t)rg * 4 * K;
+    // A operand: row = token r, 16 k per lane group q.  Rows past M repeat token 0; their D rows are not stored.
+    const int8_t* arow = xq + (size_t)(r < M ? r : 0) * K + 16 * q;
+    const uint8_t* wbase = pick(L.packed, li) + (size_t)rg * 4 * K;
     const v4i zero = {0, 0, 0, 0};
 
+    // epilogue operands first: their round trips overlap the weight stream
+    const float beta = *pick(L.w_scale, li);
+    float xs_m[4];
+    int rs_m[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        const int m = 4 * q + v;
+        xs_m[v] = m < M ? x_scale[m] : 1.0f;
+        rs_m[v] = (HAS_RS && m < M) ? x_rowsum[m] : 0;
+    }
+
     v4i acc = zero, rowsum = zero;
-    for (int kb = wave; kb < nkb; kb += WAVES * U) {
+    const v4i ones = {0x01010101, 0x01010101, 0x01010101, 0x01010101};
+    for (int kb0 = wave; kb0 < nkb; kb0 += WAVES * U) {
+        // the batch's weights, then its activation operands: all loads issued before the first MFMA
         v4u wv[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int kbu = kb + WAVES * u;
-            if (kbu < nkb) wv[u] = block_words(wbase, kbu, nfull, kbu < nfull ? 4 : Tlast, lane);
+            const int kb = min(kb0 + WAVES * u, nkb - 1);
+            wv[u] = load_block(wbase, kb, block_T(kb, nfull, Tlast), lane);
+        }
+        v4i av[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kb = min(kb0 + WAVES * u, nkb - 1);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int k = min(kb * kI2sBlockK + kSubK * j, K - kSubK);   // past a short block: any real k
+                av[u][j] = *reinterpret_cast<const v4i*>(arow + k);
+            }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int kbu = kb + WAVES * u;
-            if (kbu < nkb) block_mac<HAS_RS>(arow, kbu, kbu < nfull ? 4 : Tlast, a_on, wv[u], acc, rowsum);
+            const int kb = kb0 + WAVES * u;
+            if (kb < nkb) {
+                const int T = block_T(kb, nfull, Tlast);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (j < T) {
+                        acc = mfma16x16x64(av[u][j], unpack_codes(block_word(wv[u], j, T, lane)), acc);
+                        if (!HAS_RS) rowsum = mfma16x16x64(av[u][j], ones, rowsum);
+                    }
+                }
+            }
         }
     }
 
@@ -111,60 +154,88 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
     for (int w = 1; w < WAVES; ++w) acc += red[w][lane];
 
     // Output element v of lane l is D[row 4*(l/16) + v][col l%16]: token m = 4q + v, weight row r.
-    const float beta = *L.w_scale[li];
-    float* y = L.y[li];
-    int32_t* acc_out = L.acc[li];
+    float* y = pick(L.y, li);
+    int32_t* acc_out = pick(L.acc, li);
     const int n = rg * kRowsPerGroup + r;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
         const int m = 4 * q + v;
         if (m < M) {
-            const float sc = beta / x_scale[m];
-            const int val = HAS_RS ? acc[v] - x_rowsum[m] : acc[v];
+            const float sc = beta / xs_m[v];
+            const int val = acc[v] - rs_m[v];
             y[(size_t)m * N + n] = (float)val * sc;
             if (acc_out) acc_out[(size_t)m * N + n] = val;
         }
     }
 }
 
-// One token: quantise x (fp32 [K]) inside every work group, then the GEMV as above with A from LDS.
-// XV float4 of the row per lane (XV * 4 * 64 * WAVES >= K); U blocks per wave in one batch.
+// One token, streaming: each work group quantises the activation row once (Sec. 2.1), keeps its codes in LDS and
+// then walks the row groups g = blockIdx.x, blockIdx.x + gridDim.x, ... of the launch, one batch of WAVES * U
+// blocks at a time (a row group takes ceil(K / (256 WAVES U)) batches).  Two register sets of weight words
+// alternate: the loads of the next batch are issued before the current one is multiplied, so the weight stream
+// never waits for the arithmetic.  The last batch of a row group reduces the waves' partial sums through LDS
+// (double-buffered, one barrier) and applies the epilogue.  Every A row holds the token's codes (LDS broadcast
+// reads, no lane masking); D row 0 is the one stored.
 template <int WAVES, int U, int XV>
-__global__ __launch_bounds__(64 * WAVES) void i2s_decode_quant_kernel(FusedLinears L, const float* __restrict__ x,
+__global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinears L, const float* __restrict__ x,
                                                                       int K, int8_t* __restrict__ xq_out,
                                                                       float* __restrict__ s_out,
                                                                       int32_t* __restrict__ rs_out) {
-    extern __shared__ __align__(16) int8_t xs[];      // K codes; later reused for the wave reduction
+    extern __shared__ __align__(16) int8_t xs[];      // the K codes of the token
+    __shared__ int part[2][WAVES][16];
     __shared__ float redf[WAVES];
     __shared__ int redi[WAVES];
+    constexpr int kPerBatch = WAVES * U;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bid = xcd_logical_id(blockIdx.x, gridDim.x);
-    int li, rg;
-    locate(L, bid, li, rg);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int q = lane >> 4, r = lane & 15;
+    const int G = gridDim.x, bid = blockIdx.x;
+    const int total = L.total;
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int nfull = K / kI2sBlockK;
     const int Tlast = nkb > nfull ? (K - nfull * kI2sBlockK) / kSubK : 4;
-    const int q = lane >> 4, r = lane & 15;
-    const uint8_t* wbase = L.packed[li] + (size_t)rg * 4 * K;
-    const int K4 = K >> 2;
+    const int nb = (nkb + kPerBatch - 1) / kPerBatch;        // batches per row group
+    const int S = ((total - bid + G - 1) / G) * nb;           // this group's steps (the grid never exceeds total)
+    // lane byte offsets within a block: full blocks, and the short last block's window (see load_block)
+    const uint32_t off_full = 16u * lane;
+    const int want_tail = 4 * Tlast * lane;
+    const uint32_t off_tail = (uint32_t)min(want_tail, 256 * Tlast - 16);
+    const int sh_tail = (want_tail - (int)off_tail) >> 2;
 
-    // 1. the activation row into registers, then this wave's weights (all blocks of the first batch)
+    auto advance = [&](int& g, int& b) {
+        if (++b == nb) {
+            b = 0;
+            g += G;
+        }
+    };
+    auto issue = [&](v4u (&w)[U], int g, int b) {
+        int li, rg;
+        locate(L, g, li, rg);
+        const uint8_t* wbase = pick(L.packed, li) + (size_t)rg * 4 * K;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kb = min(b * kPerBatch + wave + WAVES * u, nkb - 1);
+            w[u] = load_stream16(wbase + (size_t)kb * 1024 + (kb < nfull ? off_full : off_tail));
+        }
+    };
+
+    // 1. the activation row into registers, the first batch of weights, then the quantisation
     const float4* x4 = reinterpret_cast<const float4*>(x);
+    const int K4 = K >> 2;
     float4 xv[XV];
 #pragma unroll
     for (int i = 0; i < XV; ++i) {
         const int e = tid + i * 64 * WAVES;
-        xv[i] = e < K4 ? x4[e] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        const float4 v = x4[e < K4 ? e : K4 - 1];
+        xv[i] = e < K4 ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     }
-    v4u wv[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int kbu = wave + WAVES * u;
-        if (kbu < nkb) wv[u] = block_words(wbase, kbu, nfull, kbu < nfull ? 4 : Tlast, lane);
-    }
+    int g_issue = bid, b_issue = 0, g_comp = bid, b_comp = 0;
+    v4u wa[U], wb[U];
+    issue(wa, g_issue, b_issue);
+    advance(g_issue, b_issue);
+    __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the quantisation arithmetic
 
-    // 2. absmax, scale, codes into LDS and their sum
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < XV; ++i)
@@ -175,13 +246,13 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_quant_kernel(FusedLinea
     amax = redf[0];
 #pragma unroll
     for (int w = 1; w < WAVES; ++w) amax = fmaxf(amax, redf[w]);
-    const float s = 127.0f / fmaxf(amax, 1e-5f);
+    const float sx = 127.0f / fmaxf(amax, 1e-5f);
     int sum = 0;
 #pragma unroll
     for (int i = 0; i < XV; ++i) {
         const int e = tid + i * 64 * WAVES;
         if (e < K4) {
-            const int c0 = q8(xv[i].x, s), c1 = q8(xv[i].y, s), c2 = q8(xv[i].z, s), c3 = q8(xv[i].w, s);
+            const int c0 = q8(xv[i].x, sx), c1 = q8(xv[i].y, sx), c2 = q8(xv[i].z, sx), c3 = q8(xv[i].w, sx);
             sum += c0 + c1 + c2 + c3;
             reinterpret_cast<uint32_t*>(xs)[e] = (uint32_t)(c0 & 0xFF) | ((uint32_t)(c1 & 0xFF) << 8) |
                                                  ((uint32_t)(c2 & 0xFF) << 16) | ((uint32_t)(c3 & 0xFF) << 24);
@@ -197,49 +268,82 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_quant_kernel(FusedLinea
         for (int e = tid; e < K4; e += 64 * WAVES)
             reinterpret_cast<uint32_t*>(xq_out)[e] = reinterpret_cast<const uint32_t*>(xs)[e];
         if (tid == 0) {
-            s_out[0] = s;
+            s_out[0] = sx;
             rs_out[0] = rowsum;
         }
     }
 
-    // 3. the GEMV: token 0 only (lanes r == 0 carry A)
-    const bool a_on = r == 0;
+    // 2. the stream
+    const v4i zero = {0, 0, 0, 0};
     const int8_t* arow = xs + 16 * q;
-    v4i acc = {0, 0, 0, 0}, unused = {0, 0, 0, 0};
-    for (int kb = wave; kb < nkb; kb += WAVES * U) {
-        if (kb != wave) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int kbu = kb + WAVES * u;
-                if (kbu < nkb) wv[u] = block_words(wbase, kbu, nfull, kbu < nfull ? 4 : Tlast, lane);
-            }
-        }
+    v4i acc = zero;
+    int par = 0;
+    auto compute = [&](const v4u (&w)[U], int g, int b) {
+        if (b == 0) acc = zero;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int kbu = kb + WAVES * u;
-            if (kbu < nkb) block_mac<true>(arow, kbu, kbu < nfull ? 4 : Tlast, a_on, wv[u], acc, unused);
-        }
-    }
-
-    __syncthreads();                  // every wave is done reading the codes: reuse the LDS
-    v4i* red = reinterpret_cast<v4i*>(xs);
-    red[wave * 64 + lane] = acc;
-    __syncthreads();
-    if (wave != 0 || q != 0) return;
+            const int kb = b * kPerBatch + wave + WAVES * u;
+            const int8_t* ab = arow + kb * kI2sBlockK;
+            if (kb < nfull) {
 #pragma unroll
-    for (int w = 1; w < WAVES; ++w) acc += red[w * 64 + lane];
-    // token 0 is D row 0: element 0 of lanes 0..15
-    const float beta = *L.w_scale[li];
-    const int n = rg * kRowsPerGroup + r;
-    const int val = acc.x - rowsum;
-    L.y[li][n] = (float)val * (beta / s);
-    if (L.acc[li]) L.acc[li][n] = val;
+                for (int j = 0; j < 4; ++j)
+                    acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(word_of(w[u], j)),
+                                       acc);
+            } else if (kb < nkb) {
+#pragma unroll
+                for (int j = 0; j < 3; ++j) {
+                    if (j < Tlast) {
+                        const int i = j + sh_tail;
+                        const uint32_t wd = i == 0 ? w[u].x : i == 1 ? w[u].y : i == 2 ? w[u].z : w[u].w;
+                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(wd), acc);
+                    }
+                }
+            }
+        }
+        if (b == nb - 1) {
+            // token 0 is D row 0: element 0 of lanes 0..15
+            if (q == 0) part[par][wave][r] = acc.x;
+            __syncthreads();
+            if (wave == 0 && q == 0) {
+                int v = 0;
+#pragma unroll
+                for (int w2 = 0; w2 < WAVES; ++w2) v += part[par][w2][r];
+                int li, rg;
+                locate(L, g, li, rg);
+                const int n = rg * kRowsPerGroup + r;
+                const int val = v - rowsum;
+                pick(L.y, li)[n] = (float)val * (*pick(L.w_scale, li) / sx);
+                int32_t* acc_out = pick(L.acc, li);
+                if (acc_out) acc_out[n] = val;
+            }
+            par ^= 1;
+        }
+    };
+    int s = 0;
+    for (; s + 2 < S; s += 2) {
+        issue(wb, g_issue, b_issue);
+        advance(g_issue, b_issue);
+        compute(wa, g_comp, b_comp);
+        advance(g_comp, b_comp);
+        issue(wa, g_issue, b_issue);
+        advance(g_issue, b_issue);
+        compute(wb, g_comp, b_comp);
+        advance(g_comp, b_comp);
+    }
+    if (s + 1 < S) {
+        issue(wb, g_issue, b_issue);
+        compute(wa, g_comp, b_comp);
+        advance(g_comp, b_comp);
+        compute(wb, g_comp, b_comp);
+    } else {
+        compute(wa, g_comp, b_comp);
+    }
 }
 
 template <int WAVES, int U>
 void launch_plain(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int M, int K,
                   hipStream_t stream) {
-    const dim3 grid((unsigned)L.rg_start[L.count]), block(64 * WAVES);
+    const dim3 grid((unsigned)L.total), block(64 * WAVES);
     if (x_rowsum)
         hipLaunchKernelGGL((i2s_decode_kernel<WAVES, U, true>), grid, block, 0, stream, L, xq, x_scale, x_rowsum, M, K);
     else
@@ -255,30 +359,47 @@ void launch_plain_u(int U, const FusedLinears& L, const int8_t* xq, const float*
     else launch_plain<WAVES, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
 }
 
-template <int WAVES, int U>
-void launch_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs, hipStream_t stream) {
-    const dim3 grid((unsigned)L.rg_start[L.count]), block(64 * WAVES);
-    const size_t lds = i2s_decode_quant_lds_bytes(K, WAVES);
-    const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
-    if (xv <= 1)
-        hipLaunchKernelGGL((i2s_decode_quant_kernel<WAVES, U, 1>), grid, block, lds, stream, L, x, K, xq, s, rs);
-    else if (xv <= 2)
-        hipLaunchKernelGGL((i2s_decode_quant_kernel<WAVES, U, 2>), grid, block, lds, stream, L, x, K, xq, s, rs);
-    else if (xv <= 4)
-        hipLaunchKernelGGL((i2s_decode_quant_kernel<WAVES, U, 4>), grid, block, lds, stream, L, x, K, xq, s, rs);
-    else if (xv <= 8)
-        hipLaunchKernelGGL((i2s_decode_quant_kernel<WAVES, U, 8>), grid, block, lds, stream, L, x, K, xq, s, rs);
-    else
-        hipLaunchKernelGGL((i2s_decode_quant_kernel<WAVES, U, 16>), grid, block, lds, stream, L, x, K, xq, s, rs);
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
 }
 
-template <int WAVES>
-void launch_quant_u(int U, const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
-                    hipStream_t stream) {
-    if (U <= 1) launch_quant<WAVES, 1>(L, x, K, xq, s, rs, stream);
-    else if (U <= 2) launch_quant<WAVES, 2>(L, x, K, xq, s, rs, stream);
-    else if (U <= 4) launch_quant<WAVES, 4>(L, x, K, xq, s, rs, stream);
-    else launch_quant<WAVES, 8>(L, x, K, xq, s, rs, stream);
+template <int WAVES, int U, int XV>
+hipError_t launch_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
+                         hipStream_t stream) {
+    auto kern = i2s_gemv1_stream_kernel<WAVES, U, XV>;
+    const size_t lds = (size_t)K;
+    // as many work groups as fit on the chip at once, balanced so that every one walks the same number of
+    // row groups (to within one)
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, reinterpret_cast<const void*>(kern), 64 * WAVES, lds) !=
+            hipSuccess || occ <= 0)
+        occ = 1;
+    const int total = L.total;
+    const int64_t max_g = (int64_t)device_cus() * occ;
+    const int64_t rounds = (total + max_g - 1) / max_g;
+    const int grid = (int)((total + rounds - 1) / rounds);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * WAVES), lds, stream, L, x, K, xq, s, rs);
+    return hipGetLastError();
+}
+
+template <int WAVES, int U>
+hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
+                            hipStream_t stream) {
+    const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
+    if (xv <= 1) return launch_stream<WAVES, U, 1>(L, x, K, xq, s, rs, stream);
+    if (xv <= 2) return launch_stream<WAVES, U, 2>(L, x, K, xq, s, rs, stream);
+    if (WAVES < 16 || xv <= 4) return launch_stream<WAVES, U, 4>(L, x, K, xq, s, rs, stream);
+    if (xv <= 8) return launch_stream<WAVES, U, 8>(L, x, K, xq, s, rs, stream);
+    return launch_stream<WAVES, U, 16>(L, x, K, xq, s, rs, stream);
 }
 
 }  // namespace
@@ -298,15 +419,10 @@ void decode_shape(int64_t groups, int64_t K, int max_u, int min_waves, int& wave
     if (u > max_u) u = max_u;
 }
 
-size_t i2s_decode_quant_lds_bytes(int64_t K, int waves) {
-    const size_t red = (size_t)waves * 64 * sizeof(v4i);
-    return (size_t)K > red ? (size_t)K : red;
-}
-
 hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                              int M, int K, hipStream_t stream) {
     int waves, u;
-    decode_shape(L.rg_start[L.count], K, 4, 4, waves, u);
+    decode_shape(L.total, K, 4, 4, waves, u);
     switch (waves) {
         case 4: launch_plain_u<4>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
         case 8: launch_plain_u<8>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
@@ -315,19 +431,25 @@ hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const floa
     return hipGetLastError();
 }
 
-hipError_t launch_i2s_decode_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                                    int32_t* x_rowsum, hipStream_t stream) {
-    // the row lives in registers: at most 16 float4 per lane
-    const int min_waves = K <= 16384 ? 4 : K <= 32768 ? 8 : 16;
-    int waves, u;
-    decode_shape(L.rg_start[L.count], K, 8, min_waves, waves, u);
-    if (waves == 16 && u > 4) u = 4;     // 16-wave groups get 128 registers per lane
-    switch (waves) {
-        case 4: launch_quant_u<4>(u, L, x, K, xq, x_scale, x_rowsum, stream); break;
-        case 8: launch_quant_u<8>(u, L, x, K, xq, x_scale, x_rowsum, stream); break;
-        default: launch_quant_u<16>(u, L, x, K, xq, x_scale, x_rowsum, stream); break;
+    const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
+    const int cus = device_cus();
+    if (L.total > 2 * cus && L.total <= 8 * cus && nkb <= 16) {
+        // every row group in flight at once: one per 4-wave work group, up to eight such groups per CU
+        const int u = (nkb + 3) / 4;
+        if (u <= 1) return launch_stream_xv<4, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+        if (u <= 2) return launch_stream_xv<4, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
+        if (u <= 3) return launch_stream_xv<4, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+        return launch_stream_xv<4, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
     }
-    return hipGetLastError();
+    // 16-wave work groups, up to four 256-k blocks per wave per batch; past two groups per CU they stream
+    constexpr int kWaves = 16;
+    const int u = (nkb + kWaves - 1) / kWaves;
+    if (u <= 1) return launch_stream_xv<kWaves, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (u <= 2) return launch_stream_xv<kWaves, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (u <= 3) return launch_stream_xv<kWaves, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+    return launch_stream_xv<kWaves, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
 }
 
 }  // namespace bitnet
