@@ -1,7 +1,8 @@
 """Benchmark of the ternary x int8 mpGEMM hot path on one MI355X.
 
 One step = one pass of the hot path over one batch of synthetic input through every linear of the
-workload, in layer order: the q/k/v group, o, the gate/up group, down.  Each group quantises its input
+workload, in layer order: the q/k/v group, o, the gate/up group, down (for a stack of layers, every layer in
+turn; the layers hold copies of one packed layer in separate HBM buffers, so every byte is streamed).  Each group quantises its input
 activation per token (int8, absmax) and multiplies it by the group's packed ternary weights with the fused
 dequantisation epilogue.  Decode (M <= 16) runs each group as one fused launch (bitnet_mpgemm_fused); the
 separate-call path (bitnet_quantize_act + one bitnet_mpgemm per weight) is timed too and reported beside
@@ -26,6 +27,7 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 MFMA, TOP/s
 ROT_BYTES = 512 << 20            # rotate through at least 2x the Infinity Cache
 DECODE_MAX_TOKENS = 16
+CPU_ROWS = 512                   # oracle timing sample per weight for stacks of layers
 METRIC = "decode GEMV weight GB/s (% HBM peak) + tokens/s; prefill int8 TOPS (% MFMA peak)"
 
 
@@ -71,7 +73,8 @@ def main():
     layout = args.layout
     linears = [(name, K, N) for name, K, N, _ in spec["linears"]]
     by_name = {name: (K, N) for name, K, N in linears}
-    if not decode:
+    n_layers = spec.get("layers", 1)
+    if not decode or n_layers > 1:
         args.steps = max(1, min(args.steps, 20))
         args.warmup = max(1, min(args.warmup, 3))
 
@@ -86,9 +89,12 @@ def main():
         packed[name], scales[name] = pk, sc
         del W
     torch.cuda.synchronize()
-    step_weight_bytes = sum(p.numel() for p in packed.values())
+    layer_weight_bytes = sum(p.numel() for p in packed.values())
+    step_weight_bytes = layer_weight_bytes * n_layers
     copies = max(1, math.ceil(ROT_BYTES / step_weight_bytes)) if decode else 1
-    rot = [packed] + [{k: v.clone() for k, v in packed.items()} for _ in range(copies - 1)]
+    # rot[c][l]: packed weights of layer l in rotating copy c (layers past the first are copies of it)
+    rot = [[packed if (c, l) == (0, 0) else {k: v.clone() for k, v in packed.items()} for l in range(n_layers)]
+           for c in range(copies)]
 
     groups = activation_groups(by_name, inputs)
     xs, xqs, sxs, rss = [], [], [], []
@@ -101,24 +107,25 @@ def main():
     ys = {n: torch.empty((M, by_name[n][1]), dtype=torch.float32, device=dev) for n in by_name}
     ws_bytes = max(B.bitnet_mpgemm_workspace_bytes(layout, M, N, K) for _, K, N in linears)
     ws = torch.zeros(max(16, ws_bytes), dtype=torch.uint8, device=dev)
-    fargs = [[B.FusedArgs([rot[c][n] for n in g], [scales[n] for n in g], [ys[n] for n in g]) for g in groups]
-             for c in range(copies)] if decode else None
+    fargs = [[[B.FusedArgs([rot[c][l][n] for n in g], [scales[n] for n in g], [ys[n] for n in g]) for g in groups]
+              for l in range(n_layers)] for c in range(copies)] if decode else None
     stream = torch.cuda.Stream()
     sptr = stream.cuda_stream
 
     def step(i, path, quantize=True):
         c = i % copies
-        for gi, g in enumerate(groups):
-            if path == "fused":
-                B.bitnet_mpgemm_fused(layout, None, None, xs[gi], xqs[gi], sxs[gi], rss[gi], None, ws, sptr,
-                                      args=fargs[c][gi])
-                continue
-            if quantize:
-                B.bitnet_quantize_act(xs[gi], xqs[gi], sxs[gi], rss[gi], sptr)
-            for n in g:
-                K, N = by_name[n]
-                B.bitnet_mpgemm(layout, rot[c][n], scales[n], N, K, xqs[gi], sxs[gi], ys[n], None, ws, sptr,
-                                x_rowsum=rss[gi])
+        for l in range(n_layers):
+            for gi, g in enumerate(groups):
+                if path == "fused":
+                    B.bitnet_mpgemm_fused(layout, None, None, xs[gi], xqs[gi], sxs[gi], rss[gi], None, ws, sptr,
+                                          args=fargs[c][l][gi])
+                    continue
+                if quantize:
+                    B.bitnet_quantize_act(xs[gi], xqs[gi], sxs[gi], rss[gi], sptr)
+                for n in g:
+                    K, N = by_name[n]
+                    B.bitnet_mpgemm(layout, rot[c][l][n], scales[n], N, K, xqs[gi], sxs[gi], ys[n], None, ws, sptr,
+                                    x_rowsum=rss[gi])
 
     def capture(fn):
         g = torch.cuda.CUDAGraph()
@@ -163,14 +170,18 @@ def main():
     if decode:
         value = step_weight_bytes / (ms_per_step * 1e-3) / 1e9
         unit = "GB/s"
-        launches = len(groups)
+        launches = len(groups) * n_layers
         grp_bytes = [sum(packed[n].numel() + 4 * M * by_name[n][1] for n in g) + 5 * M * by_name[g[0]][0] + 8 * M
                      for g in groups]
-        avg_bytes = sum(grp_bytes) / launches
+        avg_bytes = sum(grp_bytes) * n_layers / launches
         avg_launch_ms = ms_per_step / launches
         achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
-        kernel = ("i2s_decode_fused_kernel (bitnet_mpgemm_fused)" if layout == "i2s"
-                  else "bitnet_mpgemm_fused on TL2: quantiser + one ELUT launch per weight")
+        if layout != "i2s":
+            kernel = "bitnet_mpgemm_fused on TL2: quantiser + one ELUT launch per weight"
+        elif M == 1:
+            kernel = "i2s_gemv1_stream_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
+        else:
+            kernel = "bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_kernel per group"
         roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                     "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_bytes": int(avg_bytes),
@@ -208,7 +219,7 @@ def main():
         "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic",
-        "config": {"workload": spec["name"], "tokens": M, "layout": layout, "path": main_path,
+        "config": {"workload": spec["name"], "tokens": M, "layout": layout, "path": main_path, "layers": n_layers,
                    "linears": [f"{n}:{K}x{N}" for n, K, N in linears],
                    "packed_weight_bytes_per_step": step_weight_bytes, "rotating_copies": copies},
         "tokens_per_s": round(tokens_per_s, 1),
@@ -264,10 +275,16 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
     from paper_2502_11880_amd import inputs
 
     torch.set_num_threads(1)
+    n_layers = inputs.WORKLOADS[args.workload].get("layers", 1)
+    # very large layers: the first CPU_ROWS output rows of each weight stand in for all of them
+    row_cap = CPU_ROWS if n_layers > 1 else None
     ts, betas = {}, {}
+    sample_bytes = 0
     for i, (name, K, N) in enumerate(linears):
-        W = inputs.weight_f32(N, K, seed=inputs.seed_for(args.workload, i)).numpy()
+        Ns = N if row_cap is None else min(N, row_cap)
+        W = inputs.weight_f32(Ns, K, seed=inputs.seed_for(args.workload, i)).numpy()
         ts[name], betas[name] = O.ternarize(W)
+        sample_bytes += Ns * K // 4
     # prefill: a bounded sample of token rows stands in for the full M
     Mc = M if decode else min(M, 4)
     xs = [inputs.activation_f32(M, by_name[g[0]][0], seed=inputs.seed_for(args.workload, 100 + gi)).numpy()[:Mc]
@@ -284,6 +301,12 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
         if el >= args.cpu_seconds:
             break
     per_step = el / steps
+    if decode and row_cap is not None:
+        rate = sample_bytes / per_step            # packed-equivalent weight bytes per second
+        return {"value": round(rate / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": f"{steps} passes over the first {row_cap} output rows of each of the {len(linears)} "
+                          f"linears of one layer (M={M}) in {el:.1f} s; numpy int64 matmul, one thread",
+                "tokens_per_s": round(M * rate / step_weight_bytes, 6)}
     if decode:
         return {"value": round(step_weight_bytes / per_step / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                 "sample": f"{steps} full steps of the same workload (all {len(linears)} linears, M={M}) in {el:.1f} s; "
