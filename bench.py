@@ -182,8 +182,11 @@ def main():
             kernel = "i2s_gemv1_stream_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
         else:
             kernel = "bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_kernel per group"
+        default_workload = (args.workload, M, layout) == (1, 1, "i2s")
+        traffic = measured_traffic() if default_workload else None
         roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                    "traffic_unit": "bytes per launch (FETCH_SIZE x copy factor + WRITE_SIZE)" if traffic else None,
                     "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_bytes": int(avg_bytes),
                     "launches_per_step": launches}
     else:
@@ -232,6 +235,30 @@ def main():
         "parity": parity,
     }
     print(json.dumps(out), flush=True)
+
+
+TRAFFIC_PROFILE = "profiles/decode_i2s_bitnet3b_m1_hbm_traffic.md"
+TRAFFIC_SOURCES = ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")
+
+
+def measured_traffic():
+    """HBM bytes per launch of the default decode workload from the committed counter summary, or None when
+    the kernel sources no longer hash to the ones the counters were taken on."""
+    import hashlib
+    import os
+
+    root = os.path.dirname(os.path.abspath(__file__))
+    try:
+        text = open(os.path.join(root, TRAFFIC_PROFILE)).read()
+        h = hashlib.sha256()
+        for f in TRAFFIC_SOURCES:
+            h.update(open(os.path.join(root, f), "rb").read())
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines() if line.count(": ") == 1 and " " not in line.split(": ")[0])
+    if fields.get("source_sha256", "").strip() != h.hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
 
 
 def parity_spot_check(args, layout, M, linears, packed, scales, xs, dev):

@@ -49,6 +49,16 @@ def test_fused_i2s(M, K, Ns):
     _fused_case("i2s", M, K, Ns, seed=inputs.seed_for(2, M * 7 + K + len(Ns)))
 
 
+# One token at sizes that reach every launch configuration of the streaming single-token kernel on a 256-CU
+# MI355X: 2900 row groups (several row groups per work group, both ping-pong tails, a 64-k last block);
+# K = 16448 (two weight batches per row group, two row groups per work group); K = 33024 (three batches,
+# the widest activation register set).
+@pytest.mark.parametrize("K,Ns", [(1088, [16000, 16000, 14400]), (16448, [4800]), (33024, [2400])])
+def test_fused_i2s_streaming(K, Ns):
+    _announce("fused i2s streaming", 1, K, Ns)
+    _fused_case("i2s", 1, K, Ns, seed=inputs.seed_for(2, 500 + K))
+
+
 @pytest.mark.parametrize("M,K,Ns", [(1, 448, [16, 32]), (3, 4096, [64, 48])])
 def test_fused_tl2(M, K, Ns):
     _announce("fused tl2", M, K, Ns)
