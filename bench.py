@@ -241,6 +241,12 @@ TRAFFIC_PROFILE = "profiles/decode_i2s_bitnet3b_m1_hbm_traffic.md"
 TRAFFIC_SOURCES = ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")
 
 
+def code_only(text):
+    """Source text without // comments, trailing blanks and empty lines (comment edits keep the hash)."""
+    lines = (line.split("//", 1)[0].rstrip() for line in text.splitlines())
+    return "\n".join(line for line in lines if line)
+
+
 def measured_traffic():
     """HBM bytes per launch of the default decode workload from the committed counter summary, or None when
     the kernel sources no longer hash to the ones the counters were taken on."""
@@ -252,7 +258,7 @@ def measured_traffic():
         text = open(os.path.join(root, TRAFFIC_PROFILE)).read()
         h = hashlib.sha256()
         for f in TRAFFIC_SOURCES:
-            h.update(open(os.path.join(root, f), "rb").read())
+            h.update(code_only(open(os.path.join(root, f)).read()).encode())
     except OSError:
         return None
     fields = dict(line.split(": ", 1) for line in text.splitlines() if line.count(": ") == 1 and " " not in line.split(": ")[0])

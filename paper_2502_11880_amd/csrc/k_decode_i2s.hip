@@ -5,21 +5,23 @@
 // contiguous KiB per wave per 256-k block.  A 32-bit word of lane (r, q) holds 16 codes c = t + 1 of
 // row r; shifting by 2f and masking 0x03030303 gives the four int8 codes of k = 4f .. 4f+3, which is
 // exactly the byte order of the matching activation word.  So the unpacked word feeds the B operand of
-// v_mfma_i32_16x16x64_i8 directly (B column = weight row, A row = token; tokens beyond M are zero).
-// The codes carry a +1 offset, removed by subtracting sum_k xq[m, k]: read from x_rowsum (written by the
-// quantiser) when given, otherwise taken with a second MFMA against an all-ones B over the same k.
+// v_mfma_i32_16x16x64_i8 directly (B column = weight row, A row = token; rows past the tokens repeat a
+// real token and are not stored).  The codes carry a +1 offset, removed by subtracting sum_k xq[m, k]:
+// read from x_rowsum (written by the quantiser) when given, otherwise taken with a second MFMA against an
+// all-ones B over the same k.
 //
-// Work split: one work group per 16-row group, holding the whole K.  Its 4, 8 or 16 waves take every
-// WAVES-th 256-k block, issue their weight loads U blocks at a time (a GEMV of a few MB is latency-bound:
-// one DRAM round trip should cover it) and reduce through LDS; wave 0 applies the epilogue.  No work group
-// depends on another, so no device-wide fence is needed (an agent-scope release writes back the whole L2
-// of the XCD, which costs more than these GEMVs).  One launch may cover several weights that share the
-// activation (the grid concatenates their row groups).
+// Every weight load of a batch is issued before the first of them is used, as one unconditional 16-byte
+// load per lane; a conditional load shape (the short last block) would make the compiler wait for each load
+// before issuing the next.  One launch may cover several weights that share the activation (the row groups
+// of the weights are concatenated).  No work group depends on another, so no device-wide fence is needed (an
+// agent-scope release writes back the whole L2 of the XCD, which costs more than these GEMVs).
 //
-// Single-token fused variant: the work group also quantises the activation row itself (Sec. 2.1): it loads
-// the fp32 row into registers before issuing its weight loads, reduces the absmax through LDS, and writes
-// the codes to LDS, where the MFMA A operands are read; the sum of the codes replaces x_rowsum.  The weight
-// loads stay in flight during all of this.
+// i2s_decode_kernel (tokens already quantised): one work group per 16-row group holding the whole K; its 4,
+// 8 or 16 waves take every WAVES-th 256-k block and reduce through LDS.
+//
+// i2s_gemv1_stream_kernel (one token, quantiser fused, Sec. 2.1): each work group quantises the fp32 row
+// once into LDS codes and then streams row groups, keeping the next batch of weight loads in flight while it
+// multiplies the current one.
 #include "bitnet_internal.hpp"
 
 namespace bitnet {
