@@ -24,6 +24,8 @@
 // multiplies the current one.
 #include "bitnet_internal.hpp"
 
+#include <type_traits>
+
 namespace bitnet {
 namespace {
 
@@ -205,14 +207,17 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
     const uint32_t off_tail = (uint32_t)min(want_tail, 256 * Tlast - 16);
     const int sh_tail = (want_tail - (int)off_tail) >> 2;
 
-    auto advance = [&](int& g, int& b) {
-        if (++b == nb) {
-            b = 0;
-            g += G;
-        }
+    // step s = batch s % nb of row group bid + (s / nb) G
+    auto step_gb = [&](int st, int& g, int& b) {
+        const int gi = nb == 1 ? st : st / nb;
+        b = st - gi * nb;
+        g = bid + gi * G;
     };
-    auto issue = [&](v4u (&w)[U], int g, int b) {
-        int li, rg;
+    // the loads of one step: the batch's weight words, then the weight's scale (loaded with every batch, so
+    // the epilogue never waits on a load issued after it)
+    auto issue = [&](v4u (&w)[U], float& bw, int st) {
+        int g, b, li, rg;
+        step_gb(st, g, b);
         locate(L, g, li, rg);
         const uint8_t* wbase = pick(L.packed, li) + (size_t)rg * 4 * K;
 #pragma unroll
@@ -220,126 +225,141 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
             const int kb = min(b * kPerBatch + wave + WAVES * u, nkb - 1);
             w[u] = load_stream16(wbase + (size_t)kb * 1024 + (kb < nfull ? off_full : off_tail));
         }
+        bw = *pick(L.w_scale, li);
     };
 
-    // 1. the activation row into registers, the first batch of weights, then the quantisation
-    const float4* x4 = reinterpret_cast<const float4*>(x);
-    const int K4 = K >> 2;
-    float4 xv[XV];
-#pragma unroll
-    for (int i = 0; i < XV; ++i) {
-        const int e = tid + i * 64 * WAVES;
-        const float4 v = x4[e < K4 ? e : K4 - 1];
-        xv[i] = e < K4 ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    }
-    int g_issue = bid, b_issue = 0, g_comp = bid, b_comp = 0;
-    v4u wa[U], wb[U];
-    issue(wa, g_issue, b_issue);
-    advance(g_issue, b_issue);
-    __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the quantisation arithmetic
-
-    float amax = 0.0f;
-#pragma unroll
-    for (int i = 0; i < XV; ++i)
-        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(xv[i].x), fabsf(xv[i].y)), fmaxf(fabsf(xv[i].z), fabsf(xv[i].w))));
-    amax = wave_max(amax);
-    if (lane == 0) redf[wave] = amax;
-    __syncthreads();
-    amax = redf[0];
-#pragma unroll
-    for (int w = 1; w < WAVES; ++w) amax = fmaxf(amax, redf[w]);
-    const float sx = 127.0f / fmaxf(amax, 1e-5f);
-    int sum = 0;
-#pragma unroll
-    for (int i = 0; i < XV; ++i) {
-        const int e = tid + i * 64 * WAVES;
-        if (e < K4) {
-            const int c0 = q8(xv[i].x, sx), c1 = q8(xv[i].y, sx), c2 = q8(xv[i].z, sx), c3 = q8(xv[i].w, sx);
-            sum += c0 + c1 + c2 + c3;
-            reinterpret_cast<uint32_t*>(xs)[e] = (uint32_t)(c0 & 0xFF) | ((uint32_t)(c1 & 0xFF) << 8) |
-                                                 ((uint32_t)(c2 & 0xFF) << 16) | ((uint32_t)(c3 & 0xFF) << 24);
+    // The rest is instantiated twice, for work groups with one step and with several, so that neither path
+    // joins the other: a join between paths with different numbers of loads in flight makes the compiler wait
+    // for all of them.
+    auto run = [&](auto multi) {
+        constexpr bool kMulti = decltype(multi)::value;
+        // 1. the activation row into registers, the first batch of weights, then the quantisation
+        const float4* x4 = reinterpret_cast<const float4*>(x);
+        const int K4 = K >> 2;
+        float4 xv[XV];
+    #pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * 64 * WAVES;
+            const float4 v = x4[e < K4 ? e : K4 - 1];
+            xv[i] = e < K4 ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         }
-    }
-    sum = wave_sum(sum);
-    if (lane == 0) redi[wave] = sum;
-    __syncthreads();
-    int rowsum = 0;
-#pragma unroll
-    for (int w = 0; w < WAVES; ++w) rowsum += redi[w];
-    if (bid == 0) {
-        for (int e = tid; e < K4; e += 64 * WAVES)
-            reinterpret_cast<uint32_t*>(xq_out)[e] = reinterpret_cast<const uint32_t*>(xs)[e];
-        if (tid == 0) {
-            s_out[0] = sx;
-            rs_out[0] = rowsum;
-        }
-    }
+        // two batches in flight before the quantisation (steps 0 and 1), or one when there is only one step
+        v4u wa[U], wb[U];
+        float ba = 0.0f, bb = 0.0f;
+        issue(wa, ba, 0);
+        if constexpr (kMulti) issue(wb, bb, 1);
+        __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the quantisation arithmetic
 
-    // 2. the stream
-    const v4i zero = {0, 0, 0, 0};
-    const int8_t* arow = xs + 16 * q;
-    v4i acc = zero;
-    int par = 0;
-    auto compute = [&](const v4u (&w)[U], int g, int b) {
-        if (b == 0) acc = zero;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int kb = b * kPerBatch + wave + WAVES * u;
-            const int8_t* ab = arow + kb * kI2sBlockK;
-            if (kb < nfull) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(word_of(w[u], j)),
-                                       acc);
-            } else if (kb < nkb) {
-#pragma unroll
-                for (int j = 0; j < 3; ++j) {
-                    if (j < Tlast) {
-                        const int i = j + sh_tail;
-                        const uint32_t wd = i == 0 ? w[u].x : i == 1 ? w[u].y : i == 2 ? w[u].z : w[u].w;
-                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(wd), acc);
+        float amax = 0.0f;
+    #pragma unroll
+        for (int i = 0; i < XV; ++i)
+            amax = fmaxf(amax, fmaxf(fmaxf(fabsf(xv[i].x), fabsf(xv[i].y)), fmaxf(fabsf(xv[i].z), fabsf(xv[i].w))));
+        amax = wave_max(amax);
+        if (lane == 0) redf[wave] = amax;
+        __syncthreads();
+        amax = redf[0];
+    #pragma unroll
+        for (int w = 1; w < WAVES; ++w) amax = fmaxf(amax, redf[w]);
+        const float sx = 127.0f / fmaxf(amax, 1e-5f);
+        int sum = 0;
+    #pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * 64 * WAVES;
+            if (e < K4) {
+                const int c0 = q8(xv[i].x, sx), c1 = q8(xv[i].y, sx), c2 = q8(xv[i].z, sx), c3 = q8(xv[i].w, sx);
+                sum += c0 + c1 + c2 + c3;
+                reinterpret_cast<uint32_t*>(xs)[e] = (uint32_t)(c0 & 0xFF) | ((uint32_t)(c1 & 0xFF) << 8) |
+                                                     ((uint32_t)(c2 & 0xFF) << 16) | ((uint32_t)(c3 & 0xFF) << 24);
+            }
+        }
+        sum = wave_sum(sum);
+        if (lane == 0) redi[wave] = sum;
+        __syncthreads();
+        int rowsum = 0;
+    #pragma unroll
+        for (int w = 0; w < WAVES; ++w) rowsum += redi[w];
+        if (bid == 0) {
+            for (int e = tid; e < K4; e += 64 * WAVES)
+                reinterpret_cast<uint32_t*>(xq_out)[e] = reinterpret_cast<const uint32_t*>(xs)[e];
+            if (tid == 0) {
+                s_out[0] = sx;
+                rs_out[0] = rowsum;
+            }
+        }
+
+        // 2. the stream
+        const v4i zero = {0, 0, 0, 0};
+        const int8_t* arow = xs + 16 * q;
+        v4i acc = zero;
+        int par = 0;
+        auto compute = [&](const v4u (&w)[U], float bw, int st) {
+            int g, b;
+            step_gb(st, g, b);
+            if (b == 0) acc = zero;
+    #pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int kb = b * kPerBatch + wave + WAVES * u;
+                const int8_t* ab = arow + kb * kI2sBlockK;
+                if (kb < nfull) {
+    #pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(word_of(w[u], j)),
+                                           acc);
+                } else if (kb < nkb) {
+    #pragma unroll
+                    for (int j = 0; j < 3; ++j) {
+                        if (j < Tlast) {
+                            const int i = j + sh_tail;
+                            const uint32_t wd = i == 0 ? w[u].x : i == 1 ? w[u].y : i == 2 ? w[u].z : w[u].w;
+                            acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(wd), acc);
+                        }
                     }
                 }
             }
-        }
-        if (b == nb - 1) {
-            // token 0 is D row 0: element 0 of lanes 0..15
-            if (q == 0) part[par][wave][r] = acc.x;
-            __syncthreads();
-            if (wave == 0 && q == 0) {
-                int v = 0;
-#pragma unroll
-                for (int w2 = 0; w2 < WAVES; ++w2) v += part[par][w2][r];
-                int li, rg;
-                locate(L, g, li, rg);
-                const int n = rg * kRowsPerGroup + r;
-                const int val = v - rowsum;
-                pick(L.y, li)[n] = (float)val * (*pick(L.w_scale, li) / sx);
-                int32_t* acc_out = pick(L.acc, li);
-                if (acc_out) acc_out[n] = val;
+            if (b == nb - 1) {
+                // token 0 is D row 0: element 0 of lanes 0..15
+                if (q == 0) part[par][wave][r] = acc.x;
+                __syncthreads();
+                if (wave == 0 && q == 0) {
+                    int v = 0;
+    #pragma unroll
+                    for (int w2 = 0; w2 < WAVES; ++w2) v += part[par][w2][r];
+                    int li, rg;
+                    locate(L, g, li, rg);
+                    const int n = rg * kRowsPerGroup + r;
+                    const int val = v - rowsum;
+                    pick(L.y, li)[n] = (float)val * (bw / sx);
+                    int32_t* acc_out = pick(L.acc, li);
+                    if (acc_out) acc_out[n] = val;
+                }
+                par ^= 1;
             }
-            par ^= 1;
+        };
+        // steps st and st + 1 are in flight; each register set is refilled right after it is multiplied.  The last
+        // two or three steps are peeled so that no load is issued past the last step.
+        if constexpr (!kMulti) {
+            compute(wa, ba, 0);
+            return;
+        }
+        int st = 0;
+        for (; st + 3 < S; st += 2) {
+            compute(wa, ba, st);
+            issue(wa, ba, st + 2);
+            compute(wb, bb, st + 1);
+            issue(wb, bb, st + 3);
+        }
+        if (st + 2 < S) {
+            compute(wa, ba, st);
+            issue(wa, ba, st + 2);
+            compute(wb, bb, st + 1);
+            compute(wa, ba, st + 2);
+        } else {
+            compute(wa, ba, st);
+            compute(wb, bb, st + 1);
         }
     };
-    int s = 0;
-    for (; s + 2 < S; s += 2) {
-        issue(wb, g_issue, b_issue);
-        advance(g_issue, b_issue);
-        compute(wa, g_comp, b_comp);
-        advance(g_comp, b_comp);
-        issue(wa, g_issue, b_issue);
-        advance(g_issue, b_issue);
-        compute(wb, g_comp, b_comp);
-        advance(g_comp, b_comp);
-    }
-    if (s + 1 < S) {
-        issue(wb, g_issue, b_issue);
-        compute(wa, g_comp, b_comp);
-        advance(g_comp, b_comp);
-        compute(wb, g_comp, b_comp);
-    } else {
-        compute(wa, g_comp, b_comp);
-    }
+    if (S == 1) run(std::false_type{});
+    else run(std::true_type{});
 }
 
 template <int WAVES, int U>
@@ -445,9 +465,11 @@ hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K,
         if (u <= 3) return launch_stream_xv<4, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
         return launch_stream_xv<4, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
     }
-    // 16-wave work groups, up to four 256-k blocks per wave per batch; past two groups per CU they stream
+    // 16-wave work groups, up to four 256-k blocks per wave per batch, the batches of a row group balanced;
+    // past what fits on the chip at once the work groups stream
     constexpr int kWaves = 16;
-    const int u = (nkb + kWaves - 1) / kWaves;
+    const int nb = (nkb + 4 * kWaves - 1) / (4 * kWaves);
+    const int u = (nkb + kWaves * nb - 1) / (kWaves * nb);
     if (u <= 1) return launch_stream_xv<kWaves, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
     if (u <= 2) return launch_stream_xv<kWaves, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
     if (u <= 3) return launch_stream_xv<kWaves, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
