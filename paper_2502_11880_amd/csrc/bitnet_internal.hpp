@@ -34,6 +34,50 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
+// Reductions over the 64 lanes of a wave, the result in every lane: DPP steps inside each row of 16 lanes
+// (swap neighbours, swap pairs, rotate the row by 4 and by 8), then the four row results read as scalars.
+__device__ __forceinline__ int dpp_row_step(int v, int ctrl_sel) {
+    switch (ctrl_sel) {
+        case 0: return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1, 0, 3, 2]
+        case 1: return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2, 3, 0, 1]
+        case 2: return __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false);  // row_ror:4
+        default: return __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false); // row_ror:8
+    }
+}
+
+__device__ __forceinline__ float wave_max_all(float v) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v = fmaxf(v, __int_as_float(dpp_row_step(__float_as_int(v), i)));
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
+__device__ __forceinline__ int wave_sum_all(int v) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v += dpp_row_step(v, i);
+    return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) + __builtin_amdgcn_readlane(v, 32) +
+           __builtin_amdgcn_readlane(v, 48);
+}
+
+// int8 codes of four activations, packed little-endian: clamp(rint(fp32(x * s)), -128, 127) (Sec. 2.1).
+// rint gives an integer-valued float; + 128 is exact; v_cvt_pk_u8_f32 then converts it exactly (saturating
+// to [0, 255], which is the clamp) into its byte, and XOR 0x80 turns the offset byte into two's complement.
+__device__ __forceinline__ uint32_t quant4(float4 v, float s) {
+    uint32_t p = __builtin_amdgcn_cvt_pk_u8_f32(rintf(v.x * s) + 128.0f, 0, 0u);
+    p = __builtin_amdgcn_cvt_pk_u8_f32(rintf(v.y * s) + 128.0f, 1, p);
+    p = __builtin_amdgcn_cvt_pk_u8_f32(rintf(v.z * s) + 128.0f, 2, p);
+    p = __builtin_amdgcn_cvt_pk_u8_f32(rintf(v.w * s) + 128.0f, 3, p);
+    return p ^ 0x80808080u;
+}
+
+// sum of the four signed bytes of a word, added to acc
+__device__ __forceinline__ int byte_sum4(uint32_t w, int acc) {
+    return __builtin_amdgcn_sdot4((int)w, 0x01010101, acc, false);
+}
+
 // The four int8 codes of k = 4f .. 4f+3 sit in field f (bits 2f, 2f+1) of the four bytes of an I2_S word.
 __device__ __forceinline__ v4i unpack_codes(uint32_t w) {
     v4i b;

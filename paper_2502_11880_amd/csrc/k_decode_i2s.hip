@@ -254,7 +254,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
     #pragma unroll
         for (int i = 0; i < XV; ++i)
             amax = fmaxf(amax, fmaxf(fmaxf(fabsf(xv[i].x), fabsf(xv[i].y)), fmaxf(fabsf(xv[i].z), fabsf(xv[i].w))));
-        amax = wave_max(amax);
+        amax = wave_max_all(amax);
         if (lane == 0) redf[wave] = amax;
         __syncthreads();
         amax = redf[0];
@@ -266,26 +266,20 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
         for (int i = 0; i < XV; ++i) {
             const int e = tid + i * 64 * WAVES;
             if (e < K4) {
-                const int c0 = q8(xv[i].x, sx), c1 = q8(xv[i].y, sx), c2 = q8(xv[i].z, sx), c3 = q8(xv[i].w, sx);
-                sum += c0 + c1 + c2 + c3;
-                reinterpret_cast<uint32_t*>(xs)[e] = (uint32_t)(c0 & 0xFF) | ((uint32_t)(c1 & 0xFF) << 8) |
-                                                     ((uint32_t)(c2 & 0xFF) << 16) | ((uint32_t)(c3 & 0xFF) << 24);
+                const uint32_t c = quant4(xv[i], sx);
+                sum = byte_sum4(c, sum);
+                reinterpret_cast<uint32_t*>(xs)[e] = c;
+                if (bid == 0) reinterpret_cast<uint32_t*>(xq_out)[e] = c;
             }
         }
-        sum = wave_sum(sum);
+        // Codes 4e .. 4e+3 (e = tid + 64 WAVES i) lie in block e / 64, and e / 64 = wave (mod WAVES): every
+        // wave quantised exactly the blocks it multiplies, so no barrier is needed before the stream.  The
+        // waves' code sums meet in the first epilogue, which follows a barrier.
+        sum = wave_sum_all(sum);
         if (lane == 0) redi[wave] = sum;
-        __syncthreads();
+        if (bid == 0 && tid == 0) s_out[0] = sx;
         int rowsum = 0;
-    #pragma unroll
-        for (int w = 0; w < WAVES; ++w) rowsum += redi[w];
-        if (bid == 0) {
-            for (int e = tid; e < K4; e += 64 * WAVES)
-                reinterpret_cast<uint32_t*>(xq_out)[e] = reinterpret_cast<const uint32_t*>(xs)[e];
-            if (tid == 0) {
-                s_out[0] = sx;
-                rs_out[0] = rowsum;
-            }
-        }
+        bool rowsum_ready = false;
 
         // 2. the stream
         const v4i zero = {0, 0, 0, 0};
@@ -320,6 +314,11 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
                 // token 0 is D row 0: element 0 of lanes 0..15
                 if (q == 0) part[par][wave][r] = acc.x;
                 __syncthreads();
+                if (!rowsum_ready) {         // past a barrier: every wave's code sum is in LDS
+                    rowsum_ready = true;
+                    for (int w2 = 0; w2 < WAVES; ++w2) rowsum += redi[w2];
+                    if (bid == 0 && tid == 0) rs_out[0] = rowsum;
+                }
                 if (wave == 0 && q == 0) {
                     int v = 0;
     #pragma unroll
