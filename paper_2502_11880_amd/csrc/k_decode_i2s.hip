@@ -173,6 +173,197 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
     }
 }
 
+// Up to 16 tokens, already quantised, streaming (every wave's blocks of a row group fit one batch: K <= 256 U
+// WAVES).  Each wave copies the codes of its own k-blocks, all tokens, into LDS once (rows of K + 16 bytes, so
+// the 16 token rows of one MFMA operand fall in different banks); they are the MFMA A operands (row = token;
+// rows past M repeat token 0 and are not stored) of every row group it multiplies, and no other wave reads
+// them.  The work group then walks row groups as the single-token kernel does, two batches of weights in flight.
+template <int WAVES, int U, int MG, bool HAS_RS>
+__global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLinears L, const int8_t* __restrict__ xq,
+                                                                       const float* __restrict__ x_scale,
+                                                                       const int32_t* __restrict__ x_rowsum, int M,
+                                                                       int K) {
+    extern __shared__ __align__(16) int8_t xs[];      // M rows of K + 16 codes
+    __shared__ v4i part[2][WAVES][64];
+    __shared__ int tsum[WAVES][16];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int q = lane >> 4, r = lane & 15;
+    const int G = gridDim.x, bid = blockIdx.x;
+    const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
+    const int nfull = K / kI2sBlockK;
+    const int Tlast = nkb > nfull ? (K - nfull * kI2sBlockK) / kSubK : 4;
+    const int S = (L.total - bid + G - 1) / G;                // row groups of this work group, one batch each
+    const int stride = K + 16;
+    const uint32_t off_full = 16u * lane;
+    const int want_tail = 4 * Tlast * lane;
+    const uint32_t off_tail = (uint32_t)min(want_tail, 256 * Tlast - 16);
+    const int sh_tail = (want_tail - (int)off_tail) >> 2;
+
+    auto issue = [&](v4u (&w)[U], float& bw, int st) {
+        int li, rg;
+        locate(L, bid + st * G, li, rg);
+        const uint8_t* wbase = pick(L.packed, li) + (size_t)rg * 4 * K;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kb = min(wave + WAVES * u, nkb - 1);
+            w[u] = load_stream16(wbase + (size_t)kb * 1024 + (kb < nfull ? off_full : off_tail));
+        }
+        bw = *pick(L.w_scale, li);
+    };
+
+    // 1. this wave's blocks of every token, into LDS: one 16-byte chunk per lane, four token rows per load
+    //    (loads clamped to real addresses, stores only where the chunk is real)
+    constexpr int kMaxGroups = MG;                             // token groups of 4 (M <= 4 MG)
+    v4i ast[U][kMaxGroups];
+    const int c16 = lane & 15;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mg = 0; mg < kMaxGroups; ++mg) {
+            const int m = min(4 * mg + (lane >> 4), M - 1);
+            const int k = min((wave + WAVES * u) * kI2sBlockK + 16 * c16, K - 16);
+            ast[u][mg] = *reinterpret_cast<const v4i*>(xq + (size_t)m * K + k);
+        }
+    // epilogue operands of tokens m = 4q + v
+    float xs_m[4];
+    int rs_m[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        const int m = 4 * q + v;
+        xs_m[v] = m < M ? x_scale[m] : 1.0f;
+        rs_m[v] = (HAS_RS && m < M) ? x_rowsum[m] : 0;
+    }
+    // the copy into LDS (after the first weight loads are issued) and, without x_rowsum, each token's code sum
+    // over this wave's blocks: lanes of one row of 16 hold one token, reduced with DPP
+    auto stage = [&]() {
+        int tp[kMaxGroups];
+#pragma unroll
+        for (int mg = 0; mg < kMaxGroups; ++mg) tp[mg] = 0;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int mg = 0; mg < kMaxGroups; ++mg) {
+                const int m = 4 * mg + (lane >> 4);
+                const int k = (wave + WAVES * u) * kI2sBlockK + 16 * c16;
+                if (m < M && k < K) {
+                    *reinterpret_cast<v4i*>(xs + m * stride + k) = ast[u][mg];
+                    if (!HAS_RS) {
+                        const v4i a4 = ast[u][mg];
+                        tp[mg] = byte_sum4((uint32_t)a4.x, byte_sum4((uint32_t)a4.y,
+                                                                    byte_sum4((uint32_t)a4.z,
+                                                                              byte_sum4((uint32_t)a4.w, tp[mg]))));
+                    }
+                }
+            }
+        if (!HAS_RS) {
+#pragma unroll
+            for (int mg = 0; mg < kMaxGroups; ++mg) {
+                int t = tp[mg];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) t += dpp_row_step(t, i);      // sum over the 16 lanes of the row
+                if (c16 == 0 && 4 * mg + (lane >> 4) < 16) tsum[wave][4 * mg + (lane >> 4)] = t;
+            }
+        }
+    };
+
+    const v4i zero = {0, 0, 0, 0};
+    const int8_t* arow = xs + (r < M ? r : 0) * stride + 16 * q;
+    int par = 0;
+    bool rs_ready = HAS_RS;
+    auto compute = [&](const v4u (&w)[U], float bw, int st) {
+        v4i acc = zero;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kb = wave + WAVES * u;
+            const int8_t* ab = arow + kb * kI2sBlockK;
+            if (kb < nfull) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(word_of(w[u], j)),
+                                       acc);
+            } else if (kb < nkb) {
+#pragma unroll
+                for (int j = 0; j < 3; ++j) {
+                    if (j < Tlast) {
+                        const int i = j + sh_tail;
+                        const uint32_t wd = i == 0 ? w[u].x : i == 1 ? w[u].y : i == 2 ? w[u].z : w[u].w;
+                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(wd), acc);
+                    }
+                }
+            }
+        }
+        part[par][wave][lane] = acc;
+        __syncthreads();
+        if (!rs_ready) {                 // past a barrier: the waves' code sums are in LDS
+            rs_ready = true;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                int t = 0;
+                for (int w2 = 0; w2 < WAVES; ++w2) t += tsum[w2][(4 * q + v) & 15];
+                rs_m[v] = t;
+            }
+        }
+        if (wave == 0 && 4 * q < M) {
+            v4i tot = part[par][0][lane];
+#pragma unroll 4
+            for (int w2 = 1; w2 < WAVES; ++w2) tot += part[par][w2][lane];
+            int li, rg;
+            locate(L, bid + st * G, li, rg);
+            const int N = pick(L.N, li);
+            const int n = rg * kRowsPerGroup + r;
+            float* y = pick(L.y, li);
+            int32_t* acc_out = pick(L.acc, li);
+            // D element v of lane l is row 4 (l / 16) + v (token), column l % 16 (weight row)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = 4 * q + v;
+                if (m < M) {
+                    const int val = tot[v] - rs_m[v];
+                    y[(size_t)m * N + n] = (float)val * (bw / xs_m[v]);
+                    if (acc_out) acc_out[(size_t)m * N + n] = val;
+                }
+            }
+        }
+        par ^= 1;
+    };
+
+    // Steps are instantiated for one and for several row groups per work group, so that no two paths with
+    // different loads in flight join.
+    auto run = [&](auto depth) {
+        constexpr int kDepth = decltype(depth)::value;
+        v4u wa[U], wb[U];
+        float ba = 0.0f, bb = 0.0f;
+        issue(wa, ba, 0);
+        if constexpr (kDepth == 1) {
+            stage();
+            compute(wa, ba, 0);
+        } else {
+            issue(wb, bb, 1);
+            stage();
+            int st = 0;
+            for (; st + 3 < S; st += 2) {
+                compute(wa, ba, st);
+                issue(wa, ba, st + 2);
+                compute(wb, bb, st + 1);
+                issue(wb, bb, st + 3);
+            }
+            if (st + 2 < S) {
+                compute(wa, ba, st);
+                issue(wa, ba, st + 2);
+                compute(wb, bb, st + 1);
+                compute(wa, ba, st + 2);
+            } else {
+                compute(wa, ba, st);
+                compute(wb, bb, st + 1);
+            }
+        }
+    };
+    if (S == 1) run(std::integral_constant<int, 1>{});
+    else run(std::integral_constant<int, 2>{});
+}
+
 // One token, streaming: each work group quantises the activation row once (Sec. 2.1), keeps its codes in LDS and
 // then walks the row groups g = blockIdx.x, blockIdx.x + gridDim.x, ... of the launch, one batch of WAVES * U
 // blocks at a time (a row group takes ceil(K / (256 WAVES U)) batches).  Two register sets of weight words
@@ -380,6 +571,8 @@ void launch_plain_u(int U, const FusedLinears& L, const int8_t* xq, const float*
     else launch_plain<WAVES, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
 }
 
+constexpr int64_t kDecodeStageBytes = 128 * 1024;   // LDS for the tokens' codes in the multi-token stream
+
 // Compute units of the current device (cached per device).
 int device_cus() {
     static int cus[64] = {0};
@@ -423,6 +616,31 @@ hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t
     return launch_stream<WAVES, U, 16>(L, x, K, xq, s, rs, stream);
 }
 
+template <int U, int MG>
+hipError_t launch_mstream(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
+                          int M, int K, hipStream_t stream) {
+    constexpr int W = 16;
+    const void* kern = reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true>);
+    const size_t lds = (size_t)M * (K + 16);
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * W, lds) != hipSuccess || occ <= 0) occ = 1;
+    const int64_t max_g = (int64_t)device_cus() * occ;
+    const int64_t rounds = (L.total + max_g - 1) / max_g;
+    const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * W);
+    hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true>), grid, block, lds, stream, L, xq, x_scale, x_rowsum,
+                       M, K);
+    return hipGetLastError();
+}
+
+template <int U>
+hipError_t launch_mstream_m(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
+                            int M, int K, hipStream_t stream) {
+    if (M <= 4) return launch_mstream<U, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 8) return launch_mstream<U, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 12) return launch_mstream<U, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
+    return launch_mstream<U, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+}
+
 }  // namespace
 
 // Waves per work group and blocks per wave per batch.  All waves of a launch should be resident at once
@@ -442,6 +660,18 @@ void decode_shape(int64_t groups, int64_t K, int max_u, int min_waves, int& wave
 
 hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                              int M, int K, hipStream_t stream) {
+    const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
+    const int cus = device_cus();
+    const bool fits = (int64_t)M * (K + 16) <= kDecodeStageBytes;   // the tokens' codes fit in LDS
+    (void)cus;
+    if (x_rowsum && fits && nkb <= 64) {
+        // 16-wave work groups, all of a row group's blocks in one batch; past what fits on the chip they stream
+        const int u16 = (nkb + 15) / 16;
+        if (u16 <= 1) return launch_mstream_m<1>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 2) return launch_mstream_m<2>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 3) return launch_mstream_m<3>(L, xq, x_scale, x_rowsum, M, K, stream);
+        return launch_mstream_m<4>(L, xq, x_scale, x_rowsum, M, K, stream);
+    }
     int waves, u;
     decode_shape(L.total, K, 4, 4, waves, u);
     switch (waves) {

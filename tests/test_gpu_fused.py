@@ -59,6 +59,14 @@ def test_fused_i2s_streaming(K, Ns):
     _fused_case("i2s", 1, K, Ns, seed=inputs.seed_for(2, 500 + K))
 
 
+# Several tokens at sizes where the multi-token streaming kernel walks several row groups per work group
+# (2900, 600 and 1080 row groups), with a 64-k last block in the first case.
+@pytest.mark.parametrize("M,K,Ns", [(8, 1088, [16000, 16000, 14400]), (16, 4096, [9600]), (5, 3200, [8640, 8640])])
+def test_fused_i2s_streaming_tokens(M, K, Ns):
+    _announce("fused i2s streaming tokens", M, K, Ns)
+    _fused_case("i2s", M, K, Ns, seed=inputs.seed_for(2, 700 + M + K))
+
+
 @pytest.mark.parametrize("M,K,Ns", [(1, 448, [16, 32]), (3, 4096, [64, 48])])
 def test_fused_tl2(M, K, Ns):
     _announce("fused tl2", M, K, Ns)
