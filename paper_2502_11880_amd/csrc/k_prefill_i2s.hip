@@ -77,6 +77,23 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
         rg_ok[ni] = rg[ni] < nrg;
     }
     const int r16 = j32 & 15;
+    // Loads are unconditional (a conditional load shape makes the compiler wait for every load before the next):
+    // rows past N load a real row group (never stored), and the short last block (Tl 64-k sub-tiles) is read
+    // through a 16-byte window moved back to end inside it, its words shifted into place at use.
+    const int Tl = nkb > nfull ? (K - nfull * kBK) / kSubK : 4;
+    uint32_t rgoff[4];                                              // byte offset of the (clamped) row group
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) rgoff[ni] = (uint32_t)(rg[ni] < nrg ? rg[ni] : nrg - 1) * (uint32_t)rg_bytes;
+    uint32_t offb_full[2], offb_tail[2];
+    int shb_tail[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        const int ql = 16 * (2 * c + h) + r16;                     // lane of the layout's chunk
+        const int want = 4 * Tl * ql;
+        offb_full[c] = 16u * ql;
+        offb_tail[c] = (uint32_t)min(want, 256 * Tl - 16);
+        shb_tail[c] = (want - (int)offb_tail[c]) >> 2;
+    }
 
     const v4i zero4 = {0, 0, 0, 0};
     v16i acc[MT][4];
@@ -89,62 +106,43 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
     for (int i = 0; i < kChunks; ++i) rs[i] = 0;
 
     v4i a_reg[kChunks];
-    v4u b_cur[4][2], b_next[4][2];     // [tile][chunk: q = h, q = 2 + h]
+    v4u bw0[4][2], bw1[4][2];          // weight words of even / odd stages: [tile][chunk: q = h, q = 2 + h]
 
     auto stage_T = [&](int kb) { return kb < nfull ? 4 : (K - nfull * kBK) / kSubK; };   // 64-k sub-tiles
+    // 32-bit offsets from uniform bases (the library limits M K and N K / 4 below 2^32)
     auto load_a = [&](int kb) {
-        const int T = stage_T(kb);
 #pragma unroll
         for (int i = 0; i < kChunks; ++i) {
             const int c = tid + i * kThreads;
-            const int row = c >> 4, col = (c & 15) * 16;
-            a_reg[i] = (m0 + row < M && col < 64 * T)
-                           ? *reinterpret_cast<const v4i*>(xq + (size_t)(m0 + row) * K + (size_t)kb * kBK + col)
-                           : zero4;
+            const uint32_t row = (uint32_t)min(m0 + (c >> 4), M - 1);
+            const uint32_t col = (uint32_t)min(kb * kBK + (c & 15) * 16, K - 16);
+            a_reg[i] = *reinterpret_cast<const v4i*>(xq + (row * (uint32_t)K + col));
         }
     };
     auto load_b = [&](int kb, v4u (&dst)[4][2]) {
-        const int T = stage_T(kb);
+        const bool full = kb < nfull;
+        const uint8_t* pk = packed + (size_t)kb * 1024;
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
+        for (int ni = 0; ni < 4; ++ni)
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                v4u w = {0u, 0u, 0u, 0u};
-                if (rg_ok[ni]) {
-                    const int ql = 16 * (2 * c + h) + r16;              // lane of the layout's chunk
-                    const uint8_t* p = packed + (size_t)rg[ni] * rg_bytes + (size_t)kb * 1024;
-                    if (T == 4) {
-                        w = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p + 16 * ql));
-                    } else {
-                        const uint32_t* pw = reinterpret_cast<const uint32_t*>(p + 4 * T * ql);
-                        w.x = pw[0];
-                        if (T > 1) w.y = pw[1];
-                        if (T > 2) w.z = pw[2];
-                    }
-                }
-                dst[ni][c] = w;
-            }
-        }
+            for (int c = 0; c < 2; ++c)
+                dst[ni][c] = __builtin_nontemporal_load(
+                    reinterpret_cast<const v4u*>(pk + (rgoff[ni] + (full ? offb_full[c] : offb_tail[c]))));
     };
-    auto store_a = [&](int buf) {
+    auto store_a = [&](int buf, int kb) {
+        const int T = kb < nfull ? 4 : kb < nkb ? Tl : 0;     // past the last stage: nothing counts
 #pragma unroll
         for (int i = 0; i < kChunks; ++i) {
             const int c = tid + i * kThreads;
             *reinterpret_cast<v4i*>(As[buf] + (c >> 4) * kARow + (c & 15) * 16) = a_reg[i];
-            if (!HAS_RS) rs[i] += byte_sum(a_reg[i]);
+            if (!HAS_RS) {
+                const bool on = m0 + (c >> 4) < M && (c & 15) * 16 < 64 * T;
+                rs[i] += on ? byte_sum(a_reg[i]) : 0;
+            }
         }
     };
-
-    // prologue: stage 0 in LDS buffer 0 and its weights in registers; stage 1's activations in registers
-    load_a(0);
-    load_b(0, b_cur);
-    store_a(0);
-    if (nkb > 1) load_a(1);
-    for (int kb = 0; kb < nkb; ++kb) {
-        const int buf = kb & 1;
-        const int T = stage_T(kb);
-        __syncthreads();                                  // stage kb's tile is in As[buf]; As[buf ^ 1] is free
-        if (kb + 1 < nkb) load_b(kb + 1, b_next);
+    // the MFMAs of one stage: T sub-tiles of 64 k (two 32-k steps each)
+    auto mac_stage = [&](int buf, int T, const v4u (&b_cur)[4][2]) {
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
             if (s < 2 * T) {
@@ -162,14 +160,48 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
                 }
             }
         }
-        if (kb + 1 < nkb) {
-            store_a(buf ^ 1);                              // stage kb+1 (loaded during stage kb-1)
-            if (kb + 2 < nkb) load_a(kb + 2);
+    };
+    // the short last stage: move each chunk's words to the front (its load window was moved back)
+    auto align_tail = [&](v4u (&b_cur)[4][2]) {
 #pragma unroll
-            for (int ni = 0; ni < 4; ++ni)
+        for (int c = 0; c < 2; ++c) {
+            const int sh = shb_tail[c];
 #pragma unroll
-                for (int c = 0; c < 2; ++c) b_cur[ni][c] = b_next[ni][c];
+            for (int ni = 0; ni < 4; ++ni) {
+                const v4u w = b_cur[ni][c];
+                v4u t;
+                t.x = sh == 0 ? w.x : sh == 1 ? w.y : sh == 2 ? w.z : w.w;
+                t.y = sh == 0 ? w.y : sh == 1 ? w.z : w.w;
+                t.z = sh == 0 ? w.z : w.w;
+                t.w = w.w;
+                b_cur[ni][c] = t;
+            }
         }
+    };
+
+    // Stage kb's activations are in LDS buffer kb % 2 and its weight words in bw0 / bw1 (even / odd).  Every
+    // stage loads the next stage's weights at its start and, after its MFMAs, stores the next stage's
+    // activations (loaded a stage earlier) and loads the ones after.  Indices past the last stage are clamped
+    // to it: those loads repeat the last stage (cache hits) and nothing is computed from them.
+    const int last = nkb - 1;
+    load_a(0);
+    load_b(0, bw0);
+    store_a(0, 0);
+    load_a(min(1, last));
+    for (int kb = 0; kb < nkb; kb += 2) {
+        __syncthreads();                                  // stage kb is in As[0]; As[1] is free
+        load_b(min(kb + 1, last), bw1);
+        if (kb >= nfull) align_tail(bw0);
+        mac_stage(0, kb < nfull ? 4 : Tl, bw0);
+        store_a(1, kb + 1);
+        load_a(min(kb + 2, last));
+        if (kb + 1 >= nkb) break;
+        __syncthreads();                                  // stage kb + 1 is in As[1]; As[0] is free
+        load_b(min(kb + 2, last), bw0);
+        if (kb + 1 >= nfull) align_tail(bw1);
+        mac_stage(1, kb + 1 < nfull ? 4 : Tl, bw1);
+        store_a(0, kb + 2);
+        load_a(min(kb + 3, last));
     }
 
     if (HAS_RS) {
