@@ -129,35 +129,33 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
                 dst[ni][c] = __builtin_nontemporal_load(
                     reinterpret_cast<const v4u*>(pk + (rgoff[ni] + (full ? offb_full[c] : offb_tail[c]))));
     };
+    // Columns past K are stored as zeros: a short last stage then runs as a full one, the weight words past its
+    // end (whatever the shifted window holds) meeting zero activations.
     auto store_a = [&](int buf, int kb) {
-        const int T = kb < nfull ? 4 : kb < nkb ? Tl : 0;     // past the last stage: nothing counts
+        const int kcols = kb < nfull ? kBK : kb < nkb ? 64 * Tl : 0;   // past the last stage: nothing counts
 #pragma unroll
         for (int i = 0; i < kChunks; ++i) {
             const int c = tid + i * kThreads;
-            *reinterpret_cast<v4i*>(As[buf] + (c >> 4) * kARow + (c & 15) * 16) = a_reg[i];
-            if (!HAS_RS) {
-                const bool on = m0 + (c >> 4) < M && (c & 15) * 16 < 64 * T;
-                rs[i] += on ? byte_sum(a_reg[i]) : 0;
-            }
+            const bool col_on = (c & 15) * 16 < kcols;
+            const v4i a = col_on ? a_reg[i] : zero4;
+            *reinterpret_cast<v4i*>(As[buf] + (c >> 4) * kARow + (c & 15) * 16) = a;
+            if (!HAS_RS) rs[i] += (m0 + (c >> 4) < M) ? byte_sum(a) : 0;
         }
     };
-    // the MFMAs of one stage: T sub-tiles of 64 k (two 32-k steps each)
-    auto mac_stage = [&](int buf, int T, const v4u (&b_cur)[4][2]) {
+    // the MFMAs of one stage: 8 steps of 32 k
+    auto mac_stage = [&](int buf, const v4u (&b_cur)[4][2]) {
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-            if (s < 2 * T) {
-                v4i a[MT];
+            v4i a[MT];
+#pragma unroll
+            for (int mi = 0; mi < MT; ++mi)
+                a[mi] = *reinterpret_cast<const v4i*>(As[buf] + (32 * MT * wm + 32 * mi + j32) * kARow + 32 * s + 16 * h);
+#pragma unroll
+            for (int ni = 0; ni < 4; ++ni) {
+                const v4i b = unpack_codes(word_of(b_cur[ni][s & 1], s >> 1));
 #pragma unroll
                 for (int mi = 0; mi < MT; ++mi)
-                    a[mi] = *reinterpret_cast<const v4i*>(As[buf] + (32 * MT * wm + 32 * mi + j32) * kARow + 32 * s +
-                                                          16 * h);
-#pragma unroll
-                for (int ni = 0; ni < 4; ++ni) {
-                    const v4i b = unpack_codes(word_of(b_cur[ni][s & 1], s >> 1));
-#pragma unroll
-                    for (int mi = 0; mi < MT; ++mi)
-                        acc[mi][ni] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[mi], b, acc[mi][ni], 0, 0, 0);
-                }
+                    acc[mi][ni] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[mi], b, acc[mi][ni], 0, 0, 0);
             }
         }
     };
@@ -192,14 +190,14 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
         __syncthreads();                                  // stage kb is in As[0]; As[1] is free
         load_b(min(kb + 1, last), bw1);
         if (kb >= nfull) align_tail(bw0);
-        mac_stage(0, kb < nfull ? 4 : Tl, bw0);
+        mac_stage(0, bw0);
         store_a(1, kb + 1);
         load_a(min(kb + 2, last));
         if (kb + 1 >= nkb) break;
         __syncthreads();                                  // stage kb + 1 is in As[1]; As[0] is free
         load_b(min(kb + 2, last), bw0);
         if (kb + 1 >= nfull) align_tail(bw1);
-        mac_stage(1, kb + 1 < nfull ? 4 : Tl, bw1);
+        mac_stage(1, bw1);
         store_a(0, kb + 2);
         load_a(min(kb + 3, last));
     }
