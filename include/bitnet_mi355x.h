@@ -108,13 +108,12 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *   y      device fp32 [M, N]: y[m, n] = fp32(acc[m, n]) * fp32(w_scale / x_scale[m]).
  *   acc    device int32 [M, N] or NULL: when given, also receives acc[m, n] = sum_k xq[m, k] * t[n, k]
  *          exactly (the same integers for every tiling and launch shape).
- *   ws     device workspace of at least bitnet_mpgemm_workspace_bytes(layout, M, N, K) bytes, or NULL
- *          when that is 0.  It holds split-K partial sums and per-tile completion counters.  It must be
- *          zero-filled before its first use; every call resets the counters it used to zero when its
- *          kernels finish, so one workspace serves any number of calls on one stream (not concurrent
- *          calls on several streams).
- *   Shapes: M >= 1, N % 16 == 0, K % 64 == 0, K <= 132096 (127 * K < 2^24 keeps acc exact in fp32).
- *   M <= 16 runs the decode GEMV; larger M runs the prefill GEMM.
+ *   ws     device workspace of at least bitnet_mpgemm_workspace_bytes(layout, M, N, K) bytes, or NULL when
+ *          that is 0 (else BITNET_E_WORKSPACE).  It holds the exact int32 partial sums of a prefill GEMM split
+ *          along K (I2_S, M > 16, small grids; only when x_rowsum is given); any contents on entry, nothing
+ *          kept between calls.  Calls that run concurrently must not share it.
+ *   Shapes: M >= 1, N % 16 == 0, K % 64 == 0, K <= 132096 (127 * K < 2^24 keeps acc exact in fp32);
+ *   I2_S also needs N * K and M * K below 2^32.  M <= 16 runs the decode GEMV; larger M the prefill GEMM.
  */
 bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale,
                             int64_t N, int64_t K, const int8_t* xq, const float* x_scale,

@@ -95,6 +95,7 @@ bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* 
 
 size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K) {
     if (!layout_ok(layout) || !weight_shape_ok(N, K) || M < 1) return 0;
+    if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens) return bitnet::prefill_workspace_bytes(M, N, K);
     return 0;
 }
 
@@ -112,6 +113,11 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
     if (packed_bytes < packed_bytes_of(layout, N, K))
         return fail(BITNET_E_INVALID, "packed buffer holds %zu bytes, %zu needed", packed_bytes,
                     packed_bytes_of(layout, N, K));
+    if (layout == BITNET_LAYOUT_I2S && ((uint64_t)N * (uint64_t)K >= ((uint64_t)1 << 32) ||
+                                        (uint64_t)M * (uint64_t)K >= ((uint64_t)1 << 32)))
+        return fail(BITNET_E_SHAPE, "I2_S needs N*K and M*K below 2^32; got M=%lld N=%lld K=%lld", (long long)M,
+                    (long long)N, (long long)K);
+    // the workspace holds split-K slices of the prefill GEMM (used when x_rowsum is given)
     const size_t need = bitnet_mpgemm_workspace_bytes(layout, M, N, K);
     if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
 
@@ -129,7 +135,7 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
     }
     if (layout == BITNET_LAYOUT_I2S)
         return hip_status(bitnet::launch_i2s_prefill(packed, w_scale, xq, x_scale, x_rowsum, (int)M, (int)N, (int)K, y,
-                                                     acc, s),
+                                                     acc, ws, ws_bytes, s),
                           "bitnet_mpgemm launch");
     const int64_t slice = bitnet::kElutMaxTokens;
     for (int64_t m0 = 0; m0 < M; m0 += slice) {

@@ -110,9 +110,13 @@ size_t pack_workspace_bytes();
 hipError_t launch_pack(int layout, const float* W, int64_t N, int64_t K, void* packed, float* w_scale,
                        void* ws, hipStream_t stream);
 
+// Prefill (M > 16): split-K over the workspace when it is given and large enough (and x_rowsum is given).
+constexpr int kMaxSplits = 16;
+int device_cus();
+size_t prefill_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                              const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc,
-                              hipStream_t stream);
+                              const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
 
 // Up to kMaxFused weights that read the same activation, served by one decode launch.
 constexpr int kMaxFused = 8;

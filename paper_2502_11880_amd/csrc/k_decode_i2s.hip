@@ -573,19 +573,6 @@ void launch_plain_u(int U, const FusedLinears& L, const int8_t* xq, const float*
 
 constexpr int64_t kDecodeStageBytes = 128 * 1024;   // LDS for the tokens' codes in the multi-token stream
 
-// Compute units of the current device (cached per device).
-int device_cus() {
-    static int cus[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cus[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cus[dev] = n;
-    }
-    return cus[dev];
-}
-
 template <int WAVES, int U, int XV>
 hipError_t launch_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
                          hipStream_t stream) {
@@ -642,6 +629,19 @@ hipError_t launch_mstream_m(const FusedLinears& L, const int8_t* xq, const float
 }
 
 }  // namespace
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
 
 // Waves per work group and blocks per wave per batch.  All waves of a launch should be resident at once
 // (about 4096 on 256 CUs at the register use of these kernels): take the widest group (16, 8 or 4 waves) that

@@ -43,7 +43,7 @@ template <int WM, int WN, bool HAS_RS>
 __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
     const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
     const float* __restrict__ x_scale, const int32_t* __restrict__ x_rowsum, int M, int N, int K,
-    float* __restrict__ y, int32_t* __restrict__ acc_out) {
+    float* __restrict__ y, int32_t* __restrict__ acc_out, int splits, int32_t* __restrict__ part) {
     constexpr int kThreads = 64 * WM * WN;
     constexpr int kBN = 128 * WN;
     constexpr int MT = 4 / WM;                               // 32-row MFMA tiles per wave along M
@@ -56,7 +56,10 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
     const int j32 = lane & 31, h = lane >> 5;
     const int tiles_m = (M + kBM - 1) / kBM;
     const int tiles_n = (N + kBN - 1) / kBN;
-    const int L = xcd_logical_id(blockIdx.x, gridDim.x);
+    // split-K: the launch is splits slices of tiles; slice `split` takes stages [kb_lo, kb_hi)
+    const int ntiles = gridDim.x / splits;
+    const int split = blockIdx.x / ntiles;
+    const int L = xcd_logical_id(blockIdx.x - split * ntiles, ntiles);
     // grouped order: kGroupM token tiles x all weight tiles per group, token tile fastest
     const int gsize = kGroupM * tiles_n;
     const int g = L / gsize, gl = L - g * gsize;
@@ -65,6 +68,9 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
     const int m0 = tm * kBM, n0 = tn * kBN;
     const int nkb = (K + kBK - 1) / kBK;
     const int nfull = K / kBK;
+    const int per_split = (nkb + splits - 1) / splits;
+    const int kb_lo = split * per_split;
+    const int kb_hi = min(nkb, kb_lo + per_split);
     const int nrg = N / kRowsPerGroup;
     const size_t rg_bytes = (size_t)4 * K;
 
@@ -181,25 +187,42 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
     // stage loads the next stage's weights at its start and, after its MFMAs, stores the next stage's
     // activations (loaded a stage earlier) and loads the ones after.  Indices past the last stage are clamped
     // to it: those loads repeat the last stage (cache hits) and nothing is computed from them.
-    const int last = nkb - 1;
-    load_a(0);
-    load_b(0, bw0);
-    store_a(0, 0);
-    load_a(min(1, last));
-    for (int kb = 0; kb < nkb; kb += 2) {
+    const int last = kb_hi - 1;
+    load_a(kb_lo);
+    load_b(kb_lo, bw0);
+    store_a(0, kb_lo);
+    load_a(min(kb_lo + 1, last));
+    for (int kb = kb_lo; kb < kb_hi; kb += 2) {
         __syncthreads();                                  // stage kb is in As[0]; As[1] is free
         load_b(min(kb + 1, last), bw1);
         if (kb >= nfull) align_tail(bw0);
         mac_stage(0, bw0);
-        store_a(1, kb + 1);
+        store_a(1, kb + 1 < kb_hi ? kb + 1 : nkb);
         load_a(min(kb + 2, last));
-        if (kb + 1 >= nkb) break;
+        if (kb + 1 >= kb_hi) break;
         __syncthreads();                                  // stage kb + 1 is in As[1]; As[0] is free
         load_b(min(kb + 2, last), bw0);
         if (kb + 1 >= nfull) align_tail(bw1);
         mac_stage(1, bw1);
-        store_a(0, kb + 2);
+        store_a(0, kb + 2 < kb_hi ? kb + 2 : nkb);
         load_a(min(kb + 3, last));
+    }
+
+    if (part) {
+        // split-K: this slice's exact partial sums (the code offset and the scales are applied when the
+        // slices are summed)
+        int32_t* pp = part + (size_t)split * M * N;
+#pragma unroll
+        for (int mi = 0; mi < MT; ++mi)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + 32 * MT * wm + 32 * mi + 8 * (v >> 2) + 4 * h + (v & 3);
+                if (m >= M) continue;
+#pragma unroll
+                for (int ni = 0; ni < 4; ++ni)
+                    if (rg_ok[ni]) pp[(size_t)m * N + rg[ni] * kRowsPerGroup + r16] = acc[mi][ni][v];
+            }
+        return;
     }
 
     if (HAS_RS) {
@@ -242,32 +265,102 @@ __global__ __launch_bounds__(64 * WM * WN) void i2s_prefill_kernel(
     }
 }
 
+// Sum of the split-K slices, then the epilogue: y = (sum - sum_k xq[m, k]) * (beta / s_m).  Four outputs of
+// one row per thread.
+__global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __restrict__ part, int splits, int M,
+                                                             int N, const int32_t* __restrict__ x_rowsum,
+                                                             const float* __restrict__ x_scale,
+                                                             const float* __restrict__ w_scale, float* __restrict__ y,
+                                                             int32_t* __restrict__ acc_out) {
+    const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;      // index of 4 outputs
+    const int n4 = N >> 2;
+    if (i4 >= (int64_t)M * n4) return;
+    const int m = (int)(i4 / n4);
+    const size_t off = (size_t)i4 * 4;
+    v4i t = *reinterpret_cast<const v4i*>(part + off);
+    for (int sp = 1; sp < splits; ++sp) t += *reinterpret_cast<const v4i*>(part + (size_t)sp * M * N + off);
+    const int rs = x_rowsum[m];
+    t -= (v4i){rs, rs, rs, rs};
+    const float sc = *w_scale / x_scale[m];
+    float4 o;
+    o.x = (float)t.x * sc;
+    o.y = (float)t.y * sc;
+    o.z = (float)t.z * sc;
+    o.w = (float)t.w * sc;
+    *reinterpret_cast<float4*>(y + off) = o;
+    if (acc_out) *reinterpret_cast<v4i*>(acc_out + off) = t;
+}
+
 template <int WM, int WN>
 void launch_cfg(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
-                const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+                const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, int splits, int32_t* part,
+                hipStream_t stream) {
     const unsigned tiles = (unsigned)(((M + kBM - 1) / kBM) * ((N + 128 * WN - 1) / (128 * WN)));
+    const dim3 grid(tiles * (unsigned)splits), block(64 * WM * WN);
     if (x_rowsum)
-        hipLaunchKernelGGL((i2s_prefill_kernel<WM, WN, true>), dim3(tiles), dim3(64 * WM * WN), 0, stream, pk, w_scale,
-                           xq, x_scale, x_rowsum, M, N, K, y, acc);
+        hipLaunchKernelGGL((i2s_prefill_kernel<WM, WN, true>), grid, block, 0, stream, pk, w_scale, xq, x_scale,
+                           x_rowsum, M, N, K, y, acc, splits, part);
     else
-        hipLaunchKernelGGL((i2s_prefill_kernel<WM, WN, false>), dim3(tiles), dim3(64 * WM * WN), 0, stream, pk,
-                           w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc);
+        hipLaunchKernelGGL((i2s_prefill_kernel<WM, WN, false>), grid, block, 0, stream, pk, w_scale, xq, x_scale,
+                           x_rowsum, M, N, K, y, acc, splits, part);
+}
+
+// Tile shape (the widest that still gives every CU some work) and split-K factor.  Splitting K keeps small
+// grids busy: it aims at one work group per CU, with at least two 256-k stages per slice.
+void prefill_plan(int64_t M, int64_t N, int64_t K, int& wn, int& splits) {
+    const int64_t tiles_m = (M + kBM - 1) / kBM;
+    int64_t tiles;
+    if (tiles_m * ((N + 511) / 512) >= 192) {
+        wn = 4;                                           // 128 x 512, 4 waves
+        tiles = tiles_m * ((N + 511) / 512);
+    } else if (tiles_m * ((N + 255) / 256) >= 96) {
+        wn = 2;                                           // 128 x 256, 4 waves
+        tiles = tiles_m * ((N + 255) / 256);
+    } else {
+        wn = 1;                                           // 128 x 128, 2 waves
+        tiles = tiles_m * ((N + 127) / 128);
+    }
+    const int64_t nkb = (K + kBK - 1) / kBK;
+    const int64_t cus = device_cus();
+    // only grids that leave at least half the CUs idle: the slices' extra pass over M x N costs more elsewhere
+    int64_t sp = 2 * tiles <= cus ? (cus + tiles - 1) / tiles : 1;
+    if (sp > nkb / 2) sp = nkb / 2;
+    if (sp > kMaxSplits) sp = kMaxSplits;
+    splits = sp > 1 ? (int)sp : 1;
+    // slices of whole stages: no empty slice
+    if (splits > 1) {
+        const int64_t per = (nkb + splits - 1) / splits;
+        splits = (int)((nkb + per - 1) / per);
+    }
 }
 
 }  // namespace
 
+size_t prefill_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    int wn, splits;
+    prefill_plan(M, N, K, wn, splits);
+    return splits > 1 ? (size_t)splits * (size_t)M * (size_t)N * sizeof(int32_t) : 0;
+}
+
 hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                              const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc,
-                              hipStream_t stream) {
+                              const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    const long tiles_m = (M + kBM - 1) / kBM;
-    // the widest tile that still gives every CU some work
-    if (tiles_m * ((N + 511) / 512) >= 192)
-        launch_cfg<1, 4>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, stream);      // 128 x 512, 4 waves
-    else if (tiles_m * ((N + 255) / 256) >= 96)
-        launch_cfg<2, 2>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, stream);      // 128 x 256, 4 waves
-    else
-        launch_cfg<2, 1>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, stream);      // 128 x 128, 2 waves
+    int wn, splits;
+    prefill_plan(M, N, K, wn, splits);
+    // split-K needs the token sums and the workspace for the slices
+    if (!x_rowsum || !ws || ws_bytes < (size_t)splits * M * N * sizeof(int32_t)) splits = 1;
+    int32_t* part = splits > 1 ? static_cast<int32_t*>(ws) : nullptr;
+    switch (wn) {
+        case 4: launch_cfg<1, 4>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, splits, part, stream); break;
+        case 2: launch_cfg<2, 2>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, splits, part, stream); break;
+        default: launch_cfg<2, 1>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, splits, part, stream); break;
+    }
+    if (splits > 1) {
+        const int64_t n4 = (int64_t)M * (N / 4);
+        hipLaunchKernelGGL(prefill_splitk_finish, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, part,
+                           splits, M, N, x_rowsum, x_scale, w_scale, y, acc);
+    }
     return hipGetLastError();
 }
 
