@@ -111,6 +111,9 @@ def main():
               for l in range(n_layers)] for c in range(copies)] if decode else None
     stream = torch.cuda.Stream()
     sptr = stream.cuda_stream
+    # the set-up above ran on the default stream: the side stream starts after all of it
+    torch.cuda.synchronize()
+    stream.wait_stream(torch.cuda.current_stream())
 
     def step(i, path, quantize=True):
         c = i % copies
