@@ -4,10 +4,13 @@
 // MFMA-bound design for it.  (On gfx950 the 32x32x32 int8 MFMA sustains about twice the rate of the 16x16x64
 // one, so the contraction uses the former.)
 //
-// Work decomposition.  A work group of 8 waves computes a 128-token x 512-row output tile; each wave owns
+// Work decomposition.  A work group of 8 waves computes a 128-token x (128 WN)-row output tile.  Each wave owns
 // 64 tokens x 128 rows (2 x 4 MFMA tiles of 32 x 32, 128 accumulator registers), so two waves share every
-// SIMD: while one waits on LDS or on the barrier, the other keeps the matrix core busy.  K advances in 256-k
-// stages, the I2_S block size, so the packed weights of one row group and stage are one contiguous KiB.
+// SIMD: while one waits on LDS or on the barrier, the other keeps the matrix core busy.  With WN = 4 the waves
+// tile the 128 x 512 output 2 x 4; with WN = 2 they tile a 128 x 256 output 2 x 2 and each pair splits the k-steps
+// of every stage (WK = 2 K-groups), the two partial tiles summed through LDS at the end: the narrower tile doubles
+// the grid of small problems without exact partial sums going through HBM.  K advances in 256-k stages, the I2_S
+// block size, so the packed weights of one row group and stage are one contiguous KiB.
 //
 // Operands.  Both are staged in LDS, double-buffered, one barrier per stage.  Every thread loads its 16-byte
 // chunks of the next-but-one stage into registers (plain coalesced loads: a wave reads whole KiB runs) and
@@ -36,7 +39,7 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kBK = 256;                   // k per stage (one I2_S block)
 constexpr int kGroupM = 4;                 // token tiles per scheduling group
-constexpr int kBM = 128, kBN = 512;        // work group tile
+constexpr int kBM = 128;                   // tokens per work group tile
 constexpr int kWaves = 8, kThreads = 64 * kWaves;
 constexpr int kARow = kBK + 16;            // padded LDS row of the activation tile
 constexpr int kAChunks = kBM * (kBK / 16) / kThreads;         // 16-byte activation chunks per thread per stage
@@ -49,19 +52,28 @@ __device__ __forceinline__ int byte_sum(const v4i& v, int acc) {
     return __builtin_amdgcn_sdot4(v.w, ones, acc, false);
 }
 
-template <bool HAS_RS>
+template <int WN, bool HAS_RS>
 __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads) void i2s_prefill_kernel(
     const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
     const float* __restrict__ x_scale, const int32_t* __restrict__ x_rowsum, int M, int N, int K,
     float* __restrict__ y, int32_t* __restrict__ acc_out, int splits, int32_t* __restrict__ part) {
     constexpr int MT = 2, NT = 4;                                 // 32 x 32 MFMA tiles per wave
-    __shared__ __align__(16) int8_t As[2][kBM * kARow];
-    __shared__ __align__(16) v4u Ws[2][4 * 8 * 64];              // [wave column][step][lane]: one word per tile
-    __shared__ int rowsum_s[kBM];
+    constexpr int WK = 4 / WN;                                    // K-groups: waves sharing one output tile
+    constexpr int kBN = 128 * WN;
+    constexpr int kSteps = 8 / WK;                                // 32-k steps per stage of each wave
+    constexpr int kWPer = WN;                                     // 16-byte weight chunks per thread per stage
+    constexpr int kAsBytes = 2 * kBM * kARow;
+    constexpr int kWsBytes = 2 * WN * 8 * 64 * 16;
+    constexpr int kRedBytes = (WK - 1) * 2 * WN * 64 * 128 * 4;   // partial tiles of the K-groups past the first
+    constexpr int kSmem = (kAsBytes + kWsBytes) > kRedBytes ? (kAsBytes + kWsBytes) : kRedBytes;
+    __shared__ __align__(16) int8_t smem[kSmem];
+    __shared__ int rowsum_s[WK][kBM];
+    int8_t (*As)[kBM * kARow] = reinterpret_cast<int8_t (*)[kBM * kARow]>(smem);
+    v4u (*Ws)[WN * 8 * 64] = reinterpret_cast<v4u (*)[WN * 8 * 64]>(smem + kAsBytes);   // [column][step][lane]
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave & 1, wn = wave >> 1;                      // 2 waves along tokens x 4 along rows
+    const int wm = wave & 1, wn = (wave >> 1) % WN, wk = (wave >> 1) / WN;
     const int j32 = lane & 31, h = lane >> 5;
     const int tiles_m = (M + kBM - 1) / kBM;
     const int tiles_n = (N + kBN - 1) / kBN;
@@ -116,23 +128,25 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     // block, shifted into place and cleared past K before the transpose (zero codes: the activation bytes past K
     // add nothing).  Row groups past N load a real row group (never stored).
     const int Tl = nkb > nfull ? (K - nfull * kBK) / kSubK : 4;
-    const int w_col = tid >> 7, w_par = (tid >> 6) & 1, w_l = lane;
+    // with WN < 4 the records of one (column, parity, lane) are shared by 4 / WN threads, kWPer tiles each
+    const int w_combo = tid % (WN * 128), w_ni0 = (tid / (WN * 128)) * kWPer;
+    const int w_col = w_combo >> 7, w_par = (w_combo >> 6) & 1, w_l = lane;
     const int w_chunk = 16 * (2 * w_par + (w_l >> 5)) + (w_l & 15);          // layout lane chunk l
     const int w_want = 4 * Tl * w_chunk;
     const int w_off_tail = min(w_want, 256 * Tl - 16);
     const int w_sh = (w_want - w_off_tail) >> 2;
-    v4u w_reg[NT];
-    uint32_t w_rgb[NT];
+    v4u w_reg[kWPer];
+    uint32_t w_rgb[kWPer];
 #pragma unroll
-    for (int ni = 0; ni < NT; ++ni) {
-        const int rgl = 8 * w_col + 2 * ni + ((w_l >> 4) & 1);
-        w_rgb[ni] = (uint32_t)min(rg0 + rgl, nrg - 1) * (4u * (uint32_t)K);
+    for (int i = 0; i < kWPer; ++i) {
+        const int rgl = 8 * w_col + 2 * (w_ni0 + i) + ((w_l >> 4) & 1);
+        w_rgb[i] = (uint32_t)min(rg0 + rgl, nrg - 1) * (4u * (uint32_t)K);
     }
     auto load_w = [&](int kb) {
         const uint8_t* pk = packed + (size_t)kb * 1024;
         const uint32_t off = kb < nfull ? 16u * (uint32_t)w_chunk : (uint32_t)w_off_tail;
 #pragma unroll
-        for (int ni = 0; ni < NT; ++ni) w_reg[ni] = *reinterpret_cast<const v4u*>(pk + (w_rgb[ni] + off));
+        for (int i = 0; i < kWPer; ++i) w_reg[i] = *reinterpret_cast<const v4u*>(pk + (w_rgb[i] + off));
     };
     // Record j (step 2 j + parity) of this thread.  The window shift is a two-step barrel shift on the bits of the
     // lane's word shift, all selects: a branch (or a compare chain, which the compiler turns into one) here makes it
@@ -141,16 +155,18 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
         const int sh = full ? 0 : w_sh;
         const bool s1 = (sh & 1) != 0, s2 = (sh & 2) != 0;
         const bool live = full || j < Tl;
-        uint32_t rec[NT];
+        uint32_t rec[kWPer];
 #pragma unroll
-        for (int ni = 0; ni < NT; ++ni) {
-            const v4u w = w_reg[ni];
+        for (int i = 0; i < kWPer; ++i) {
+            const v4u w = w_reg[i];
             const uint32_t u0 = s1 ? w.y : w.x, u1 = s1 ? w.z : w.y, u2 = s1 ? w.w : w.z, u3 = w.w;
             const uint32_t t0 = s2 ? u2 : u0, t1 = s2 ? u3 : u1;
             const uint32_t wj = j == 0 ? t0 : j == 1 ? t1 : j == 2 ? u2 : u3;
-            rec[ni] = live ? wj : 0u;
+            rec[i] = live ? wj : 0u;
         }
-        Ws[buf][(w_col * 8 + 2 * j + w_par) * 64 + w_l] = v4u{rec[0], rec[1], rec[2], rec[3]};
+        uint32_t* dst = reinterpret_cast<uint32_t*>(&Ws[buf][(w_col * 8 + 2 * j + w_par) * 64 + w_l]) + w_ni0;
+        if constexpr (kWPer == 4) *reinterpret_cast<v4u*>(dst) = v4u{rec[0], rec[1], rec[2], rec[3]};
+        else *reinterpret_cast<uint2*>(dst) = make_uint2(rec[0], rec[1]);
     };
     auto store_w = [&](int buf, bool full) {
 #pragma unroll
@@ -171,15 +187,17 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     // The activation operands of step s + 1 are read while step s multiplies (two register sets), so a wave never
     // waits on LDS between steps; the sched barriers keep the compiler from moving the reads back to their use.
     auto mac_stage = [&](int buf, int live, auto&& after_step) {
+        const int s0 = wk * kSteps;                               // this K-group's first k-step of the stage
         v4i a[2][MT];
         v4u b[2];
 #pragma unroll
-        for (int mi = 0; mi < MT; ++mi) a[0][mi] = *reinterpret_cast<const v4i*>(As[buf] + a_lane + 32 * kARow * mi);
-        b[0] = Ws[buf][w_lane];
+        for (int mi = 0; mi < MT; ++mi)
+            a[0][mi] = *reinterpret_cast<const v4i*>(As[buf] + a_lane + 32 * kARow * mi + 32 * s0);
+        b[0] = Ws[buf][w_lane + 64 * s0];
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            const int cur = s & 1;
-            if (s + 1 < 8) {
+        for (int i = 0; i < kSteps; ++i) {
+            const int cur = i & 1, s = s0 + i;
+            if (i + 1 < kSteps) {
 #pragma unroll
                 for (int mi = 0; mi < MT; ++mi)
                     a[cur ^ 1][mi] = *reinterpret_cast<const v4i*>(As[buf] + a_lane + 32 * kARow * mi + 32 * (s + 1));
@@ -198,7 +216,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
                 for (int mi = 0; mi < MT; ++mi)
                     acc[mi][ni] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[cur][mi], bq, acc[mi][ni], 0, 0, 0);
             }
-            after_step(s);
+            after_step(i);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -208,7 +226,10 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     // a whole stage earlier) into the other buffer, one after each 32-k step, and reloads each register with the
     // stage after: the waves sharing a SIMD then always have MFMAs to issue while the copies drain.  Stage indices
     // past the slice are clamped to its last stage: those loads repeat it and nothing is computed from them.
-    static_assert(kAChunks == 4, "one activation chunk copy per step of the first half-stage");
+    static_assert(kAChunks == 4, "four activation chunks per thread per stage");
+    // copies per step: WK = 1 spreads the 4 activation chunks over steps 0-3 and the 4 weight records over 4-7;
+    // WK = 2 does one of each per step
+    constexpr int kWStep = kSteps == 8 ? 4 : 0;
     const int last = kb_hi - 1;
     if (kb_lo < kb_hi) {
         load_a(kb_lo);
@@ -222,17 +243,59 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
             __syncthreads();
             const int nxt = min(kb + 1, last), nxt2 = min(kb + 2, last);
             const bool nxt_full = nxt < nfull;
-            mac_stage(buf, kb < nfull ? 8 : 2 * Tl, [&](int s) {
-                if (s < kAChunks) {
-                    store_a1(buf ^ 1, s);
-                    load_a1(nxt2, s);
-                } else {
-                    store_w1(buf ^ 1, nxt_full, s - kAChunks);
-                    if (s == 7) load_w(nxt2);
+            mac_stage(buf, kb < nfull ? 8 : 2 * Tl, [&](int i) {
+                if (i < kAChunks) {
+                    store_a1(buf ^ 1, i);
+                    load_a1(nxt2, i);
                 }
+                if (i >= kWStep) store_w1(buf ^ 1, nxt_full, i - kWStep);
+                if (i == kSteps - 1) load_w(nxt2);
             });
             buf ^= 1;
         }
+    }
+
+    // The K-groups past the first hand their partial tiles to the first through LDS (the staging buffers are free
+    // once every wave has passed the barrier below); every wave passes every barrier, and only the first K-group
+    // stores.  Token sums: from x_rowsum, or each K-group's partial from its activation operands.
+    __syncthreads();
+    v4i* red = reinterpret_cast<v4i*>(smem);                      // [wave tile][mi][ni][4 words][lane]
+    const int slot = (wm * WN + wn) * (MT * NT * 4);
+    if (WK > 1 && wk == 1) {
+#pragma unroll
+        for (int mi = 0; mi < MT; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NT; ++ni)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4)
+                    red[(slot + (mi * NT + ni) * 4 + q4) * 64 + lane] =
+                        v4i{acc[mi][ni][4 * q4], acc[mi][ni][4 * q4 + 1], acc[mi][ni][4 * q4 + 2], acc[mi][ni][4 * q4 + 3]};
+    }
+    if (HAS_RS) {
+        if (tid < kBM) rowsum_s[0][tid] = (m0 + tid < M) ? x_rowsum[m0 + tid] : 0;
+    } else if (wn == 0) {
+        // lanes j and j + 32 summed the two halves of token row 64 wm + 32 mi + j over this K-group's steps
+#pragma unroll
+        for (int mi = 0; mi < MT; ++mi) {
+            const int v = rs_part[mi] + __shfl_xor(rs_part[mi], 32, 64);
+            if (h == 0) rowsum_s[wk][64 * wm + 32 * mi + j32] = v;
+        }
+    }
+    __syncthreads();
+    if (wk != 0) return;                                          // no barrier follows
+    if (WK > 1) {
+#pragma unroll
+        for (int mi = 0; mi < MT; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NT; ++ni)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const v4i o = red[(slot + (mi * NT + ni) * 4 + q4) * 64 + lane];
+                    acc[mi][ni][4 * q4] += o.x;
+                    acc[mi][ni][4 * q4 + 1] += o.y;
+                    acc[mi][ni][4 * q4 + 2] += o.z;
+                    acc[mi][ni][4 * q4 + 3] += o.w;
+                }
     }
 
     if (part) {
@@ -254,18 +317,6 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
         return;
     }
 
-    if (HAS_RS) {
-        if (tid < kBM) rowsum_s[tid] = (m0 + tid < M) ? x_rowsum[m0 + tid] : 0;
-    } else if (wn == 0) {
-        // lanes j and j + 32 summed the two halves of token row 64 wm + 32 mi + j
-#pragma unroll
-        for (int mi = 0; mi < MT; ++mi) {
-            const int v = rs_part[mi] + __shfl_xor(rs_part[mi], 32, 64);
-            if (h == 0) rowsum_s[64 * wm + 32 * mi + j32] = v;
-        }
-    }
-    __syncthreads();
-
     // D element v of lane (j, h): row 8 (v / 4) + 4 h + v % 4, column j (weight row n0 + 128 wn + 32 ni + j).
     const float beta = *w_scale;
 #pragma unroll
@@ -275,7 +326,11 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
             const int ml = 64 * wm + 32 * mi + 8 * (v >> 2) + 4 * h + (v & 3);
             const int m = m0 + ml;
             if (m >= M) continue;
-            const int rsum = rowsum_s[ml];
+            int rsum = rowsum_s[0][ml];
+            if (!HAS_RS) {
+#pragma unroll
+                for (int g = 1; g < WK; ++g) rsum += rowsum_s[g][ml];
+            }
             const float sc = beta / x_scale[m];
 #pragma unroll
             for (int ni = 0; ni < NT; ++ni) {
@@ -315,29 +370,47 @@ __global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __re
     if (acc_out) *reinterpret_cast<v4i*>(acc_out + off) = t;
 }
 
-// Split-K factor: splitting K keeps small grids busy.  It aims at one work group per CU, with at least two
-// 256-k stages per slice, and only for grids that leave at least half the CUs idle (the slices' extra pass over
-// M x N costs more elsewhere).
-int prefill_splits(int64_t M, int64_t N, int64_t K) {
+// Tile width and split-K factor.  The 128 x 512 tile where its grid gives every CU a work group, else the
+// 128 x 256 one (two K-groups per tile).  Splitting K keeps still smaller grids busy: it aims at one work group per
+// CU, with at least two 256-k stages per slice, and only for grids that leave at least half the CUs idle (the
+// slices' extra pass over M x N costs more elsewhere).
+void prefill_plan(int64_t M, int64_t N, int64_t K, int& wn, int& splits) {
     const int64_t cus = device_cus();
-    const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+    const int64_t tiles_m = (M + kBM - 1) / kBM;
+    const int64_t t4 = tiles_m * ((N + 511) / 512);
+    wn = t4 >= cus ? 4 : 2;
+    const int64_t tiles = wn == 4 ? t4 : tiles_m * ((N + 255) / 256);
     const int64_t nkb = (K + kBK - 1) / kBK;
     int64_t sp = 2 * tiles <= cus ? (cus + tiles - 1) / tiles : 1;
     if (sp > nkb / 2) sp = nkb / 2;
     if (sp > kMaxSplits) sp = kMaxSplits;
-    int splits = sp > 1 ? (int)sp : 1;
+    splits = sp > 1 ? (int)sp : 1;
     // slices of whole stages: no empty slice
     if (splits > 1) {
         const int64_t per = (nkb + splits - 1) / splits;
         splits = (int)((nkb + per - 1) / per);
     }
-    return splits;
+}
+
+template <int WN>
+void launch_wn(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
+               const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, int splits, int32_t* part,
+               hipStream_t stream) {
+    const unsigned tiles = (unsigned)(((M + kBM - 1) / kBM) * ((N + 128 * WN - 1) / (128 * WN)));
+    const dim3 grid(tiles * (unsigned)splits), block(kThreads);
+    if (x_rowsum)
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, true>), grid, block, 0, stream, pk, w_scale, xq, x_scale, x_rowsum,
+                           M, N, K, y, acc, splits, part);
+    else
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, false>), grid, block, 0, stream, pk, w_scale, xq, x_scale,
+                           x_rowsum, M, N, K, y, acc, splits, part);
 }
 
 }  // namespace
 
 size_t prefill_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    const int splits = prefill_splits(M, N, K);
+    int wn, splits;
+    prefill_plan(M, N, K, wn, splits);
     return splits > 1 ? (size_t)splits * (size_t)M * (size_t)N * sizeof(int32_t) : 0;
 }
 
@@ -345,18 +418,15 @@ hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const in
                               const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, void* ws,
                               size_t ws_bytes, hipStream_t stream) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    int splits = prefill_splits(M, N, K);
+    int wn, splits;
+    prefill_plan(M, N, K, wn, splits);
     // split-K needs the token sums and the workspace for the slices
     if (!x_rowsum || !ws || ws_bytes < (size_t)splits * M * N * sizeof(int32_t)) splits = 1;
     int32_t* part = splits > 1 ? static_cast<int32_t*>(ws) : nullptr;
-    const unsigned tiles = (unsigned)(((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN));
-    const dim3 grid(tiles * (unsigned)splits), block(kThreads);
-    if (x_rowsum)
-        hipLaunchKernelGGL((i2s_prefill_kernel<true>), grid, block, 0, stream, pk, w_scale, xq, x_scale, x_rowsum, M,
-                           N, K, y, acc, splits, part);
+    if (wn == 4)
+        launch_wn<4>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, splits, part, stream);
     else
-        hipLaunchKernelGGL((i2s_prefill_kernel<false>), grid, block, 0, stream, pk, w_scale, xq, x_scale, x_rowsum,
-                           M, N, K, y, acc, splits, part);
+        launch_wn<2>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, splits, part, stream);
     if (splits > 1) {
         const int64_t n4 = (int64_t)M * (N / 4);
         hipLaunchKernelGGL(prefill_splitk_finish, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, part,

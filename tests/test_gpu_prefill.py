@@ -43,6 +43,14 @@ def test_i2s_prefill_parity(M, N, K, rowsum):
     _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(4, M * 131 + N * 7 + K), rowsum=rowsum)
 
 
+@pytest.mark.parametrize("M,N,K", [(2048, 8192, 512), (2000, 8208, 320)])
+@pytest.mark.parametrize("rowsum", [True, False])
+def test_i2s_prefill_wide_tiles(M, N, K, rowsum):
+    # grids of at least one 128 x 512 tile per CU take the widest tile; K = 320 ends in a short block
+    _announce("i2s prefill wide tiles", M, N, K, rowsum)
+    _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(4, 7 * M + N + K), sample_rows=12, rowsum=rowsum)
+
+
 def test_i2s_prefill_extreme_values():
     _announce("i2s prefill extremes")
     import torch
