@@ -4,9 +4,11 @@ One step = one pass of the hot path over one batch of synthetic input through ev
 workload, in layer order: the q/k/v group, o, the gate/up group, down (for a stack of layers, every layer in
 turn; the layers hold copies of one packed layer in separate HBM buffers, so every byte is streamed).  Each group quantises its input
 activation per token (int8, absmax) and multiplies it by the group's packed ternary weights with the fused
-dequantisation epilogue.  Decode (M <= 16) runs each group as one fused launch (bitnet_mpgemm_fused); the
-separate-call path (bitnet_quantize_act + one bitnet_mpgemm per weight) is timed too and reported beside
-it.  Prefill (M > 16) runs the quantiser and the MFMA GEMM per weight.  Weights are ternarised and packed
+dequantisation epilogue.  Each group is one bitnet_mpgemm_fused call: at one token a single launch that also
+quantises; otherwise the quantiser, then one launch for all the group's weights (the decode GEMV for M <= 16,
+the MFMA GEMM over the weights' concatenated row tiles for M > 16).  Decode also times the separate-call path
+(bitnet_quantize_act + one bitnet_mpgemm per weight) and reports it beside the value; prefill times the fused
+GEMM launches alone (on the already quantised activations) for its roofline.  Weights are ternarised and packed
 once before timing (offline preprocessing); packed copies rotate so every step streams its weights from HBM
 rather than from the 256 MB Infinity Cache.
 
@@ -106,9 +108,11 @@ def main():
         rss.append(torch.empty(M, dtype=torch.int32, device=dev))
     ys = {n: torch.empty((M, by_name[n][1]), dtype=torch.float32, device=dev) for n in by_name}
     ws_bytes = max(B.bitnet_mpgemm_workspace_bytes(layout, M, N, K) for _, K, N in linears)
+    ws_bytes = max([ws_bytes] + [B.bitnet_mpgemm_fused_workspace_bytes(layout, [by_name[n][1] for n in g],
+                                                                       by_name[g[0]][0], M) for g in groups])
     ws = torch.zeros(max(16, ws_bytes), dtype=torch.uint8, device=dev)
     fargs = [[[B.FusedArgs([rot[c][l][n] for n in g], [scales[n] for n in g], [ys[n] for n in g]) for g in groups]
-              for l in range(n_layers)] for c in range(copies)] if decode else None
+              for l in range(n_layers)] for c in range(copies)]
     stream = torch.cuda.Stream()
     sptr = stream.cuda_stream
     # the set-up above ran on the default stream: the side stream starts after all of it
@@ -120,8 +124,9 @@ def main():
         for l in range(n_layers):
             for gi, g in enumerate(groups):
                 if path == "fused":
-                    B.bitnet_mpgemm_fused(layout, None, None, xs[gi], xqs[gi], sxs[gi], rss[gi], None, ws, sptr,
-                                          args=fargs[c][l][gi])
+                    # quantize=False: the products alone, on the activation the warm-up steps quantised
+                    B.bitnet_mpgemm_fused(layout, None, None, xs[gi] if quantize else None, xqs[gi], sxs[gi], rss[gi],
+                                          None, ws, sptr, args=fargs[c][l][gi])
                     continue
                 if quantize:
                     B.bitnet_quantize_act(xs[gi], xqs[gi], sxs[gi], rss[gi], sptr)
@@ -137,7 +142,7 @@ def main():
                 fn(args.warmup + i)
         return g
 
-    main_path = "fused" if decode else "separate"
+    main_path = "fused"
     with torch.cuda.stream(stream):
         for i in range(args.warmup):
             step(i, main_path)
@@ -146,10 +151,10 @@ def main():
     torch.cuda.synchronize()
 
     # Graphs: the K steps on the main path, the same steps on the separate-call path (decode), or the
-    # mpGEMM launches alone (prefill: the dominant kernel).
+    # fused GEMM launches alone (prefill: the dominant kernel).
     g_main = capture(lambda i: step(i, main_path))
     g_second = capture(lambda i: step(i, "separate")) if decode else \
-        capture(lambda i: step(i, "separate", quantize=False))
+        capture(lambda i: step(i, "fused", quantize=False))
     with torch.cuda.stream(stream):
         g_main.replay()
         g_second.replay()
@@ -195,10 +200,11 @@ def main():
     else:
         value = flops / (ms_per_step * 1e-3) / 1e12
         unit = "TOP/s"
-        launches = len(linears)
+        launches = len(groups) * n_layers
         avg_launch_ms = second_ms / launches
         achieved = (flops / launches) / (avg_launch_ms * 1e-3) / 1e12
-        roofline = {"bound": "mfma", "kernel": "i2s_prefill_kernel (bitnet_mpgemm, M > 16)",
+        roofline = {"bound": "mfma", "kernel": "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per "
+                                               "activation group)",
                     "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": None,
                     "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_ops": int(flops / launches),

@@ -121,19 +121,31 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
                             size_t ws_bytes, void* stream);
 
 /*
+ * Workspace bytes bitnet_mpgemm_fused needs to split K for these n_linears weights (host array N of rows, shared
+ * K, M tokens; 0 is a valid answer and 0 is also returned for invalid arguments).  A fused I2_S prefill launch
+ * (M > 16) splits K over all its weights at once, so this can exceed the largest bitnet_mpgemm_workspace_bytes of
+ * the weights; given less (but at least that largest one), the call runs without splitting.
+ */
+size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int64_t* N, int64_t K, int64_t M);
+
+/*
  * bitnet_mpgemm_fused -- one activation, several weights: bitnet_quantize_act followed by bitnet_mpgemm for
- * each weight, as one launch where possible (the decode step of the linears that read the same input, such
- * as q/k/v or gate/up).  Results are identical to those separate calls.
+ * each weight, as one launch where possible (the linears that read the same input, such as q/k/v or gate/up).
+ * Results are identical to those separate calls.
  *   n_linears                   1..8.
  *   packed, packed_bytes, w_scale, N, y
  *                               HOST arrays of n_linears entries: device packed buffer, its size, device beta,
  *                               rows of that weight, device fp32 output [M, N[i]].
- *   K, x, M                     the shared reduction length and the device fp32 activation [M, K].
+ *   K, x, M                     the shared reduction length and the device fp32 activation [M, K]; x may be
+ *                               NULL when xq, x_scale and x_rowsum already hold its quantised form (as written
+ *                               by bitnet_quantize_act): then they are inputs and only the products run.
  *   xq, x_scale, x_rowsum       device outputs as in bitnet_quantize_act (all three required).
- *   ws                          as for bitnet_mpgemm, at least the largest workspace of the n products.
- *   Shapes: 1 <= M <= 16; each weight as in bitnet_mpgemm.  I2_S with M == 1 and K <= 61440 runs as one launch
- *   (every work group quantises the row itself, keeping the codes in LDS); other I2_S cases run the quantiser
- *   and then all products in one launch; TL2 runs the quantiser and one launch per weight.
+ *   ws                          as for bitnet_mpgemm, at least the largest workspace of the n products
+ *                               (bitnet_mpgemm_fused_workspace_bytes lets a prefill launch split K).
+ *   Shapes: 1 <= M <= 2^24; each weight as in bitnet_mpgemm.  I2_S with M == 1 and K <= 61440 runs as one
+ *   launch (every work group quantises the row itself, keeping the codes in LDS); other I2_S cases run the
+ *   quantiser and then all products in one launch (the decode GEMV for M <= 16, the prefill GEMM over the
+ *   weights' concatenated row tiles above); TL2 runs the quantiser and one launch per weight.
  */
 bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* packed, const size_t* packed_bytes,
                                   const float* const* w_scale, const int64_t* N, int64_t K, const float* x,

@@ -37,6 +37,8 @@ _SIGNATURES = [
      [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    ("bitnet_mpgemm_fused_workspace_bytes", ctypes.c_size_t,
+     [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
     ("bitnet_mpgemm_fused", ctypes.c_int,
      [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
       ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -162,6 +164,12 @@ def bitnet_mpgemm(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=N
     _check("bitnet_mpgemm", st)
 
 
+def bitnet_mpgemm_fused_workspace_bytes(layout, Ns, K: int, M: int) -> int:
+    """Workspace bytes bitnet_mpgemm_fused needs to split K over the weights of rows Ns (a list) at M tokens."""
+    arr = (ctypes.c_int64 * len(Ns))(*Ns)
+    return int(lib().bitnet_mpgemm_fused_workspace_bytes(_layout(layout), len(Ns), arr, K, M))
+
+
 class FusedArgs:
     """Host arrays for bitnet_mpgemm_fused, built once so repeated calls only pass pointers."""
 
@@ -179,16 +187,18 @@ class FusedArgs:
 
 def bitnet_mpgemm_fused(layout, packed, w_scales, x, xq, x_scale, x_rowsum, ys, ws=None, stream=None,
                         args: FusedArgs = None) -> None:
-    """Quantise x (fp32 [M, K]) and multiply it by every packed weight (lists of equal length) in one call."""
+    """Quantise x (fp32 [M, K]) and multiply it by every packed weight (lists of equal length) in one call.
+    With x None, xq / x_scale / x_rowsum already hold the quantised activation and only the products run."""
     import torch
-    M, K = x.shape
+    M, K = (x if x is not None else xq).shape
     a = args if args is not None else FusedArgs(packed, w_scales, ys)
     if a.n < 1:
         raise ValueError("bitnet_mpgemm_fused needs at least one weight")
     ws_ptr = _ptr(ws, "ws") if ws is not None else None
     ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
     st = lib().bitnet_mpgemm_fused(_layout(layout), a.n, a.packed, a.packed_bytes, a.w_scale, a.N, K,
-                                   _ptr(x, "x", torch.float32), M, _ptr(xq, "xq", torch.int8),
+                                   _ptr(x, "x", torch.float32) if x is not None else None, M,
+                                   _ptr(xq, "xq", torch.int8),
                                    _ptr(x_scale, "x_scale", torch.float32), _ptr(x_rowsum, "x_rowsum", torch.int32),
                                    a.y, ws_ptr, ws_bytes, _stream(stream))
     _check("bitnet_mpgemm_fused", st)

@@ -31,8 +31,8 @@ bitnet_status hip_status(hipError_t e, const char* what) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-constexpr int64_t kMaxK = 132096;
-constexpr int64_t kDecodeMaxTokens = 16;   // up to 16 tokens fill the rows of one 16x16x64 MFMA   // 127 * K < 2^24: accumulators stay exact in fp32
+constexpr int64_t kMaxK = 132096;          // 127 * K < 2^24: accumulators stay exact in fp32
+constexpr int64_t kDecodeMaxTokens = 16;   // up to 16 tokens fill the rows of one 16x16x64 MFMA
 
 bool weight_shape_ok(int64_t N, int64_t K) {
     return N > 0 && K > 0 && N % bitnet::kRowsPerGroup == 0 && K % bitnet::kSubK == 0 && K <= kMaxK &&
@@ -46,6 +46,18 @@ size_t packed_bytes_of(int layout, int64_t N, int64_t K) {
     const int64_t three = (K / bitnet::kTl2BlockK) * bitnet::kTl2BlockK;
     const int64_t two = K - three;
     return (size_t)N * three / 6 + (size_t)N * three / 24 + (size_t)N * two / 4;
+}
+
+bitnet::FusedLinears one_linear(const void* packed, const float* w_scale, int64_t N, float* y, int32_t* acc) {
+    bitnet::FusedLinears L{};
+    L.count = 1;
+    L.packed[0] = static_cast<const uint8_t*>(packed);
+    L.w_scale[0] = w_scale;
+    L.y[0] = y;
+    L.acc[0] = acc;
+    L.N[0] = (int)N;
+    bitnet::seal_fused(L);
+    return L;
 }
 
 }  // namespace
@@ -95,8 +107,28 @@ bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* 
 
 size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K) {
     if (!layout_ok(layout) || !weight_shape_ok(N, K) || M < 1) return 0;
-    if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens) return bitnet::prefill_workspace_bytes(M, N, K);
+    if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens)
+        return bitnet::prefill_workspace_bytes(one_linear(nullptr, nullptr, N, nullptr, nullptr), M, K);
     return 0;
+}
+
+size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int64_t* N, int64_t K, int64_t M) {
+    if (!layout_ok(layout) || !N || n_linears < 1 || n_linears > bitnet::kMaxFused || M < 1) return 0;
+    for (int i = 0; i < n_linears; ++i)
+        if (!weight_shape_ok(N[i], K)) return 0;
+    if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens) {
+        bitnet::FusedLinears L{};
+        L.count = n_linears;
+        for (int i = 0; i < n_linears; ++i) L.N[i] = (int)N[i];
+        bitnet::seal_fused(L);
+        return bitnet::prefill_workspace_bytes(L, M, K);
+    }
+    size_t need = 0;
+    for (int i = 0; i < n_linears; ++i) {
+        const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
+        need = w > need ? w : need;
+    }
+    return need;
 }
 
 bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale, int64_t N,
@@ -122,20 +154,13 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
     if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
 
     hipStream_t s = (hipStream_t)stream;
-    if (layout == BITNET_LAYOUT_I2S && M <= kDecodeMaxTokens) {
-        bitnet::FusedLinears L{};
-        L.count = 1;
-        L.packed[0] = static_cast<const uint8_t*>(packed);
-        L.w_scale[0] = w_scale;
-        L.y[0] = y;
-        L.acc[0] = acc;
-        L.N[0] = (int)N;
-        bitnet::seal_fused(L);
-        return hip_status(bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s), "bitnet_mpgemm launch");
-    }
+    if (layout == BITNET_LAYOUT_I2S && M <= kDecodeMaxTokens)
+        return hip_status(bitnet::launch_i2s_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
+                                                    (int)M, (int)K, s),
+                          "bitnet_mpgemm launch");
     if (layout == BITNET_LAYOUT_I2S)
-        return hip_status(bitnet::launch_i2s_prefill(packed, w_scale, xq, x_scale, x_rowsum, (int)M, (int)N, (int)K, y,
-                                                     acc, ws, ws_bytes, s),
+        return hip_status(bitnet::launch_i2s_prefill(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
+                                                     (int)M, (int)K, ws, ws_bytes, s),
                           "bitnet_mpgemm launch");
     const int64_t slice = bitnet::kElutMaxTokens;
     for (int64_t m0 = 0; m0 < M; m0 += slice) {
@@ -154,9 +179,10 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
     if (n_linears < 1 || n_linears > bitnet::kMaxFused)
         return fail(BITNET_E_INVALID, "n_linears must be 1..%d; got %d", bitnet::kMaxFused, n_linears);
-    if (!packed || !packed_bytes || !w_scale || !N || !y || !x || !xq || !x_scale || !x_rowsum)
+    if (!packed || !packed_bytes || !w_scale || !N || !y || !xq || !x_scale || !x_rowsum)
         return fail(BITNET_E_INVALID, "null pointer argument");
-    if (M < 1 || M > kDecodeMaxTokens) return fail(BITNET_E_SHAPE, "fused decode needs 1 <= M <= 16; got %lld", (long long)M);
+    const bool quantise = x != nullptr;       // NULL x: xq, x_scale and x_rowsum already hold the activation
+    if (M < 1 || M > ((int64_t)1 << 24)) return fail(BITNET_E_SHAPE, "need 1 <= M <= 2^24; got M=%lld", (long long)M);
     if (!aligned(x, 16) || !aligned(xq, 16) || !aligned(x_scale, 4) || !aligned(x_rowsum, 4))
         return fail(BITNET_E_ALIGN, "x and xq need 16-byte alignment, x_scale and x_rowsum 4-byte");
     size_t need = 0;
@@ -169,9 +195,14 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
         if (packed_bytes[i] < packed_bytes_of(layout, N[i], K))
             return fail(BITNET_E_INVALID, "weight %d: packed buffer holds %zu bytes, %zu needed", i, packed_bytes[i],
                         packed_bytes_of(layout, N[i], K));
+        if (layout == BITNET_LAYOUT_I2S && ((uint64_t)N[i] * (uint64_t)K >= ((uint64_t)1 << 32) ||
+                                            (uint64_t)M * (uint64_t)K >= ((uint64_t)1 << 32)))
+            return fail(BITNET_E_SHAPE, "weight %d: I2_S needs N*K and M*K below 2^32", i);
         const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
         need = w > need ? w : need;
     }
+    // a fused prefill launch splits K only where ws holds the slices of all its weights; the largest single
+    // workspace is always enough for the call to run
     if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "workspace needs %zu bytes", need);
     if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
 
@@ -190,15 +221,18 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
         }
         if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
         bitnet::seal_fused(L);
-        if (M == 1 && K <= bitnet::kFusedMaxK)      // one launch: quantise inside every work group
+        if (quantise && M == 1 && K <= bitnet::kFusedMaxK)   // one launch: quantise inside every work group
             return hip_status(bitnet::launch_i2s_gemv1_stream(L, x, (int)K, xq, x_scale, x_rowsum, s),
                               "bitnet_mpgemm_fused launch");
-        hipError_t e = bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s);
-        if (e == hipSuccess) e = bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s);
+        hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
+        if (e == hipSuccess)
+            e = M <= kDecodeMaxTokens
+                    ? bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s)
+                    : bitnet::launch_i2s_prefill(L, xq, x_scale, x_rowsum, (int)M, (int)K, ws, ws_bytes, s);
         return hip_status(e, "bitnet_mpgemm_fused launch");
     }
     // TL2: the quantiser once, then one table-lookup launch per weight.
-    hipError_t e = bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s);
+    hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
     if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm_fused launch");
     for (int i = 0; i < n_linears; ++i) {
         const bitnet_status st = bitnet_mpgemm(layout, packed[i], packed_bytes[i], w_scale[i], N[i], K, xq, x_scale,

@@ -110,13 +110,8 @@ size_t pack_workspace_bytes();
 hipError_t launch_pack(int layout, const float* W, int64_t N, int64_t K, void* packed, float* w_scale,
                        void* ws, hipStream_t stream);
 
-// Prefill (M > 16): split-K over the workspace when it is given and large enough (and x_rowsum is given).
 constexpr int kMaxSplits = 16;
 int device_cus();
-size_t prefill_workspace_bytes(int64_t M, int64_t N, int64_t K);
-hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                              const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, void* ws,
-                              size_t ws_bytes, hipStream_t stream);
 
 // Up to kMaxFused weights that read the same activation, served by one decode launch.
 constexpr int kMaxFused = 8;
@@ -141,6 +136,11 @@ inline void seal_fused(FusedLinears& L) {
     L.total = (int)rgs;
     for (int i = L.count; i <= kMaxFused; ++i) L.rg_start[i] = i == L.count ? L.total : 0x7fffffff;
 }
+// Prefill (M > 16): one launch for up to kMaxFused weights that read the same activation; split-K over the
+// workspace when it is given and large enough (and x_rowsum is given).
+size_t prefill_workspace_bytes(const FusedLinears& L, int64_t M, int64_t K);
+hipError_t launch_i2s_prefill(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
+                              int M, int K, void* ws, size_t ws_bytes, hipStream_t stream);
 constexpr int64_t kFusedMaxK = 61440;   // single-token fused quantise+GEMV keeps the K codes in LDS
 hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                              int M, int K, hipStream_t stream);

@@ -52,11 +52,33 @@ __device__ __forceinline__ int byte_sum(const v4i& v, int acc) {
     return __builtin_amdgcn_sdot4(v.w, ones, acc, false);
 }
 
+// The weights of one launch: each owns a run of weight tiles (tile_start), its own rows, beta and outputs, and
+// its slice of a split-K partial buffer (part_off; a slice holds M x sum N).
+struct PrefillLinears {
+    const uint8_t* packed[kMaxFused];
+    const float* w_scale[kMaxFused];
+    float* y[kMaxFused];
+    int32_t* acc[kMaxFused];
+    long long part_off[kMaxFused];
+    int N[kMaxFused];
+    int tile_start[kMaxFused + 1];   // first weight tile of each linear; INT_MAX past the last
+    int tile_start_lo[kMaxFused];     // the same, 0 past the last (the value subtracted)
+    int tiles_n;                      // weight tiles of the launch
+    long long n_total;                // sum of N
+};
+
+template <typename T>
+__device__ __forceinline__ T pick_linear(const T (&a)[kMaxFused], int li) {
+    T v = a[0];
+#pragma unroll
+    for (int i = 1; i < kMaxFused; ++i) v = li == i ? a[i] : v;
+    return v;
+}
+
 template <int WN, bool HAS_RS>
 __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads) void i2s_prefill_kernel(
-    const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
-    const float* __restrict__ x_scale, const int32_t* __restrict__ x_rowsum, int M, int N, int K,
-    float* __restrict__ y, int32_t* __restrict__ acc_out, int splits, int32_t* __restrict__ part) {
+    PrefillLinears P, const int8_t* __restrict__ xq, const float* __restrict__ x_scale,
+    const int32_t* __restrict__ x_rowsum, int M, int K, int splits, int32_t* __restrict__ part_all) {
     constexpr int MT = 2, NT = 4;                                 // 32 x 32 MFMA tiles per wave
     constexpr int WK = 4 / WN;                                    // K-groups: waves sharing one output tile
     constexpr int kBN = 128 * WN;
@@ -76,7 +98,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     const int wm = wave & 1, wn = (wave >> 1) % WN, wk = (wave >> 1) / WN;
     const int j32 = lane & 31, h = lane >> 5;
     const int tiles_m = (M + kBM - 1) / kBM;
-    const int tiles_n = (N + kBN - 1) / kBN;
+    const int tiles_n = P.tiles_n;
     // split-K: the launch is `splits` slices of tiles; slice `split` takes stages [kb_lo, kb_hi)
     const int ntiles = gridDim.x / splits;
     const int split = blockIdx.x / ntiles;
@@ -85,7 +107,18 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     const int gsize = kGroupM * tiles_n;
     const int g = L / gsize, gl = L - g * gsize;
     const int gm = (tiles_m - g * kGroupM) < kGroupM ? (tiles_m - g * kGroupM) : kGroupM;
-    const int tm = g * kGroupM + gl % gm, tn = gl / gm;
+    const int tm = g * kGroupM + gl % gm, tn_all = gl / gm;
+    // the weight this tile belongs to (uniform: a scalar compare chain over the fixed maximum)
+    int li = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxFused; ++i) li = tn_all >= P.tile_start[i] ? i : li;
+    const int tn = tn_all - pick_linear(P.tile_start_lo, li);
+    const int N = pick_linear(P.N, li);
+    const uint8_t* __restrict__ packed = pick_linear(P.packed, li);
+    const float* __restrict__ w_scale = pick_linear(P.w_scale, li);
+    float* __restrict__ y = pick_linear(P.y, li);
+    int32_t* __restrict__ acc_out = pick_linear(P.acc, li);
+    int32_t* __restrict__ part = part_all ? part_all + pick_linear(P.part_off, li) : nullptr;
     const int m0 = tm * kBM, n0 = tn * kBN;
     const int nkb = (K + kBK - 1) / kBK;
     const int nfull = K / kBK;
@@ -301,7 +334,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     if (part) {
         // split-K: this slice's exact partial sums (the code offset and the scales are applied when the slices
         // are summed)
-        int32_t* pp = part + (size_t)split * M * N;
+        int32_t* pp = part + (size_t)split * M * P.n_total;
 #pragma unroll
         for (int mi = 0; mi < MT; ++mi)
 #pragma unroll
@@ -344,10 +377,11 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     }
 }
 
-// Sum of the split-K slices, then the epilogue: y = (sum - sum_k xq[m, k]) * (beta / s_m).  Four outputs of
-// one row per thread.
-__global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __restrict__ part, int splits, int M,
-                                                             int N, const int32_t* __restrict__ x_rowsum,
+// Sum of the split-K slices of one weight (its M x N block in every slice of `slice` words), then the epilogue:
+// y = (sum - sum_k xq[m, k]) * (beta / s_m).  Four outputs of one row per thread.
+__global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __restrict__ part, int64_t slice,
+                                                             int splits, int M, int N,
+                                                             const int32_t* __restrict__ x_rowsum,
                                                              const float* __restrict__ x_scale,
                                                              const float* __restrict__ w_scale, float* __restrict__ y,
                                                              int32_t* __restrict__ acc_out) {
@@ -357,7 +391,7 @@ __global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __re
     const int m = (int)(i4 / n4);
     const size_t off = (size_t)i4 * 4;
     v4i t = *reinterpret_cast<const v4i*>(part + off);
-    for (int sp = 1; sp < splits; ++sp) t += *reinterpret_cast<const v4i*>(part + (size_t)sp * M * N + off);
+    for (int sp = 1; sp < splits; ++sp) t += *reinterpret_cast<const v4i*>(part + (size_t)sp * slice + off);
     const int rs = x_rowsum[m];
     t -= (v4i){rs, rs, rs, rs};
     const float sc = *w_scale / x_scale[m];
@@ -370,16 +404,20 @@ __global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __re
     if (acc_out) *reinterpret_cast<v4i*>(acc_out + off) = t;
 }
 
-// Tile width and split-K factor.  The 128 x 512 tile where its grid gives every CU a work group, else the
-// 128 x 256 one (two K-groups per tile).  Splitting K keeps still smaller grids busy: it aims at one work group per
-// CU, with at least two 256-k stages per slice, and only for grids that leave at least half the CUs idle (the
-// slices' extra pass over M x N costs more elsewhere).
-void prefill_plan(int64_t M, int64_t N, int64_t K, int& wn, int& splits) {
+// Tile width and split-K factor for the weight tiles of a launch.  The 128 x 512 tile where its grid gives every
+// CU a work group, else the 128 x 256 one (two K-groups per tile).  Splitting K keeps still smaller grids busy: it
+// aims at one work group per CU, with at least two 256-k stages per slice, and only for grids that leave at least
+// half the CUs idle (the slices' extra pass over M x N costs more elsewhere).
+void prefill_plan(const FusedLinears& L, int64_t M, int64_t K, int& wn, int& splits) {
     const int64_t cus = device_cus();
     const int64_t tiles_m = (M + kBM - 1) / kBM;
-    const int64_t t4 = tiles_m * ((N + 511) / 512);
-    wn = t4 >= cus ? 4 : 2;
-    const int64_t tiles = wn == 4 ? t4 : tiles_m * ((N + 255) / 256);
+    int64_t n4 = 0, n2 = 0;
+    for (int i = 0; i < L.count; ++i) {
+        n4 += (L.N[i] + 511) / 512;
+        n2 += (L.N[i] + 255) / 256;
+    }
+    wn = tiles_m * n4 >= cus ? 4 : 2;
+    const int64_t tiles = tiles_m * (wn == 4 ? n4 : n2);
     const int64_t nkb = (K + kBK - 1) / kBK;
     int64_t sp = 2 * tiles <= cus ? (cus + tiles - 1) / tiles : 1;
     if (sp > nkb / 2) sp = nkb / 2;
@@ -392,45 +430,83 @@ void prefill_plan(int64_t M, int64_t N, int64_t K, int& wn, int& splits) {
     }
 }
 
+int64_t total_rows(const FusedLinears& L) {
+    int64_t n = 0;
+    for (int i = 0; i < L.count; ++i) n += L.N[i];
+    return n;
+}
+
 template <int WN>
-void launch_wn(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
-               const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, int splits, int32_t* part,
-               hipStream_t stream) {
-    const unsigned tiles = (unsigned)(((M + kBM - 1) / kBM) * ((N + 128 * WN - 1) / (128 * WN)));
-    const dim3 grid(tiles * (unsigned)splits), block(kThreads);
+void launch_wn(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int M, int K,
+               int splits, int32_t* part, hipStream_t stream) {
+    PrefillLinears P{};
+    int tiles = 0;
+    long long off = 0;
+    for (int i = 0; i < kMaxFused; ++i) {
+        if (i < L.count) {
+            P.packed[i] = L.packed[i];
+            P.w_scale[i] = L.w_scale[i];
+            P.y[i] = L.y[i];
+            P.acc[i] = L.acc[i];
+            P.N[i] = L.N[i];
+            P.part_off[i] = off;
+            P.tile_start[i] = tiles;
+            P.tile_start_lo[i] = tiles;
+            off += (long long)M * L.N[i];
+            tiles += (L.N[i] + 128 * WN - 1) / (128 * WN);
+        } else {
+            P.packed[i] = L.packed[0];
+            P.w_scale[i] = L.w_scale[0];
+            P.y[i] = L.y[0];
+            P.acc[i] = L.acc[0];
+            P.N[i] = L.N[0];
+            P.part_off[i] = 0;
+            P.tile_start[i] = 0x7fffffff;
+            P.tile_start_lo[i] = 0;
+        }
+    }
+    P.tile_start[kMaxFused] = 0x7fffffff;
+    P.tiles_n = tiles;
+    P.n_total = total_rows(L);
+    const unsigned grid_tiles = (unsigned)(((M + kBM - 1) / kBM) * tiles);
+    const dim3 grid(grid_tiles * (unsigned)splits), block(kThreads);
     if (x_rowsum)
-        hipLaunchKernelGGL((i2s_prefill_kernel<WN, true>), grid, block, 0, stream, pk, w_scale, xq, x_scale, x_rowsum,
-                           M, N, K, y, acc, splits, part);
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, true>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M, K,
+                           splits, part);
     else
-        hipLaunchKernelGGL((i2s_prefill_kernel<WN, false>), grid, block, 0, stream, pk, w_scale, xq, x_scale,
-                           x_rowsum, M, N, K, y, acc, splits, part);
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, false>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M, K,
+                           splits, part);
 }
 
 }  // namespace
 
-size_t prefill_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+size_t prefill_workspace_bytes(const FusedLinears& L, int64_t M, int64_t K) {
     int wn, splits;
-    prefill_plan(M, N, K, wn, splits);
-    return splits > 1 ? (size_t)splits * (size_t)M * (size_t)N * sizeof(int32_t) : 0;
+    prefill_plan(L, M, K, wn, splits);
+    return splits > 1 ? (size_t)splits * (size_t)M * (size_t)total_rows(L) * sizeof(int32_t) : 0;
 }
 
-hipError_t launch_i2s_prefill(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                              const int32_t* x_rowsum, int M, int N, int K, float* y, int32_t* acc, void* ws,
-                              size_t ws_bytes, hipStream_t stream) {
-    const uint8_t* pk = static_cast<const uint8_t*>(packed);
+hipError_t launch_i2s_prefill(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
+                              int M, int K, void* ws, size_t ws_bytes, hipStream_t stream) {
     int wn, splits;
-    prefill_plan(M, N, K, wn, splits);
+    prefill_plan(L, M, K, wn, splits);
+    const int64_t ntot = total_rows(L);
     // split-K needs the token sums and the workspace for the slices
-    if (!x_rowsum || !ws || ws_bytes < (size_t)splits * M * N * sizeof(int32_t)) splits = 1;
+    if (!x_rowsum || !ws || ws_bytes < (size_t)splits * M * ntot * sizeof(int32_t)) splits = 1;
     int32_t* part = splits > 1 ? static_cast<int32_t*>(ws) : nullptr;
     if (wn == 4)
-        launch_wn<4>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, splits, part, stream);
+        launch_wn<4>(L, xq, x_scale, x_rowsum, M, K, splits, part, stream);
     else
-        launch_wn<2>(pk, w_scale, xq, x_scale, x_rowsum, M, N, K, y, acc, splits, part, stream);
+        launch_wn<2>(L, xq, x_scale, x_rowsum, M, K, splits, part, stream);
     if (splits > 1) {
-        const int64_t n4 = (int64_t)M * (N / 4);
-        hipLaunchKernelGGL(prefill_splitk_finish, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, part,
-                           splits, M, N, x_rowsum, x_scale, w_scale, y, acc);
+        int64_t off = 0;
+        for (int i = 0; i < L.count; ++i) {
+            const int64_t n4 = (int64_t)M * (L.N[i] / 4);
+            hipLaunchKernelGGL(prefill_splitk_finish, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream,
+                               part + off, (int64_t)M * ntot, splits, M, L.N[i], x_rowsum, x_scale, L.w_scale[i],
+                               L.y[i], L.acc[i]);
+            off += (int64_t)M * L.N[i];
+        }
     }
     return hipGetLastError();
 }

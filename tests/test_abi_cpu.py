@@ -117,3 +117,15 @@ def test_status_strings():
     for st in range(7):
         assert B.bitnet_status_string(st)
     assert B.bitnet_status_string(99) == "unknown status"
+
+
+def test_fused_workspace_query():
+    # decode needs no workspace; a fused prefill split holds whole M x sum(N) int32 slices; bad input gives 0
+    assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [4096, 1024, 1024], 4096, 8) == 0
+    for M, Ns, K in [(512, [4096, 1024, 1024], 4096), (40, [48, 16, 64], 832), (300, [3200] * 3, 3200)]:
+        w = B.bitnet_mpgemm_fused_workspace_bytes("i2s", Ns, K, M)
+        assert w % (M * sum(Ns) * 4) == 0
+        assert w >= max(B.bitnet_mpgemm_workspace_bytes("i2s", M, N, K) for N in Ns)
+    assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [4096, 1000], 4096, 512) == 0
+    assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [], 4096, 512) == 0
+    assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [64] * 9, 256, 512) == 0
