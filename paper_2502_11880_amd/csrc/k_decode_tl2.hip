@@ -104,6 +104,8 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        // Lookups without branches: tokens past M (MT > M) read token 0's tables and are never stored, so all
+        // 32 x MT reads of a lane can be in flight together (a guarded read per triple waits for each one).
         const uint8_t* base = lut + skewed_slot(32 * q) * kSlot;
 #pragma unroll
         for (int i = 0; i < 32; ++i) {
@@ -112,8 +114,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
             const int msk = -(int)((sw >> i) & 1u);
             const uint8_t* e = base + i * kSlot + 2 * idx;
 #pragma unroll
-            for (int m = 0; m < MT; ++m)
-                if (m < M) acc[m] += lds_i16(e + m * kTokenStride) ^ msk;
+            for (int m = 0; m < MT; ++m) acc[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride) ^ msk;
         }
         const int nneg = __popc(sw);
 #pragma unroll
@@ -146,8 +147,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
                 const int code = (int)((word >> (4 * i)) & 15u);
                 const uint8_t* e = lut + (8 * q + i) * kSlot + 2 * code;
 #pragma unroll
-                for (int m = 0; m < MT; ++m)
-                    if (m < M) acc[m] += lds_i16(e + m * kTokenStride);
+                for (int m = 0; m < MT; ++m) acc[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride);
             }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
             __builtin_amdgcn_wave_barrier();
