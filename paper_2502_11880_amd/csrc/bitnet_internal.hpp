@@ -126,6 +126,29 @@ struct FusedLinears {
     int total;                     // row groups in the launch
 };
 
+// Which weight the launch's row group g belongs to, and its row group within that weight.  The bounds are
+// increasing (INT_MAX past the last weight), so a compare-and-select chain over the fixed maximum finds it; for a
+// uniform g it is all scalar.
+__device__ __forceinline__ void locate(const FusedLinears& L, int g, int& li, int& rg) {
+    int l = 0, start = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxFused; ++i) {
+        const int st = L.rg_start[i];
+        l = g >= st ? i : l;
+        start = g >= st ? st : start;
+    }
+    li = l;
+    rg = g - start;
+}
+
+template <typename T>
+__device__ __forceinline__ T pick(const T (&a)[kMaxFused], int li) {
+    T v = a[0];
+#pragma unroll
+    for (int i = 1; i < kMaxFused; ++i) v = li == i ? a[i] : v;
+    return v;
+}
+
 // Fill the launch totals once the first `count` entries are set.
 inline void seal_fused(FusedLinears& L) {
     int64_t rgs = 0;
@@ -153,5 +176,10 @@ hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, cons
                                   const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
                                   hipStream_t stream);
 hipError_t launch_elut_tables(const int8_t* xq, int M, int K, int16_t* lut, int16_t* lut1, hipStream_t stream);
+// One token, TL2, every weight of a group in one launch; x (fp32) is quantised inside, or, when x is NULL, xq is
+// read.  Only where the whole row's tables fit in LDS (tl2_stream_fits); the caller falls back otherwise.
+bool tl2_stream_fits(int K);
+hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                             int32_t* x_rowsum, hipStream_t stream);
 
 }  // namespace bitnet

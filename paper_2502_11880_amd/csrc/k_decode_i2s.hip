@@ -39,29 +39,6 @@ __device__ __forceinline__ int wave_sum(int v) {
     return v;
 }
 
-// Which weight the launch's row group g belongs to, and its row group within that weight.  The bounds are
-// increasing (INT_MAX past the last weight), so a compare-and-select chain over the fixed maximum finds it; for a
-// uniform g it is all scalar.
-__device__ __forceinline__ void locate(const FusedLinears& L, int g, int& li, int& rg) {
-    int l = 0, start = 0;
-#pragma unroll
-    for (int i = 1; i < kMaxFused; ++i) {
-        const int st = L.rg_start[i];
-        l = g >= st ? i : l;
-        start = g >= st ? st : start;
-    }
-    li = l;
-    rg = g - start;
-}
-
-template <typename T>
-__device__ __forceinline__ T pick(const T (&a)[kMaxFused], int li) {
-    T v = a[0];
-#pragma unroll
-    for (int i = 1; i < kMaxFused; ++i) v = li == i ? a[i] : v;
-    return v;
-}
-
 // Words per lane of block kb: 4 for a full 256-k block, (K mod 256) / 64 for a short last one.
 __device__ __forceinline__ int block_T(int kb, int nfull, int Tlast) { return kb < nfull ? 4 : Tlast; }
 

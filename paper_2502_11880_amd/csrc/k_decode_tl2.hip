@@ -18,6 +18,7 @@
 #include "bitnet_internal.hpp"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace bitnet {
 namespace {
@@ -183,6 +184,228 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
     }
 }
 
+// One token, streaming (Algorithm TL2 with the table build amortised over every row the work group visits).
+// Each persistent work group quantises the token row once (Sec. 2.1; or reads the codes when they are given), then
+// every wave builds the tables of its own 384-k blocks once: 14 int16 sums in a 28-byte slot per triple, 132
+// slots per block (a one-slot skew after every 32 triples puts the four lane quarters on disjoint banks), and the
+// wave holding the TL1 tail builds its pair tables.  The work group then walks the row groups g = blockIdx.x +
+// j gridDim.x of all the launch's weights: the next row group's index and sign words are loaded while the current
+// one is looked up, and one barrier per row group reduces the waves' sums (double-buffered) for the epilogue.
+constexpr int kSlot28 = 28;                                  // 14 int16 per triple table
+constexpr int kBlockBytes28 = (kTl2BlockK / 3 + 4) * kSlot28;
+constexpr int kMaxUnits = kTl2BlockK / kSubK - 1;            // TL1 tail: at most 5 units of 64 k
+
+__device__ __forceinline__ void store_words(uint8_t* slot, const uint32_t* w, int n) {
+    for (int i = 0; i < n; ++i) reinterpret_cast<uint32_t*>(slot)[i] = w[i];
+}
+
+template <int WAVES, int U, int XV, bool QUANT>
+__global__ __launch_bounds__(64 * WAVES) void tl2_stream_kernel(FusedLinears L, const float* __restrict__ x, int K,
+                                                                int8_t* __restrict__ xq, float* __restrict__ x_scale,
+                                                                int32_t* __restrict__ x_rowsum) {
+    extern __shared__ __align__(16) uint8_t lds[];    // codes | block tables | pair tables
+    __shared__ int part[2][WAVES][16];
+    __shared__ float redf[WAVES];
+    __shared__ int redi[WAVES];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int q = lane >> 4, r = lane & 15;
+    const int G = gridDim.x, bid = blockIdx.x;
+    const int three = (K / kTl2BlockK) * kTl2BlockK;
+    const int nblk = three / kTl2BlockK;
+    const int units = (K - three) / kSubK;
+    const int tail_wave = nblk % WAVES;                        // a wave with the fewest blocks
+    uint8_t* codes = lds;
+    uint8_t* tables = lds + ((K + 15) & ~15);
+    uint8_t* pairs = tables + (size_t)nblk * kBlockBytes28;
+    const int S = (L.total - bid + G - 1) / G;                 // row groups of this work group (grid <= total)
+
+    // the loads of row group step st (all unconditional: a conditional load shape makes the compiler wait for
+    // every load in flight where the paths join); blocks past nblk and tail units past `units` repeat real ones
+    auto issue = [&](v4u (&iw)[U], uint32_t (&sw)[U], uint32_t (&tw)[kMaxUnits], float& bw, int st) {
+        int li, rg;
+        locate(L, bid + st * G, li, rg);
+        const size_t Nl = (size_t)pick(L.N, li);
+        const uint8_t* idx_plane = pick(L.packed, li);
+        const uint8_t* sign_plane = idx_plane + Nl * (three / 6);
+        const uint8_t* tail_plane = sign_plane + Nl * (three / 24);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const size_t tile = (size_t)rg * nblk + min(wave + WAVES * u, nblk - 1);
+            iw[u] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * lane));
+            sw[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * lane));
+        }
+        // without a tail the words are read from the start of the index plane instead (never used)
+        const int um = units > 0 ? units : 1;
+        const uint8_t* tail_base = units > 0 ? tail_plane : idx_plane;
+        const size_t tail_row = units > 0 ? ((size_t)rg * 64 * um + (size_t)lane * um) : 0;
+#pragma unroll
+        for (int t = 0; t < kMaxUnits; ++t)
+            tw[t] = *reinterpret_cast<const uint32_t*>(tail_base + (tail_row + (units > 0 ? min(t, um - 1) : 0)) * 4);
+        bw = *pick(L.w_scale, li);
+    };
+
+    auto run = [&](auto multi) {
+        constexpr bool kMulti = decltype(multi)::value;
+        // 1. the activation row, the first row groups' weights, then the quantisation (or the given codes)
+        const float4* x4 = reinterpret_cast<const float4*>(x);
+        const int K4 = K >> 2;
+        float4 xv[XV];
+        if (QUANT) {
+#pragma unroll
+            for (int i = 0; i < XV; ++i) {
+                const int e = tid + i * 64 * WAVES;
+                const float4 v = x4[e < K4 ? e : K4 - 1];
+                xv[i] = e < K4 ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+        }
+        v4u iwa[U], iwb[U];
+        uint32_t swa[U], swb[U], twa[kMaxUnits], twb[kMaxUnits];
+        float ba = 0.0f, bb = 0.0f;
+        issue(iwa, swa, twa, ba, 0);
+        if constexpr (kMulti) issue(iwb, swb, twb, bb, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        float sx;
+        if (QUANT) {
+            float amax = 0.0f;
+#pragma unroll
+            for (int i = 0; i < XV; ++i)
+                amax = fmaxf(amax, fmaxf(fmaxf(fabsf(xv[i].x), fabsf(xv[i].y)), fmaxf(fabsf(xv[i].z), fabsf(xv[i].w))));
+            amax = wave_max_all(amax);
+            if (lane == 0) redf[wave] = amax;
+            __syncthreads();
+            amax = redf[0];
+#pragma unroll
+            for (int w = 1; w < WAVES; ++w) amax = fmaxf(amax, redf[w]);
+            sx = 127.0f / fmaxf(amax, 1e-5f);
+            int sum = 0;
+#pragma unroll
+            for (int i = 0; i < XV; ++i) {
+                const int e = tid + i * 64 * WAVES;
+                if (e < K4) {
+                    const uint32_t c = quant4(xv[i], sx);
+                    sum = byte_sum4(c, sum);
+                    reinterpret_cast<uint32_t*>(codes)[e] = c;
+                    if (bid == 0) reinterpret_cast<uint32_t*>(xq)[e] = c;
+                }
+            }
+            sum = wave_sum_all(sum);
+            if (lane == 0) redi[wave] = sum;
+        } else {
+            for (int e = tid; e < K4; e += 64 * WAVES)
+                reinterpret_cast<uint32_t*>(codes)[e] = reinterpret_cast<const uint32_t*>(xq)[e];
+            sx = x_scale[0];
+        }
+        __syncthreads();                                   // every code (and every wave's code sum) is in LDS
+        if (QUANT && bid == 0 && tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < WAVES; ++w) tot += redi[w];
+            x_scale[0] = sx;
+            x_rowsum[0] = tot;
+        }
+
+        // 2. this wave's tables, once: lane builds triples lane and lane + 64 of each of its blocks
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int blk = wave + WAVES * u;
+            if (blk < nblk) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int g = lane + 64 * h;
+                    const int8_t* a = reinterpret_cast<const int8_t*>(codes) + blk * kTl2BlockK + 3 * g;
+                    uint32_t w[8];
+                    triple_table(a[0], a[1], a[2], w);
+                    store_words(tables + blk * kBlockBytes28 + skewed_slot(g) * kSlot28, w, 7);
+                }
+            }
+        }
+        if (wave == tail_wave && lane < 32) {
+            for (int t = 0; t < units; ++t) {
+                const int8_t* b = reinterpret_cast<const int8_t*>(codes) + three + kSubK * t + 2 * lane;
+                uint32_t w[8];
+                pair_table(b[0], b[1], w);
+                store_words(pairs + (t * 32 + lane) * kSlot28, w, 5);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+
+        // 3. the stream
+        int par = 0;
+        auto compute = [&](const v4u (&iw)[U], const uint32_t (&sw)[U], const uint32_t (&tw)[kMaxUnits], float bw,
+                           int st) {
+            int acc = 0;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int blk = wave + WAVES * u;
+                if (blk < nblk) {
+                    const uint8_t* base = tables + blk * kBlockBytes28 + skewed_slot(32 * q) * kSlot28;
+#pragma unroll
+                    for (int i = 0; i < 32; ++i) {
+                        const uint32_t word = i < 8 ? iw[u].x : i < 16 ? iw[u].y : i < 24 ? iw[u].z : iw[u].w;
+                        const int idx = (int)((word >> (4 * (i & 7))) & 15u);
+                        const int msk = -(int)((sw[u] >> i) & 1u);
+                        acc += lds_i16(base + i * kSlot28 + 2 * idx) ^ msk;
+                    }
+                    acc += __popc(sw[u]);
+                }
+            }
+            if (wave == tail_wave) {
+#pragma unroll
+                for (int t = 0; t < kMaxUnits; ++t) {
+                    if (t < units) {
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            const int code = (int)((tw[t] >> (4 * i)) & 15u);
+                            acc += lds_i16(pairs + (t * 32 + 8 * q + i) * kSlot28 + 2 * code);
+                        }
+                    }
+                }
+            }
+            acc += __shfl_xor(acc, 16, 64);
+            acc += __shfl_xor(acc, 32, 64);
+            if (lane < 16) part[par][wave][lane] = acc;
+            __syncthreads();
+            if (wave == 0 && lane < 16) {
+                int v = 0;
+#pragma unroll
+                for (int w = 0; w < WAVES; ++w) v += part[par][w][lane];
+                int li, rg;
+                locate(L, bid + st * G, li, rg);
+                const int n = rg * kRowsPerGroup + lane;
+                pick(L.y, li)[n] = (float)v * (bw / sx);
+                int32_t* acc_out = pick(L.acc, li);
+                if (acc_out) acc_out[n] = v;
+            }
+            par ^= 1;
+        };
+        if constexpr (!kMulti) {
+            compute(iwa, swa, twa, ba, 0);
+            return;
+        }
+        int st = 0;
+        for (; st + 3 < S; st += 2) {
+            compute(iwa, swa, twa, ba, st);
+            issue(iwa, swa, twa, ba, st + 2);
+            compute(iwb, swb, twb, bb, st + 1);
+            issue(iwb, swb, twb, bb, st + 3);
+        }
+        if (st + 2 < S) {
+            compute(iwa, swa, twa, ba, st);
+            issue(iwa, swa, twa, ba, st + 2);
+            compute(iwb, swb, twb, bb, st + 1);
+            compute(iwa, swa, twa, ba, st + 2);
+        } else {
+            compute(iwa, swa, twa, ba, st);
+            compute(iwb, swb, twb, bb, st + 1);
+        }
+    };
+    if (S == 1) run(std::false_type{});
+    else run(std::true_type{});
+}
+
 // Standalone table precompute: the same tables, written to global memory for inspection.
 __global__ __launch_bounds__(256) void elut_tables_kernel(const int8_t* __restrict__ xq, int M, int K,
                                                           int16_t* __restrict__ lut, int16_t* __restrict__ lut1) {
@@ -260,6 +483,55 @@ hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, cons
     if (M <= 2) return launch_elut_mt<2>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
     if (M <= 4) return launch_elut_mt<4>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
     return launch_elut_mt<8>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+}
+
+size_t tl2_stream_lds_bytes(int K) {
+    const int three = (K / kTl2BlockK) * kTl2BlockK;
+    return (size_t)((K + 15) & ~15) + (size_t)(three / kTl2BlockK) * kBlockBytes28 +
+           (size_t)((K - three) / kSubK) * 32 * kSlot28;
+}
+
+bool tl2_stream_fits(int K) {
+    return K >= kTl2BlockK && tl2_stream_lds_bytes(K) + 2 * 16 * 16 * 4 + 256 <= 160 * 1024;
+}
+
+template <int WAVES, int U, int XV>
+hipError_t launch_stream_cfg(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
+                             hipStream_t stream) {
+    const size_t lds = tl2_stream_lds_bytes(K);
+    const void* kern = x ? reinterpret_cast<const void*>(tl2_stream_kernel<WAVES, U, XV, true>)
+                         : reinterpret_cast<const void*>(tl2_stream_kernel<WAVES, U, XV, false>);
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * WAVES, lds) != hipSuccess || occ <= 0) occ = 1;
+    const int64_t max_g = (int64_t)device_cus() * occ;
+    const int64_t rounds = (L.total + max_g - 1) / max_g;
+    const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * WAVES);
+    if (x)
+        hipLaunchKernelGGL((tl2_stream_kernel<WAVES, U, XV, true>), grid, block, lds, stream, L, x, K, xq, s, rs);
+    else
+        hipLaunchKernelGGL((tl2_stream_kernel<WAVES, U, XV, false>), grid, block, lds, stream, L, x, K, xq, s, rs);
+    return hipGetLastError();
+}
+
+template <int WAVES, int U>
+hipError_t launch_stream_u(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
+                           hipStream_t stream) {
+    const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
+    if (xv <= 1) return launch_stream_cfg<WAVES, U, 1>(L, x, K, xq, s, rs, stream);
+    if (xv <= 2) return launch_stream_cfg<WAVES, U, 2>(L, x, K, xq, s, rs, stream);
+    if (xv <= 4) return launch_stream_cfg<WAVES, U, 4>(L, x, K, xq, s, rs, stream);
+    return launch_stream_cfg<WAVES, U, 8>(L, x, K, xq, s, rs, stream);
+}
+
+// Waves and blocks per wave: every block of a row has its wave (at most three per wave).
+hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                             int32_t* x_rowsum, hipStream_t stream) {
+    const int nblk = K / kTl2BlockK;
+    if (nblk <= 4) return launch_stream_u<4, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nblk <= 8) return launch_stream_u<8, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nblk <= 16) return launch_stream_u<8, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nblk <= 32) return launch_stream_u<16, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
+    return launch_stream_u<16, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
 }
 
 hipError_t launch_elut_tables(const int8_t* xq, int M, int K, int16_t* lut, int16_t* lut1, hipStream_t stream) {

@@ -108,3 +108,22 @@ def test_tl2_workload_shapes(workload):
         for M in spec["tokens"]:
             _announce("tl2 workload", workload, name, M, N, K)
             _tl2_vs_oracle(M, N, K, seed=inputs.seed_for(workload, i), repeat=False)
+
+
+# One token through the streaming kernel (tables of the whole row built once per work group): every wave /
+# blocks-per-wave configuration (4x1, 8x1, 8x2, 16x2, 16x3), with and without a TL1 tail, the largest K whose
+# tables fit in LDS, and enough row groups that work groups walk several of them (both ping-pong tails).
+@pytest.mark.parametrize("N,K", [(16, 1536), (48, 1600), (32, 3200), (2400, 4096), (64, 8640), (4112, 12288),
+                                 (32, 14336), (9616, 448)])
+def test_tl2_stream_one_token(N, K):
+    _announce("tl2 stream one token", N, K)
+    _tl2_vs_oracle(1, N, K, seed=inputs.seed_for(8, 77 + N + K))
+
+
+# The same kernel as one launch for several weights that share the activation (quantised inside the launch).
+@pytest.mark.parametrize("K,Ns", [(3200, [3200, 3200, 3200]), (4096, [4096, 1024, 1024]), (8640, [3200, 16]),
+                                  (14336, [4096])])
+def test_tl2_stream_fused(K, Ns):
+    _announce("tl2 stream fused", K, Ns)
+    from tests.test_gpu_fused import _fused_case
+    _fused_case("tl2", 1, K, Ns, seed=inputs.seed_for(8, 300 + K + len(Ns)))
