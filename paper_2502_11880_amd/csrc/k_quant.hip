@@ -6,9 +6,10 @@
 //   xq      = clamp(rint(x * s_m), -128, 127)     (fp32 multiply, ties to even)
 //   rowsum  = sum_k xq[m, k]                      (optional; exact int32)
 //
-// One work group per token row.  The row is read once into registers (up to 16 float4 per lane), reduced
-// to its absmax, then quantised from registers; rows too long for that take a second pass over memory.
-// HBM-bound: 4 bytes read and 1 byte written per element.
+// Many rows of up to 4096: one wave per row, reduced inside the wave.  Otherwise one work group per row.  The
+// row is read once into registers (up to 16 float4 per lane), reduced to its absmax, then quantised from
+// registers; rows too long for that take a second pass over memory.  HBM-bound: 4 bytes read and 1 byte
+// written per element.
 #include "bitnet_internal.hpp"
 
 namespace bitnet {
@@ -74,16 +75,54 @@ __global__ __launch_bounds__(BLOCK) void quantize_rows_reg(const float* __restri
     for (int i = 0; i < VPT; ++i) {
         const int idx = threadIdx.x + i * BLOCK;
         if (idx < K4) {
-            const int c0 = quant_one(v[i].x, s), c1 = quant_one(v[i].y, s), c2 = quant_one(v[i].z, s),
-                      c3 = quant_one(v[i].w, s);
-            sum += c0 + c1 + c2 + c3;
-            q4[idx] = (uint32_t)(c0 & 0xFF) | ((uint32_t)(c1 & 0xFF) << 8) | ((uint32_t)(c2 & 0xFF) << 16) |
-                      ((uint32_t)(c3 & 0xFF) << 24);
+            const uint32_t c = quant4(v[i], s);
+            sum = byte_sum4(c, sum);
+            q4[idx] = c;
         }
     }
     if (x_rowsum) {
         sum = block_sum<BLOCK>(sum, redi);
         if (threadIdx.x == 0) x_rowsum[m] = sum;
+    }
+}
+
+// One wave per row (K <= 4096): the row in registers (up to 16 float4 per lane), absmax and code sum by DPP
+// reductions inside the wave (no barrier), the codes packed four to a word by quant4.  A work group holds
+// four independent rows.
+template <int VPT>
+__global__ __launch_bounds__(256) void quantize_rows_wave(const float* __restrict__ x, int64_t M, int K,
+                                                          int8_t* __restrict__ xq, float* __restrict__ x_scale,
+                                                          int32_t* __restrict__ x_rowsum) {
+    const int lane = threadIdx.x & 63;
+    const int64_t m = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (m >= M) return;
+    const float4* x4 = reinterpret_cast<const float4*>(x + m * (size_t)K);
+    uint32_t* q4 = reinterpret_cast<uint32_t*>(xq + m * (size_t)K);
+    const int K4 = K >> 2;
+    float4 v[VPT];
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int idx = lane + 64 * i;
+        v[i] = idx < K4 ? x4[idx] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[i].x), fabsf(v[i].y)), fmaxf(fabsf(v[i].z), fabsf(v[i].w))));
+    }
+    amax = wave_max_all(amax);
+    const float s = 127.0f / fmaxf(amax, 1e-5f);
+    int sum = 0;
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int idx = lane + 64 * i;
+        if (idx < K4) {
+            const uint32_t c = quant4(v[i], s);
+            sum = byte_sum4(c, sum);
+            q4[idx] = c;
+        }
+    }
+    if (lane == 0) x_scale[m] = s;
+    if (x_rowsum) {
+        sum = wave_sum_all(sum);
+        if (lane == 0) x_rowsum[m] = sum;
     }
 }
 
@@ -135,12 +174,24 @@ hipError_t launch_block(const float* x, int64_t M, int64_t K, int8_t* xq, float*
     return hipGetLastError();
 }
 
+template <int VPT>
+hipError_t launch_wave(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale, int32_t* x_rowsum,
+                       hipStream_t stream) {
+    hipLaunchKernelGGL((quantize_rows_wave<VPT>), dim3((unsigned)((M + 3) / 4)), dim3(256), 0, stream, x, M, (int)K, xq,
+                       x_scale, x_rowsum);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
                                int32_t* x_rowsum, hipStream_t stream) {
-    // Few rows: wide groups so one row is spread over many lanes.  Many rows: one 256-lane group each.
+    // Few rows: wide groups so one row is spread over many lanes.  Many rows of up to 4096: one wave each;
+    // longer rows: one 256-lane group each.
     if (M <= 64) return launch_block<1024>(x, M, K, xq, x_scale, x_rowsum, stream);
+    if (K % 4 == 0 && K <= 1024) return launch_wave<4>(x, M, K, xq, x_scale, x_rowsum, stream);
+    if (K % 4 == 0 && K <= 2048) return launch_wave<8>(x, M, K, xq, x_scale, x_rowsum, stream);
+    if (K % 4 == 0 && K <= 4096) return launch_wave<16>(x, M, K, xq, x_scale, x_rowsum, stream);
     return launch_block<256>(x, M, K, xq, x_scale, x_rowsum, stream);
 }
 

@@ -33,6 +33,22 @@ def test_quantize_act_bit_exact(M, K):
     assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
 
 
+# More than 64 rows: one wave per row up to K = 4096, one work group per row above; constructed ties and an
+# all-zero row placed among random rows.
+@pytest.mark.parametrize("K", [64, 1024, 1600, 4096, 4160, 14336])
+def test_quantize_act_many_rows(K):
+    _announce("quantize many rows", 130, K)
+    x = inputs.activation_f32(130, K, seed=inputs.seed_for(9, 5000 + K))
+    x[7] = 0.0
+    x[8, :6] = torch.tensor([127.0, 63.5, -0.5, 1.5, 2.5, -127.0])
+    x[8, 6:] = 0.25
+    xq, s, rs = H.quantize(x, with_rowsum=True)
+    xq_ref, s_ref = O.quantize_act(x.numpy())
+    assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(H.to_np(xq), xq_ref)
+    assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
+
+
 def test_quantize_act_constructed_ties_and_zero_rows():
     _announce("quantize constructed")
     x = torch.zeros((3, 64), dtype=torch.float32)
