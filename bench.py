@@ -184,12 +184,14 @@ def main():
         avg_bytes = sum(grp_bytes) * n_layers / launches
         avg_launch_ms = ms_per_step / launches
         achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
-        if layout != "i2s":
-            kernel = "bitnet_mpgemm_fused on TL2: quantiser + one ELUT launch per weight"
+        if layout != "i2s" and M == 1:
+            kernel = "tl2_stream_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
+        elif layout != "i2s":
+            kernel = "bitnet_mpgemm_fused on TL2: quantize_rows_reg + tl2_mfma_decode_kernel per group"
         elif M == 1:
             kernel = "i2s_gemv1_stream_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
         else:
-            kernel = "bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_kernel per group"
+            kernel = "bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_stream_kernel per group"
         default_workload = (args.workload, M, layout) == (1, 1, "i2s")
         traffic = measured_traffic() if default_workload else None
         roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,

@@ -166,6 +166,10 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
         return hip_status(bitnet::launch_tl2_stream(one_linear(packed, w_scale, N, y, acc), nullptr, (int)K,
                                                     const_cast<int8_t*>(xq), const_cast<float*>(x_scale), nullptr, s),
                           "bitnet_mpgemm launch");
+    if (bitnet::tl2_mfma_max_tokens((int)K) > 0)
+        return hip_status(bitnet::launch_tl2_mfma_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, (int)M,
+                                                         (int)K, s),
+                          "bitnet_mpgemm launch");
     const int64_t slice = bitnet::kElutMaxTokens;
     for (int64_t m0 = 0; m0 < M; m0 += slice) {
         const int mc = (int)((M - m0) < slice ? (M - m0) : slice);
@@ -235,19 +239,23 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
                     : bitnet::launch_i2s_prefill(L, xq, x_scale, x_rowsum, (int)M, (int)K, ws, ws_bytes, s);
         return hip_status(e, "bitnet_mpgemm_fused launch");
     }
-    // TL2: one token whose tables fit in LDS: one streaming launch for every weight (quantising inside);
-    // otherwise the quantiser once, then one table-lookup launch per weight.
+    // TL2: one token whose tables fit in LDS: one streaming launch for every weight (quantising inside).  Otherwise
+    // the quantiser once, then one MFMA launch for every weight (token slices that fit in LDS) or, where that path
+    // does not cover K, one table-lookup launch per weight.
+    bitnet::FusedLinears L{};
+    L.count = n_linears;
+    int64_t rgs = 0;
+    for (int i = 0; i < n_linears; ++i) {
+        L.packed[i] = static_cast<const uint8_t*>(packed[i]);
+        L.w_scale[i] = w_scale[i];
+        L.y[i] = y[i];
+        L.acc[i] = nullptr;
+        L.N[i] = (int)N[i];
+        rgs += N[i] / bitnet::kRowsPerGroup;
+    }
+    if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
+    bitnet::seal_fused(L);
     if (M == 1 && bitnet::tl2_stream_fits((int)K)) {
-        bitnet::FusedLinears L{};
-        L.count = n_linears;
-        for (int i = 0; i < n_linears; ++i) {
-            L.packed[i] = static_cast<const uint8_t*>(packed[i]);
-            L.w_scale[i] = w_scale[i];
-            L.y[i] = y[i];
-            L.acc[i] = nullptr;
-            L.N[i] = (int)N[i];
-        }
-        bitnet::seal_fused(L);
         if (!quantise) return hip_status(bitnet::launch_tl2_stream(L, nullptr, (int)K, xq, x_scale, x_rowsum, s),
                                          "bitnet_mpgemm_fused launch");
         return hip_status(bitnet::launch_tl2_stream(L, x, (int)K, xq, x_scale, x_rowsum, s),
@@ -255,6 +263,9 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     }
     hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
     if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm_fused launch");
+    if (bitnet::tl2_mfma_max_tokens((int)K) > 0)
+        return hip_status(bitnet::launch_tl2_mfma_decode(L, xq, x_scale, (int)M, (int)K, s),
+                          "bitnet_mpgemm_fused launch");
     for (int i = 0; i < n_linears; ++i) {
         const bitnet_status st = bitnet_mpgemm(layout, packed[i], packed_bytes[i], w_scale[i], N[i], K, xq, x_scale,
                                                x_rowsum, M, y[i], nullptr, ws, ws_bytes, stream);

@@ -406,6 +406,260 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_stream_kernel(FusedLinears L, 
     else run(std::true_type{});
 }
 
+// Several tokens (up to 16 per launch), TL2 on int8 MFMA.  Table lookups cost one LDS read per token and triple,
+// so past one token the packed triples are instead expanded to int8 weights in registers and multiplied on
+// v_mfma_i32_16x16x64_i8, the same contraction the I2_S kernels run; the expansion is shared by every token.
+// Two small tables in LDS do the expansion (Eq. 5: a set sign bit negates all three weights of its triple):
+//   - index table, 1024 entries of 8 bytes: a byte of the index plane (the 4-bit indices of two neighbouring
+//     triples) and their two sign bits give the six weights, one signed byte each;
+//   - pair table, 256 entries of 4 bytes: a byte of a TL1 tail word (two 4-bit pair codes, Table 5) gives
+//     the four weights.
+// Lane (q, r) holds triples 32q .. 32q+31 of row r of a 384-k block, that is k = 96q .. 96q+95 of the block in
+// order; MFMA step s (0..5) takes the lane's weights 16s .. 16s+15, so its A operand is the tokens' codes at
+// k = 96q + 16s.  (The contraction pairs A and B bytes by lane quarter and byte position, so any k order the two
+// operands share gives the same sum.)  A tail unit's word holds k = 16q .. 16q+15 of its 64, in order.
+// The weights are signed, so no code-sum correction is needed.
+//
+// Persistent work groups: each wave copies the codes of its own blocks (every token) into LDS and the group
+// builds the two tables; then the group walks row groups g = blockIdx.x + j gridDim.x of all the launch's weights
+// with the next row group's index, sign and tail words in flight, one barrier per row group for the reduction.
+constexpr int kIdxTableBytes = 1024 * 8;
+constexpr int kPairTableBytes = 256 * 4;
+constexpr int kTl2MfmaTables = kIdxTableBytes + kPairTableBytes;
+constexpr int kTl2MfmaMaxBlocks = 48;                         // 16 waves x 3 blocks
+
+// Weight of balanced-ternary digit d (0 = leading) of a triple index 0..13 (index = 9 d0 + 3 d1 + d2); 0 for the
+// unused indices 14 and 15.
+__device__ __forceinline__ int triple_digit(int idx, int d) {
+    if (idx > 13) return 0;
+    const int d2 = (idx + 1) % 3 - 1;
+    const int rest = (idx - d2) / 3;
+    const int d1 = (rest + 1) % 3 - 1;
+    const int d0 = (rest - d1) / 3;
+    return d == 0 ? d0 : d == 1 ? d1 : d2;
+}
+
+__device__ __forceinline__ uint32_t byte_of(int v, int pos) { return ((uint32_t)v & 0xFFu) << (8 * pos); }
+
+__device__ void build_mfma_tables(uint8_t* lds, int tid, int nthreads) {
+    uint2* itab = reinterpret_cast<uint2*>(lds);
+    uint32_t* ptab = reinterpret_cast<uint32_t*>(lds + kIdxTableBytes);
+    for (int e = tid; e < 1024 + 256; e += nthreads) {
+        if (e < 1024) {
+            const int n0 = e & 15, n1 = (e >> 4) & 15;
+            const int g0 = (e >> 8) & 1 ? -1 : 1, g1 = (e >> 9) & 1 ? -1 : 1;
+            uint2 v;
+            v.x = byte_of(g0 * triple_digit(n0, 0), 0) | byte_of(g0 * triple_digit(n0, 1), 1) |
+                  byte_of(g0 * triple_digit(n0, 2), 2) | byte_of(g1 * triple_digit(n1, 0), 3);
+            v.y = byte_of(g1 * triple_digit(n1, 1), 0) | byte_of(g1 * triple_digit(n1, 2), 1);
+            itab[e] = v;
+        } else {
+            const int b = e - 1024, c0 = b & 15, c1 = b >> 4;
+            uint32_t v = 0;
+            if (c0 <= 8) v |= byte_of(c0 / 3 - 1, 0) | byte_of(c0 % 3 - 1, 1);
+            if (c1 <= 8) v |= byte_of(c1 / 3 - 1, 2) | byte_of(c1 % 3 - 1, 3);
+            ptab[b] = v;
+        }
+    }
+}
+
+// The 96 weights of a lane's 32 triples (index words iw, sign word sw) as 24 words, k in order.
+__device__ __forceinline__ void expand_triples(const v4u& iw, uint32_t sw, const uint2* itab, uint32_t (&wd)[24]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t w = word_of(iw, j);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int p = 4 * j + 2 * h;                 // bytes p, p + 1: triples 2p .. 2p + 3
+            const uint32_t i0 = ((w >> (16 * h)) & 0xFFu) | (((sw >> (2 * p)) & 3u) << 8);
+            const uint32_t i1 = ((w >> (16 * h + 8)) & 0xFFu) | (((sw >> (2 * p + 2)) & 3u) << 8);
+            const uint2 e0 = itab[i0], e1 = itab[i1];
+            const int d = 6 * j + 3 * h;
+            wd[d] = e0.x;
+            wd[d + 1] = e0.y | (e1.x << 16);
+            wd[d + 2] = (e1.x >> 16) | (e1.y << 16);
+        }
+    }
+}
+
+template <int WAVES, int U, int CH>
+__global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinears L, const int8_t* __restrict__ xq,
+                                                                     const float* __restrict__ x_scale, int M, int K) {
+    extern __shared__ __align__(16) uint8_t lds[];    // index table | pair table | M rows of K + 16 codes
+    __shared__ v4i part[2][WAVES][64];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int q = lane >> 4, r = lane & 15;
+    const int G = gridDim.x, bid = blockIdx.x;
+    const int three = (K / kTl2BlockK) * kTl2BlockK;
+    const int nblk = three / kTl2BlockK;                       // >= 1 (the launcher checks)
+    const int units = (K - three) / kSubK;
+    const int tail_wave = nblk % WAVES;                        // a wave with the fewest blocks
+    const int S = (L.total - bid + G - 1) / G;                 // row groups of this work group (grid <= total)
+    const int stride = K + 16;
+    const uint2* itab = reinterpret_cast<const uint2*>(lds);
+    const uint32_t* ptab = reinterpret_cast<const uint32_t*>(lds + kIdxTableBytes);
+    int8_t* xs = reinterpret_cast<int8_t*>(lds + kTl2MfmaTables);
+
+    // the loads of row group step st, all unconditional (blocks past nblk repeat a real one; the tail words of
+    // waves other than the tail wave, and of units past `units`, repeat one real word)
+    const bool tail_mine = wave == tail_wave && units > 0;
+    auto issue = [&](v4u (&iw)[U], uint32_t (&sw)[U], uint32_t (&tw)[kMaxUnits], float& bw, int st) {
+        int li, rg;
+        locate(L, bid + st * G, li, rg);
+        const size_t Nl = (size_t)pick(L.N, li);
+        const uint8_t* idx_plane = pick(L.packed, li);
+        const uint8_t* sign_plane = idx_plane + Nl * (three / 6);
+        const uint8_t* tail_plane = sign_plane + Nl * (three / 24);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const size_t tile = (size_t)rg * nblk + min(wave + WAVES * u, nblk - 1);
+            iw[u] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * lane));
+            sw[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * lane));
+        }
+        const int um = units > 0 ? units : 1;
+        const uint8_t* tail_base = units > 0 ? tail_plane : idx_plane;
+        const size_t tail_row = tail_mine ? (size_t)rg * 64 * um + (size_t)lane * um : 0;
+#pragma unroll
+        for (int t = 0; t < kMaxUnits; ++t)
+            tw[t] = *reinterpret_cast<const uint32_t*>(tail_base + (tail_row + (tail_mine ? min(t, um - 1) : 0)) * 4);
+        bw = *pick(L.w_scale, li);
+    };
+
+    // epilogue operands of tokens m = 4q + v
+    float xs_m[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) xs_m[v] = 4 * q + v < M ? x_scale[4 * q + v] : 1.0f;
+
+    // this wave's codes: 24 chunks of 16 bytes per token and block (4 per token and tail unit), loads first;
+    // CH chunks per lane and block cover 64 CH / 24 tokens
+    constexpr int kChunks = CH;
+    auto stage = [&]() {
+        v4i c[U][kChunks];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int blk = min(wave + WAVES * u, nblk - 1);
+#pragma unroll
+            for (int i = 0; i < kChunks; ++i) {
+                const int ch = min(lane + 64 * i, M * 24 - 1);
+                const int m = ch / 24, k = blk * kTl2BlockK + 16 * (ch % 24);
+                c[u][i] = *reinterpret_cast<const v4i*>(xq + (size_t)m * K + k);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int blk = wave + WAVES * u;
+#pragma unroll
+            for (int i = 0; i < kChunks; ++i) {
+                const int ch = lane + 64 * i;
+                if (blk < nblk && ch < M * 24) {
+                    const int m = ch / 24, k = blk * kTl2BlockK + 16 * (ch % 24);
+                    *reinterpret_cast<v4i*>(xs + m * stride + k) = c[u][i];
+                }
+            }
+        }
+        if (tail_mine) {
+            for (int ch = lane; ch < M * 4 * units; ch += 64) {
+                const int m = ch / (4 * units), k = three + 16 * (ch % (4 * units));
+                *reinterpret_cast<v4i*>(xs + m * stride + k) = *reinterpret_cast<const v4i*>(xq + (size_t)m * K + k);
+            }
+        }
+    };
+
+    const v4i zero = {0, 0, 0, 0};
+    const int8_t* arow = xs + (r < M ? r : 0) * stride;
+    int par = 0;
+    auto compute = [&](const v4u (&iw)[U], const uint32_t (&sw)[U], const uint32_t (&tw)[kMaxUnits], float bw,
+                       int st) {
+        v4i acc = zero;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int blk = wave + WAVES * u;
+            if (blk < nblk) {
+                uint32_t wd[24];
+                expand_triples(iw[u], sw[u], itab, wd);
+                const int8_t* ab = arow + blk * kTl2BlockK + 96 * q;
+#pragma unroll
+                for (int s6 = 0; s6 < 6; ++s6) {
+                    const v4i b = {(int)wd[4 * s6], (int)wd[4 * s6 + 1], (int)wd[4 * s6 + 2], (int)wd[4 * s6 + 3]};
+                    acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + 16 * s6), b, acc);
+                }
+            }
+        }
+        if (tail_mine) {
+#pragma unroll
+            for (int t = 0; t < kMaxUnits; ++t) {
+                if (t < units) {
+                    const uint32_t w = tw[t];
+                    const v4i b = {(int)ptab[w & 0xFFu], (int)ptab[(w >> 8) & 0xFFu], (int)ptab[(w >> 16) & 0xFFu],
+                                   (int)ptab[w >> 24]};
+                    acc = mfma16x16x64(*reinterpret_cast<const v4i*>(arow + three + kSubK * t + 16 * q), b, acc);
+                }
+            }
+        }
+        part[par][wave][lane] = acc;
+        __syncthreads();
+        if (wave == 0 && 4 * q < M) {
+            v4i tot = part[par][0][lane];
+#pragma unroll 4
+            for (int w2 = 1; w2 < WAVES; ++w2) tot += part[par][w2][lane];
+            int li, rg;
+            locate(L, bid + st * G, li, rg);
+            const int N = pick(L.N, li);
+            const int n = rg * kRowsPerGroup + r;
+            float* y = pick(L.y, li);
+            int32_t* acc_out = pick(L.acc, li);
+            // D element v of lane l is row 4 (l / 16) + v (token), column l % 16 (weight row)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = 4 * q + v;
+                if (m < M) {
+                    y[(size_t)m * N + n] = (float)tot[v] * (bw / xs_m[v]);
+                    if (acc_out) acc_out[(size_t)m * N + n] = tot[v];
+                }
+            }
+        }
+        par ^= 1;
+    };
+
+    // one and several row groups per work group are separate instantiations, so no two paths with different
+    // loads in flight join
+    auto run = [&](auto multi) {
+        constexpr bool kMulti = decltype(multi)::value;
+        v4u iwa[U], iwb[U];
+        uint32_t swa[U], swb[U], twa[kMaxUnits], twb[kMaxUnits];
+        float ba = 0.0f, bb = 0.0f;
+        issue(iwa, swa, twa, ba, 0);
+        if constexpr (kMulti) issue(iwb, swb, twb, bb, 1);
+        stage();
+        build_mfma_tables(lds, tid, 64 * WAVES);
+        __syncthreads();                                   // the tables are shared by every wave
+        if constexpr (!kMulti) {
+            compute(iwa, swa, twa, ba, 0);
+            return;
+        }
+        int st = 0;
+        for (; st + 3 < S; st += 2) {
+            compute(iwa, swa, twa, ba, st);
+            issue(iwa, swa, twa, ba, st + 2);
+            compute(iwb, swb, twb, bb, st + 1);
+            issue(iwb, swb, twb, bb, st + 3);
+        }
+        if (st + 2 < S) {
+            compute(iwa, swa, twa, ba, st);
+            issue(iwa, swa, twa, ba, st + 2);
+            compute(iwb, swb, twb, bb, st + 1);
+            compute(iwa, swa, twa, ba, st + 2);
+        } else {
+            compute(iwa, swa, twa, ba, st);
+            compute(iwb, swb, twb, bb, st + 1);
+        }
+    };
+    if (S == 1) run(std::false_type{});
+    else run(std::true_type{});
+}
+
 // Standalone table precompute: the same tables, written to global memory for inspection.
 __global__ __launch_bounds__(256) void elut_tables_kernel(const int8_t* __restrict__ xq, int M, int K,
                                                           int16_t* __restrict__ lut, int16_t* __restrict__ lut1) {
@@ -532,6 +786,64 @@ hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_
     if (nblk <= 16) return launch_stream_u<8, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
     if (nblk <= 32) return launch_stream_u<16, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
     return launch_stream_u<16, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+}
+
+size_t tl2_mfma_lds_bytes(int M, int K) { return (size_t)kTl2MfmaTables + (size_t)M * (K + 16); }
+
+int tl2_mfma_max_tokens(int K) {
+    const int nblk = K / kTl2BlockK;
+    if (nblk < 1 || nblk > kTl2MfmaMaxBlocks) return 0;
+    const int waves = nblk <= 4 ? 4 : nblk <= 16 ? 8 : 16;
+    const size_t budget = 160 * 1024 - (size_t)2 * waves * 64 * 16 - 256;   // less the reduction buffers
+    // past 32 blocks (three per wave) the staging registers allow 8 tokens per slice
+    for (int m = nblk > 32 ? 8 : kTl2MfmaMaxTokens; m >= 1; --m)
+        if (tl2_mfma_lds_bytes(m, K) <= budget) return m;
+    return 0;
+}
+
+template <int WAVES, int U>
+hipError_t launch_mfma_cfg(const FusedLinears& L, const int8_t* xq, const float* x_scale, int M, int K,
+                           hipStream_t stream) {
+    const size_t lds = tl2_mfma_lds_bytes(M, K);
+    constexpr int kWide = U >= 3 ? 3 : 6;      // the slices of three blocks per wave hold at most 8 tokens
+    const void* kern = M <= 8 ? reinterpret_cast<const void*>(tl2_mfma_decode_kernel<WAVES, U, 3>)
+                              : reinterpret_cast<const void*>(tl2_mfma_decode_kernel<WAVES, U, kWide>);
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * WAVES, lds) != hipSuccess || occ <= 0) occ = 1;
+    const int64_t max_g = (int64_t)device_cus() * occ;
+    const int64_t rounds = (L.total + max_g - 1) / max_g;
+    const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * WAVES);
+    if (M <= 8)
+        hipLaunchKernelGGL((tl2_mfma_decode_kernel<WAVES, U, 3>), grid, block, lds, stream, L, xq, x_scale, M, K);
+    else
+        hipLaunchKernelGGL((tl2_mfma_decode_kernel<WAVES, U, kWide>), grid, block, lds, stream, L, xq, x_scale, M, K);
+    return hipGetLastError();
+}
+
+// Waves and blocks per wave: every block of a row has its wave.  Tokens go in slices that fit in LDS.
+hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, int M, int K,
+                                  hipStream_t stream) {
+    const int nblk = K / kTl2BlockK;
+    const int mc = tl2_mfma_max_tokens(K);
+    if (mc < 1) return hipErrorInvalidValue;
+    for (int m0 = 0; m0 < M; m0 += mc) {
+        const int m = M - m0 < mc ? M - m0 : mc;
+        FusedLinears Ls = L;
+        for (int i = 0; i < L.count; ++i) {
+            Ls.y[i] = L.y[i] + (size_t)m0 * L.N[i];
+            Ls.acc[i] = L.acc[i] ? L.acc[i] + (size_t)m0 * L.N[i] : nullptr;
+        }
+        const int8_t* xs = xq + (size_t)m0 * K;
+        const float* ss = x_scale + m0;
+        hipError_t e;
+        if (nblk <= 4) e = launch_mfma_cfg<4, 1>(Ls, xs, ss, m, K, stream);
+        else if (nblk <= 8) e = launch_mfma_cfg<8, 1>(Ls, xs, ss, m, K, stream);
+        else if (nblk <= 16) e = launch_mfma_cfg<8, 2>(Ls, xs, ss, m, K, stream);
+        else if (nblk <= 32) e = launch_mfma_cfg<16, 2>(Ls, xs, ss, m, K, stream);
+        else e = launch_mfma_cfg<16, 3>(Ls, xs, ss, m, K, stream);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_elut_tables(const int8_t* xq, int M, int K, int16_t* lut, int16_t* lut1, hipStream_t stream) {

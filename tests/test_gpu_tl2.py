@@ -127,3 +127,31 @@ def test_tl2_stream_fused(K, Ns):
     _announce("tl2 stream fused", K, Ns)
     from tests.test_gpu_fused import _fused_case
     _fused_case("tl2", 1, K, Ns, seed=inputs.seed_for(8, 300 + K + len(Ns)))
+
+
+# Several tokens through the MFMA kernel (triples expanded to int8 through the LDS tables): every wave / blocks-per-
+# wave configuration (4x1, 8x1, 8x2, 16x2, 16x3), TL1 tails of 1 to 5 units, 1 to 16 tokens per launch (both
+# staging widths), token slices (16 tokens at K = 14336 take two launches of 8; 40 tokens take 16 + 16 + 8), one
+# token where the single-token streaming kernel's tables do not fit (K = 16384), and past the kernel's 48 blocks
+# the table-lookup kernel (K = 19200).
+@pytest.mark.parametrize("M,N,K", [(2, 48, 832), (3, 64, 1600), (8, 96, 1536), (4, 208, 3200), (16, 64, 4096),
+                                   (9, 32, 8640), (12, 48, 6080), (5, 16, 14336), (16, 32, 14336), (40, 48, 4096),
+                                   (1, 64, 16384), (2, 16, 19200), (7, 16, 384)])
+def test_tl2_mfma_decode(M, N, K):
+    _announce("tl2 mfma decode", M, N, K)
+    _tl2_vs_oracle(M, N, K, seed=inputs.seed_for(8, 900 + M * 17 + N + K))
+
+
+# Enough row groups that work groups walk 2, 3 or more of them (both ends of the two-register-set pipeline).
+@pytest.mark.parametrize("M,N", [(8, 16 * 2000), (3, 16 * 3000), (8, 16 * 5000)])
+def test_tl2_mfma_decode_streaming(M, N):
+    _announce("tl2 mfma decode streaming", M, N, 448)
+    _tl2_vs_oracle(M, N, 448, seed=inputs.seed_for(8, 1300 + M + N), repeat=False)
+
+
+# The 8B-class groups at 8 tokens as one launch per group (quantised once).
+@pytest.mark.parametrize("K,Ns", [(4096, [4096, 1024, 1024]), (4096, [14336]), (14336, [4096])])
+def test_tl2_mfma_fused(K, Ns):
+    _announce("tl2 mfma fused", 8, K, Ns)
+    from tests.test_gpu_fused import _fused_case
+    _fused_case("tl2", 8, K, Ns, seed=inputs.seed_for(8, 1500 + K + len(Ns)))
