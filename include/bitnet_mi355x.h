@@ -121,10 +121,11 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
                             size_t ws_bytes, void* stream);
 
 /*
- * Workspace bytes bitnet_mpgemm_fused needs to split K for these n_linears weights (host array N of rows, shared
- * K, M tokens; 0 is a valid answer and 0 is also returned for invalid arguments).  A fused I2_S prefill launch
- * (M > 16) splits K over all its weights at once, so this can exceed the largest bitnet_mpgemm_workspace_bytes of
- * the weights; given less (but at least that largest one), the call runs without splitting.
+ * Workspace bytes with which bitnet_mpgemm_fused runs every split it can use for these n_linears weights (host
+ * array N of rows, shared K, M tokens; 0 is a valid answer and 0 is also returned for invalid arguments): at
+ * least the largest bitnet_mpgemm_workspace_bytes of the weights (the minimum the call accepts), and for a fused
+ * I2_S prefill launch (M > 16), which splits K over all its weights at once, enough for that split.  Given less
+ * (but at least that minimum), the fused launch runs without splitting.
  */
 size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int64_t* N, int64_t K, int64_t M);
 

@@ -165,7 +165,8 @@ def bitnet_mpgemm(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=N
 
 
 def bitnet_mpgemm_fused_workspace_bytes(layout, Ns, K: int, M: int) -> int:
-    """Workspace bytes bitnet_mpgemm_fused needs to split K over the weights of rows Ns (a list) at M tokens."""
+    """Workspace bytes with which bitnet_mpgemm_fused runs every K split it can use for weights of rows Ns (a list)
+    at M tokens: at least the largest single-weight workspace."""
     arr = (ctypes.c_int64 * len(Ns))(*Ns)
     return int(lib().bitnet_mpgemm_fused_workspace_bytes(_layout(layout), len(Ns), arr, K, M))
 

@@ -116,17 +116,18 @@ size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int6
     if (!layout_ok(layout) || !N || n_linears < 1 || n_linears > bitnet::kMaxFused || M < 1) return 0;
     for (int i = 0; i < n_linears; ++i)
         if (!weight_shape_ok(N[i], K)) return 0;
+    size_t need = 0;
+    for (int i = 0; i < n_linears; ++i) {
+        const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
+        need = w > need ? w : need;
+    }
     if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens) {
         bitnet::FusedLinears L{};
         L.count = n_linears;
         for (int i = 0; i < n_linears; ++i) L.N[i] = (int)N[i];
         bitnet::seal_fused(L);
-        return bitnet::prefill_workspace_bytes(L, M, K);
-    }
-    size_t need = 0;
-    for (int i = 0; i < n_linears; ++i) {
-        const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
-        need = w > need ? w : need;
+        const size_t split = bitnet::prefill_workspace_bytes(L, M, K);
+        need = split > need ? split : need;
     }
     return need;
 }

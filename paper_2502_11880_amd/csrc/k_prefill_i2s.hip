@@ -404,10 +404,11 @@ __global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __re
     if (acc_out) *reinterpret_cast<v4i*>(acc_out + off) = t;
 }
 
-// Tile width and split-K factor for the weight tiles of a launch.  The 128 x 512 tile where its grid gives every
-// CU a work group, else the 128 x 256 one (two K-groups per tile).  Splitting K keeps still smaller grids busy: it
-// aims at one work group per CU, with at least two 256-k stages per slice, and only for grids that leave at least
-// half the CUs idle (the slices' extra pass over M x N costs more elsewhere).
+// Tile width and split-K factor for the weight tiles of a launch.  Whichever of the 128 x 512 and 128 x 256 tiles
+// (two K-groups) needs fewer rounds of work groups over the CUs, weighting a round of the narrow tile at 0.84 of a
+// wide one (measured at K = 4096 and 14336).  Splitting K keeps still smaller grids busy: as many slices as keep
+// one round (at least two 256-k stages per slice), only for grids that leave at least half the CUs idle (the
+// slices' extra pass over M x N costs more elsewhere).
 void prefill_plan(const FusedLinears& L, int64_t M, int64_t K, int& wn, int& splits) {
     const int64_t cus = device_cus();
     const int64_t tiles_m = (M + kBM - 1) / kBM;
@@ -416,10 +417,11 @@ void prefill_plan(const FusedLinears& L, int64_t M, int64_t K, int& wn, int& spl
         n4 += (L.N[i] + 511) / 512;
         n2 += (L.N[i] + 255) / 256;
     }
-    wn = tiles_m * n4 >= cus ? 4 : 2;
+    const int64_t r4 = (tiles_m * n4 + cus - 1) / cus, r2 = (tiles_m * n2 + cus - 1) / cus;
+    wn = r2 * 84 < r4 * 100 ? 2 : 4;
     const int64_t tiles = tiles_m * (wn == 4 ? n4 : n2);
     const int64_t nkb = (K + kBK - 1) / kBK;
-    int64_t sp = 2 * tiles <= cus ? (cus + tiles - 1) / tiles : 1;
+    int64_t sp = 2 * tiles <= cus ? cus / tiles : 1;
     if (sp > nkb / 2) sp = nkb / 2;
     if (sp > kMaxSplits) sp = kMaxSplits;
     splits = sp > 1 ? (int)sp : 1;

@@ -124,8 +124,9 @@ def test_fused_workspace_query():
     assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [4096, 1024, 1024], 4096, 8) == 0
     for M, Ns, K in [(512, [4096, 1024, 1024], 4096), (40, [48, 16, 64], 832), (300, [3200] * 3, 3200)]:
         w = B.bitnet_mpgemm_fused_workspace_bytes("i2s", Ns, K, M)
-        assert w % (M * sum(Ns) * 4) == 0
-        assert w >= max(B.bitnet_mpgemm_workspace_bytes("i2s", M, N, K) for N in Ns)
+        single = max(B.bitnet_mpgemm_workspace_bytes("i2s", M, N, K) for N in Ns)
+        assert w >= single
+        assert w == single or w % (M * sum(Ns) * 4) == 0
     assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [4096, 1000], 4096, 512) == 0
     assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [], 4096, 512) == 0
     assert B.bitnet_mpgemm_fused_workspace_bytes("i2s", [64] * 9, 256, 512) == 0
