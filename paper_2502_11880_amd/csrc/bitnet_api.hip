@@ -256,6 +256,9 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     }
     if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
     bitnet::seal_fused(L);
+    if (M == 1 && quantise && bitnet::tl2_mfma_max_tokens((int)K) > 0)
+        return hip_status(bitnet::launch_tl2_mfma_quant(L, x, (int)K, xq, x_scale, x_rowsum, s),
+                          "bitnet_mpgemm_fused launch");
     if (M == 1 && bitnet::tl2_stream_fits((int)K)) {
         if (!quantise) return hip_status(bitnet::launch_tl2_stream(L, nullptr, (int)K, xq, x_scale, x_rowsum, s),
                                          "bitnet_mpgemm_fused launch");

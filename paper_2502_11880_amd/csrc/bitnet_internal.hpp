@@ -186,6 +186,8 @@ constexpr int kTl2MfmaMaxTokens = 16;
 int tl2_mfma_max_tokens(int K);
 hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, int M, int K,
                                   hipStream_t stream);
+hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                                 int32_t* x_rowsum, hipStream_t stream);
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                              int32_t* x_rowsum, hipStream_t stream);
 

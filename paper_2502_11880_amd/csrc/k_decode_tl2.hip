@@ -430,7 +430,7 @@ constexpr int kTl2MfmaMaxBlocks = 48;                         // 16 waves x 3 bl
 
 // Weight of balanced-ternary digit d (0 = leading) of a triple index 0..13 (index = 9 d0 + 3 d1 + d2); 0 for the
 // unused indices 14 and 15.
-__device__ __forceinline__ int triple_digit(int idx, int d) {
+constexpr int triple_digit(int idx, int d) {
     if (idx > 13) return 0;
     const int d2 = (idx + 1) % 3 - 1;
     const int rest = (idx - d2) / 3;
@@ -439,29 +439,31 @@ __device__ __forceinline__ int triple_digit(int idx, int d) {
     return d == 0 ? d0 : d == 1 ? d1 : d2;
 }
 
-__device__ __forceinline__ uint32_t byte_of(int v, int pos) { return ((uint32_t)v & 0xFFu) << (8 * pos); }
+constexpr uint32_t byte_of(int v, int pos) { return ((uint32_t)v & 0xFFu) << (8 * pos); }
 
-__device__ void build_mfma_tables(uint8_t* lds, int tid, int nthreads) {
-    uint2* itab = reinterpret_cast<uint2*>(lds);
-    uint32_t* ptab = reinterpret_cast<uint32_t*>(lds + kIdxTableBytes);
-    for (int e = tid; e < 1024 + 256; e += nthreads) {
-        if (e < 1024) {
+// The two expansion tables as one constant image (computed at compile time), copied into LDS by each work group:
+// index-table entry e (two words) for index byte e & 255 and sign bits e >> 8, then the 256 pair-table words.
+struct ExpandTables {
+    uint32_t w[kTl2MfmaTables / 4];
+    constexpr ExpandTables() : w{} {
+        for (int e = 0; e < 1024; ++e) {
             const int n0 = e & 15, n1 = (e >> 4) & 15;
             const int g0 = (e >> 8) & 1 ? -1 : 1, g1 = (e >> 9) & 1 ? -1 : 1;
-            uint2 v;
-            v.x = byte_of(g0 * triple_digit(n0, 0), 0) | byte_of(g0 * triple_digit(n0, 1), 1) |
-                  byte_of(g0 * triple_digit(n0, 2), 2) | byte_of(g1 * triple_digit(n1, 0), 3);
-            v.y = byte_of(g1 * triple_digit(n1, 1), 0) | byte_of(g1 * triple_digit(n1, 2), 1);
-            itab[e] = v;
-        } else {
-            const int b = e - 1024, c0 = b & 15, c1 = b >> 4;
+            w[2 * e] = byte_of(g0 * triple_digit(n0, 0), 0) | byte_of(g0 * triple_digit(n0, 1), 1) |
+                       byte_of(g0 * triple_digit(n0, 2), 2) | byte_of(g1 * triple_digit(n1, 0), 3);
+            w[2 * e + 1] = byte_of(g1 * triple_digit(n1, 1), 0) | byte_of(g1 * triple_digit(n1, 2), 1);
+        }
+        for (int b = 0; b < 256; ++b) {
+            const int c0 = b & 15, c1 = b >> 4;
             uint32_t v = 0;
             if (c0 <= 8) v |= byte_of(c0 / 3 - 1, 0) | byte_of(c0 % 3 - 1, 1);
             if (c1 <= 8) v |= byte_of(c1 / 3 - 1, 2) | byte_of(c1 % 3 - 1, 3);
-            ptab[b] = v;
+            w[2048 + b] = v;
         }
     }
-}
+};
+__device__ __align__(16) constexpr ExpandTables kExpandTables{};
+constexpr int kTableChunks = kTl2MfmaTables / 16;              // 16-byte chunks of the image
 
 // The 96 weights of a lane's 32 triples (index words iw, sign word sw) as 24 words, k in order.
 __device__ __forceinline__ void expand_triples(const v4u& iw, uint32_t sw, const uint2* itab, uint32_t (&wd)[24]) {
@@ -482,11 +484,17 @@ __device__ __forceinline__ void expand_triples(const v4u& iw, uint32_t sw, const
     }
 }
 
-template <int WAVES, int U, int CH>
-__global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinears L, const int8_t* __restrict__ xq,
-                                                                     const float* __restrict__ x_scale, int M, int K) {
+// XV = 0: the codes and scales are read (xq, x_scale).  XV > 0: one token (M = 1), its fp32 row x quantised here
+// (Sec. 2.1; XV float4 per thread), as in the single-token I2_S kernel: the row is loaded before the first weights,
+// reduced to its absmax through LDS and converted into the LDS codes; work group 0 writes xq, x_scale, x_rowsum.
+template <int WAVES, int U, int CH, int XV>
+__global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinears L, const float* __restrict__ x,
+                                                                     int8_t* xq, float* x_scale,
+                                                                     int32_t* x_rowsum, int M, int K) {
     extern __shared__ __align__(16) uint8_t lds[];    // index table | pair table | M rows of K + 16 codes
     __shared__ v4i part[2][WAVES][64];
+    __shared__ float redf[WAVES];
+    __shared__ int redi[WAVES];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -527,16 +535,31 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
         bw = *pick(L.w_scale, li);
     };
 
-    // epilogue operands of tokens m = 4q + v
+    // epilogue operands of tokens m = 4q + v (XV > 0: the scale computed below)
     float xs_m[4];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) xs_m[v] = 4 * q + v < M ? x_scale[4 * q + v] : 1.0f;
+    for (int v = 0; v < 4; ++v) xs_m[v] = (XV == 0 && 4 * q + v < M) ? x_scale[4 * q + v] : 1.0f;
 
-    // this wave's codes: 24 chunks of 16 bytes per token and block (4 per token and tail unit), loads first;
-    // CH chunks per lane and block cover 64 CH / 24 tokens
+    // the expansion tables: chunk tid + 64 WAVES i of the constant image, loaded first, stored into LDS later
+    constexpr int kTabPer = (kTableChunks + 64 * WAVES - 1) / (64 * WAVES);
+    v4u tabv[kTabPer];
+    auto load_tables = [&]() {
+#pragma unroll
+        for (int i = 0; i < kTabPer; ++i)
+            tabv[i] = reinterpret_cast<const v4u*>(kExpandTables.w)[min(tid + 64 * WAVES * i, kTableChunks - 1)];
+    };
+    auto store_tables = [&]() {
+#pragma unroll
+        for (int i = 0; i < kTabPer; ++i)
+            if (tid + 64 * WAVES * i < kTableChunks) reinterpret_cast<v4u*>(lds)[tid + 64 * WAVES * i] = tabv[i];
+    };
+
+    // this wave's codes: 24 chunks of 16 bytes per token and block (4 per token and tail unit); CH chunks per lane
+    // and block cover 64 CH / 24 tokens.  Loads issued before the first weights are usable before those arrive
+    // (loads complete in order); the stores follow the tables.
     constexpr int kChunks = CH;
-    auto stage = [&]() {
-        v4i c[U][kChunks];
+    v4i cc[XV == 0 ? U : 1][kChunks];
+    auto load_codes = [&]() {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int blk = min(wave + WAVES * u, nblk - 1);
@@ -544,9 +567,11 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
             for (int i = 0; i < kChunks; ++i) {
                 const int ch = min(lane + 64 * i, M * 24 - 1);
                 const int m = ch / 24, k = blk * kTl2BlockK + 16 * (ch % 24);
-                c[u][i] = *reinterpret_cast<const v4i*>(xq + (size_t)m * K + k);
+                cc[u][i] = *reinterpret_cast<const v4i*>(xq + (size_t)m * K + k);
             }
         }
+    };
+    auto store_codes = [&]() {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int blk = wave + WAVES * u;
@@ -555,7 +580,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
                 const int ch = lane + 64 * i;
                 if (blk < nblk && ch < M * 24) {
                     const int m = ch / 24, k = blk * kTl2BlockK + 16 * (ch % 24);
-                    *reinterpret_cast<v4i*>(xs + m * stride + k) = c[u][i];
+                    *reinterpret_cast<v4i*>(xs + m * stride + k) = cc[u][i];
                 }
             }
         }
@@ -565,6 +590,46 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
                 *reinterpret_cast<v4i*>(xs + m * stride + k) = *reinterpret_cast<const v4i*>(xq + (size_t)m * K + k);
             }
         }
+    };
+    // one token: the fp32 row, float4 e = tid + 64 WAVES i per thread
+    constexpr int kXv = XV > 0 ? XV : 1;
+    float4 xv[kXv];
+    const int K4 = K >> 2;
+    auto load_row = [&]() {
+#pragma unroll
+        for (int i = 0; i < kXv; ++i) {
+            const int e = tid + i * 64 * WAVES;
+            const float4 v = reinterpret_cast<const float4*>(x)[e < K4 ? e : K4 - 1];
+            xv[i] = e < K4 ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        }
+    };
+    auto quantise_row = [&]() {
+        float amax = 0.0f;
+#pragma unroll
+        for (int i = 0; i < kXv; ++i)
+            amax = fmaxf(amax, fmaxf(fmaxf(fabsf(xv[i].x), fabsf(xv[i].y)), fmaxf(fabsf(xv[i].z), fabsf(xv[i].w))));
+        amax = wave_max_all(amax);
+        if (lane == 0) redf[wave] = amax;
+        __syncthreads();
+        amax = redf[0];
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) amax = fmaxf(amax, redf[w]);
+        const float sx = 127.0f / fmaxf(amax, 1e-5f);
+        int sum = 0;
+#pragma unroll
+        for (int i = 0; i < kXv; ++i) {
+            const int e = tid + i * 64 * WAVES;
+            if (e < K4) {
+                const uint32_t c = quant4(xv[i], sx);
+                sum = byte_sum4(c, sum);
+                reinterpret_cast<uint32_t*>(xs)[e] = c;
+                if (bid == 0) reinterpret_cast<uint32_t*>(xq)[e] = c;
+            }
+        }
+        sum = wave_sum_all(sum);
+        if (lane == 0) redi[wave] = sum;
+        xs_m[0] = sx;
+        if (bid == 0 && tid == 0) x_scale[0] = sx;
     };
 
     const v4i zero = {0, 0, 0, 0};
@@ -630,11 +695,25 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
         v4u iwa[U], iwb[U];
         uint32_t swa[U], swb[U], twa[kMaxUnits], twb[kMaxUnits];
         float ba = 0.0f, bb = 0.0f;
+        // codes loaded ahead of the weights where their registers fit beside them (one token-group of chunks per
+        // wave), after them otherwise
+        constexpr bool kEarly = XV == 0 && U * CH <= 3;
+        load_tables();
+        if constexpr (XV > 0) load_row();
+        else if constexpr (kEarly) load_codes();
         issue(iwa, swa, twa, ba, 0);
         if constexpr (kMulti) issue(iwb, swb, twb, bb, 1);
-        stage();
-        build_mfma_tables(lds, tid, 64 * WAVES);
-        __syncthreads();                                   // the tables are shared by every wave
+        __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the tables and the conversion
+        if constexpr (XV == 0 && !kEarly) load_codes();
+        store_tables();
+        if constexpr (XV > 0) quantise_row();
+        else store_codes();
+        __syncthreads();                                   // the tables (and codes) are shared by every wave
+        if (XV > 0 && bid == 0 && tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < WAVES; ++w) tot += redi[w];
+            x_rowsum[0] = tot;
+        }
         if constexpr (!kMulti) {
             compute(iwa, swa, twa, ba, 0);
             return;
@@ -801,23 +880,52 @@ int tl2_mfma_max_tokens(int K) {
     return 0;
 }
 
-template <int WAVES, int U>
-hipError_t launch_mfma_cfg(const FusedLinears& L, const int8_t* xq, const float* x_scale, int M, int K,
-                           hipStream_t stream) {
+template <int WAVES, int U, int CH, int XV>
+hipError_t launch_mfma_kernel(const FusedLinears& L, const float* x, int8_t* xq, float* x_scale, int32_t* x_rowsum,
+                              int M, int K, hipStream_t stream) {
     const size_t lds = tl2_mfma_lds_bytes(M, K);
-    constexpr int kWide = U >= 3 ? 3 : 6;      // the slices of three blocks per wave hold at most 8 tokens
-    const void* kern = M <= 8 ? reinterpret_cast<const void*>(tl2_mfma_decode_kernel<WAVES, U, 3>)
-                              : reinterpret_cast<const void*>(tl2_mfma_decode_kernel<WAVES, U, kWide>);
+    const void* kern = reinterpret_cast<const void*>(tl2_mfma_decode_kernel<WAVES, U, CH, XV>);
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * WAVES, lds) != hipSuccess || occ <= 0) occ = 1;
     const int64_t max_g = (int64_t)device_cus() * occ;
     const int64_t rounds = (L.total + max_g - 1) / max_g;
     const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * WAVES);
-    if (M <= 8)
-        hipLaunchKernelGGL((tl2_mfma_decode_kernel<WAVES, U, 3>), grid, block, lds, stream, L, xq, x_scale, M, K);
-    else
-        hipLaunchKernelGGL((tl2_mfma_decode_kernel<WAVES, U, kWide>), grid, block, lds, stream, L, xq, x_scale, M, K);
+    hipLaunchKernelGGL((tl2_mfma_decode_kernel<WAVES, U, CH, XV>), grid, block, lds, stream, L, x, xq, x_scale,
+                       x_rowsum, M, K);
     return hipGetLastError();
+}
+
+template <int WAVES, int U>
+hipError_t launch_mfma_cfg(const FusedLinears& L, const int8_t* xq, const float* x_scale, int M, int K,
+                           hipStream_t stream) {
+    constexpr int kWide = U >= 3 ? 3 : 6;      // the slices of three blocks per wave hold at most 8 tokens
+    int8_t* q = const_cast<int8_t*>(xq);
+    float* s = const_cast<float*>(x_scale);
+    if (M <= 8) return launch_mfma_kernel<WAVES, U, 3, 0>(L, nullptr, q, s, nullptr, M, K, stream);
+    return launch_mfma_kernel<WAVES, U, kWide, 0>(L, nullptr, q, s, nullptr, M, K, stream);
+}
+
+// One token quantised inside: XV float4 of the row per thread.
+template <int WAVES, int U>
+hipError_t launch_mfma_quant(const FusedLinears& L, const float* x, int8_t* xq, float* x_scale, int32_t* x_rowsum,
+                             int K, hipStream_t stream) {
+    const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
+    if (xv <= 1) return launch_mfma_kernel<WAVES, U, 1, 1>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
+    if (xv <= 2) return launch_mfma_kernel<WAVES, U, 1, 2>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
+    if (xv <= 4) return launch_mfma_kernel<WAVES, U, 1, 4>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
+    return launch_mfma_kernel<WAVES, U, 1, 8>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
+}
+
+// One token, quantised inside (tl2_mfma_max_tokens(K) >= 1).
+hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                                 int32_t* x_rowsum, hipStream_t stream) {
+    const int nblk = K / kTl2BlockK;
+    if (tl2_mfma_max_tokens(K) < 1) return hipErrorInvalidValue;
+    if (nblk <= 4) return launch_mfma_quant<4, 1>(L, x, xq, x_scale, x_rowsum, K, stream);
+    if (nblk <= 8) return launch_mfma_quant<8, 1>(L, x, xq, x_scale, x_rowsum, K, stream);
+    if (nblk <= 16) return launch_mfma_quant<8, 2>(L, x, xq, x_scale, x_rowsum, K, stream);
+    if (nblk <= 32) return launch_mfma_quant<16, 2>(L, x, xq, x_scale, x_rowsum, K, stream);
+    return launch_mfma_quant<16, 3>(L, x, xq, x_scale, x_rowsum, K, stream);
 }
 
 // Waves and blocks per wave: every block of a row has its wave.  Tokens go in slices that fit in LDS.

@@ -120,11 +120,13 @@ def test_tl2_stream_one_token(N, K):
     _tl2_vs_oracle(1, N, K, seed=inputs.seed_for(8, 77 + N + K))
 
 
-# The same kernel as one launch for several weights that share the activation (quantised inside the launch).
+# One token as one launch for several weights that share the activation, quantised inside the launch (the MFMA
+# kernel with the row converted in each work group): every wave configuration, 1 to 8 float4 of the row per
+# thread (K = 16512: five, rounded up to eight), with and without a TL1 tail.
 @pytest.mark.parametrize("K,Ns", [(3200, [3200, 3200, 3200]), (4096, [4096, 1024, 1024]), (8640, [3200, 16]),
-                                  (14336, [4096])])
-def test_tl2_stream_fused(K, Ns):
-    _announce("tl2 stream fused", K, Ns)
+                                  (14336, [4096]), (1536, [64, 48]), (16512, [32]), (448, [2400])])
+def test_tl2_one_token_fused(K, Ns):
+    _announce("tl2 one token fused", K, Ns)
     from tests.test_gpu_fused import _fused_case
     _fused_case("tl2", 1, K, Ns, seed=inputs.seed_for(8, 300 + K + len(Ns)))
 
