@@ -11,10 +11,15 @@
 // Summed over a lane's 32 triples the "- m" terms are just the number of negative triples, popcount(sign word),
 // so each lookup costs one XOR-add.
 //
-// Work split: one work group per 16-row group.  Each wave takes every WAVES-th 384-k block, builds the tables of
-// that block's 128 triples for the M tokens in its own LDS slice, and looks up its 16 rows x 128 triples.  The
-// slices of different q quarters are skewed by 32 bytes so the four quarters read disjoint LDS banks.  Waves
-// reduce through LDS; wave 0 applies the epilogue.
+// Three kernels:
+//   tl2_elut_decode_kernel   one work group per 16-row group; each wave takes every WAVES-th 384-k block, builds
+//                            the tables of that block's 128 triples for up to 8 tokens in its own LDS slice and
+//                            looks up its 16 rows x 128 triples (slices of different lane quarters skewed by 32 bytes
+//                            so the quarters read disjoint banks); waves reduce through LDS.
+//   tl2_stream_kernel        one token: persistent work groups build the tables of the whole row once and walk
+//                            row groups (the table-lookup route where the tables fit in LDS).
+//   tl2_mfma_decode_kernel   no activation tables: the packed triples are expanded to int8 weights through two
+//                            small constant tables and multiplied on int8 MFMA, shared by up to 16 tokens.
 #include "bitnet_internal.hpp"
 
 #include <algorithm>
