@@ -15,6 +15,8 @@ rather than from the 256 MB Infinity Cache.
 The K timed steps are captured once in a HIP graph and replayed, so the GPU runs them back to back.
 Prints one JSON line.  Decode: `value` = packed weight bytes per step / step time (GB/s), `roofline` bound
 "hbm".  Prefill: `value` = int8 TOP/s of the step (2*M*N*K per linear), `roofline` bound "mfma".
+`gweights_per_s` counts ternary weights per second (I2_S and TL2 on one scale); `ms_per_step_spread` gives the
+10th/50th/90th percentile of the per-step time over ten replays of the same graph (the first is the timed one).
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -22,6 +24,7 @@ from __future__ import annotations
 import argparse
 import json
 import math
+import os
 import sys
 import time
 
@@ -173,8 +176,22 @@ def main():
     wall = time.perf_counter() - w0
     ms_per_step = ev[0].elapsed_time(ev[1]) / args.steps
     second_ms = ev[1].elapsed_time(ev[2]) / args.steps
+    # spread: the same K steps replayed again, each replay timed on its own (outside the timed region above)
+    reps = [ms_per_step]
+    with torch.cuda.stream(stream):
+        for _ in range(SPREAD_REPLAYS - 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g_main.replay()
+            e1.record(stream)
+            e1.synchronize()
+            reps.append(e0.elapsed_time(e1) / args.steps)
+    reps.sort()
+    spread = {"replays": len(reps), "p10": round(reps[len(reps) // 10], 5), "p50": round(reps[len(reps) // 2], 5),
+              "p90": round(reps[min(len(reps) - 1, (9 * len(reps)) // 10)], 5)}
 
     flops = sum(2.0 * M * N * K for _, K, N in linears)
+    step_weights = sum(N * K for _, K, N in linears) * n_layers   # ternary weights read per step
     if decode:
         value = step_weight_bytes / (ms_per_step * 1e-3) / 1e9
         unit = "GB/s"
@@ -237,6 +254,8 @@ def main():
                    "linears": [f"{n}:{K}x{N}" for n, K, N in linears],
                    "packed_weight_bytes_per_step": step_weight_bytes, "rotating_copies": copies},
         "tokens_per_s": round(tokens_per_s, 1),
+        "gweights_per_s": round(step_weights / (ms_per_step * 1e-3) / 1e9, 2),
+        "ms_per_step_spread": spread,
         "hbm_frac_step": round(step_weight_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "mfma_frac_step": round(flops / (ms_per_step * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
         ("separate_path_ms_per_step" if decode else "gemm_only_ms_per_step"): round(second_ms, 5),
@@ -248,6 +267,7 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+SPREAD_REPLAYS = 10
 TRAFFIC_PROFILE = "profiles/decode_i2s_bitnet3b_m1_hbm_traffic.md"
 TRAFFIC_SOURCES = ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")
 
@@ -311,6 +331,17 @@ def parity_spot_check(args, layout, M, linears, packed, scales, xs, dev):
             "y_max_rel_err": rel}
 
 
+def cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or None."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, decode):
     """Time the oracle (quantise + exact integer accumulation + epilogue) on the host for ~cpu_seconds."""
     import torch
@@ -345,19 +376,20 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
         if el >= args.cpu_seconds:
             break
     per_step = el / steps
+    host = {"cpu_model": cpu_model(), "host_threads": os.cpu_count()}
     if decode and row_cap is not None:
         rate = sample_bytes / per_step            # packed-equivalent weight bytes per second
         return {"value": round(rate / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                 "sample": f"{steps} passes over the first {row_cap} output rows of each of the {len(linears)} "
                           f"linears of one layer (M={M}) in {el:.1f} s; numpy int64 matmul, one thread",
-                "tokens_per_s": round(M * rate / step_weight_bytes, 6)}
+                "tokens_per_s": round(M * rate / step_weight_bytes, 6), **host}
     if decode:
         return {"value": round(step_weight_bytes / per_step / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                 "sample": f"{steps} full steps of the same workload (all {len(linears)} linears, M={M}) in {el:.1f} s; "
-                          "numpy int64 matmul, one thread", "tokens_per_s": round(M / per_step, 3)}
+                          "numpy int64 matmul, one thread", "tokens_per_s": round(M / per_step, 3), **host}
     return {"value": round(flops * Mc / M / per_step / 1e12, 6), "unit": "TOP/s", "cores": 1, "kind": "oracle",
             "sample": f"{steps} steps of the same linears on {Mc} of the {M} token rows in {el:.1f} s; "
-                      "numpy int64 matmul, one thread", "tokens_per_s": round(Mc / per_step, 3)}
+                      "numpy int64 matmul, one thread", "tokens_per_s": round(Mc / per_step, 3), **host}
 
 
 if __name__ == "__main__":
