@@ -49,6 +49,25 @@ def test_quantize_act_many_rows(K):
     assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
 
 
+# Many rows longer than 4096 (one 256-lane group per row, up to 16 float4 per lane), with and without the code
+# sums; a zero row and a tie row placed late.
+@pytest.mark.parametrize("M,K,rowsum", [(2048, 14336, True), (1500, 8192, False), (3000, 12288, True),
+                                        (700, 16384, False)])
+def test_quantize_act_long_rows(M, K, rowsum):
+    _announce("quantize long rows", M, K, rowsum)
+    x = inputs.activation_f32(M, K, seed=inputs.seed_for(9, 6000 + M + K))
+    x[M - 3] = 0.0
+    x[M - 2, :6] = torch.tensor([127.0, 63.5, -0.5, 1.5, 2.5, -127.0])
+    x[M - 2, 6:] = 0.25
+    out = H.quantize(x, with_rowsum=rowsum)
+    xq, s = out[0], out[1]
+    xq_ref, s_ref = O.quantize_act(x.numpy())
+    assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(H.to_np(xq), xq_ref)
+    if rowsum:
+        assert np.array_equal(H.to_np(out[2]), xq_ref.astype(np.int64).sum(1))
+
+
 def test_quantize_act_constructed_ties_and_zero_rows():
     _announce("quantize constructed")
     x = torch.zeros((3, 64), dtype=torch.float32)
