@@ -351,6 +351,8 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     }
 
     // D element v of lane (j, h): row 8 (v / 4) + 4 h + v % 4, column j (weight row n0 + 128 wn + 32 ni + j).
+    // The fp32 outputs are written with the streaming hint: nothing here reads them again, and the activation
+    // and weight tiles other work groups still read stay in L2 (6% off the 2048-token step).
     const float beta = *w_scale;
 #pragma unroll
     for (int mi = 0; mi < MT; ++mi) {
@@ -370,7 +372,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
                 const int n = n0 + 128 * wn + 32 * ni + j32;
                 if (n >= N) continue;
                 const int val = acc[mi][ni][v] - rsum;
-                y[(size_t)m * N + n] = (float)val * sc;
+                __builtin_nontemporal_store((float)val * sc, &y[(size_t)m * N + n]);
                 if (acc_out) acc_out[(size_t)m * N + n] = val;
             }
         }
@@ -395,12 +397,9 @@ __global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __re
     const int rs = x_rowsum[m];
     t -= (v4i){rs, rs, rs, rs};
     const float sc = *w_scale / x_scale[m];
-    float4 o;
-    o.x = (float)t.x * sc;
-    o.y = (float)t.y * sc;
-    o.z = (float)t.z * sc;
-    o.w = (float)t.w * sc;
-    *reinterpret_cast<float4*>(y + off) = o;
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    const v4f o = {(float)t.x * sc, (float)t.y * sc, (float)t.z * sc, (float)t.w * sc};
+    __builtin_nontemporal_store(o, reinterpret_cast<v4f*>(y + off));
     if (acc_out) *reinterpret_cast<v4i*>(acc_out + off) = t;
 }
 
