@@ -222,8 +222,10 @@ def main():
         launches = len(groups) * n_layers
         avg_launch_ms = second_ms / launches
         achieved = (flops / launches) / (avg_launch_ms * 1e-3) / 1e12
-        roofline = {"bound": "mfma", "kernel": "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per "
-                                               "activation group)",
+        kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
+        if layout != "i2s":
+            kernel = "tl2_to_i2s_kernel per weight + " + kernel
+        roofline = {"bound": "mfma", "kernel": kernel,
                     "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": None,
                     "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_ops": int(flops / launches),

@@ -110,13 +110,16 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *          exactly (the same integers for every tiling and launch shape).
  *   ws     device workspace of at least bitnet_mpgemm_workspace_bytes(layout, M, N, K) bytes, or NULL when
  *          that is 0 (else BITNET_E_WORKSPACE).  It holds the exact int32 partial sums of a prefill GEMM split
- *          along K (I2_S, M > 16, small grids; only when x_rowsum is given); any contents on entry, nothing
- *          kept between calls.  Calls that run concurrently must not share it.
+ *          along K (M > 16, small grids; only when x_rowsum is given) and, for TL2 with M > 16, the weights
+ *          rewritten in the I2_S layout (N * K / 4 bytes) that the prefill GEMM reads; any contents on entry,
+ *          nothing kept between calls.  Calls that run concurrently must not share it.
  *   Shapes: M >= 1, N % 16 == 0, K % 64 == 0, K <= 132096 (127 * K < 2^24 keeps acc exact in fp32);
  *   I2_S also needs N * K and M * K below 2^32.  I2_S: M <= 16 runs the decode GEMV, larger M the prefill GEMM.
  *   TL2: one token runs the table lookups of Eq. 3 (tables built in LDS) where the row's tables fit (K <= 14336);
- *   otherwise, for 384 <= K < 18816, the packed triples are expanded to int8 weights and multiplied on int8 MFMA,
- *   in slices of up to 16 tokens; the remaining shapes run the table lookups in slices of 8 tokens.
+ *   otherwise, up to 16 tokens with 384 <= K < 18816, the packed triples are expanded to int8 weights and
+ *   multiplied on int8 MFMA; more than 16 tokens (with N * K and M * K below 2^32) rewrite the weights in the
+ *   I2_S layout in the workspace and run the I2_S prefill GEMM; the remaining shapes run the table lookups in
+ *   slices of 8 tokens.
  */
 bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale,
                             int64_t N, int64_t K, const int8_t* xq, const float* x_scale,
@@ -151,7 +154,9 @@ size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int6
  *   quantiser and then all products in one launch (the decode GEMV for M <= 16, the prefill GEMM over the
  *   weights' concatenated row tiles above).  TL2 with M == 1 and 384 <= K < 18816 also runs as one launch (the
  *   row quantised in every work group, the triples expanded for MFMA); other TL2 cases run the quantiser and
- *   then one launch for all weights (the MFMA expansion, K < 18816) or one table-lookup launch per weight.
+ *   then one launch for all weights (the MFMA expansion for M <= 16 and K < 18816; for M > 16, every weight
+ *   rewritten in the I2_S layout and one prefill launch, where ws holds all of them) or one bitnet_mpgemm call
+ *   per weight.
  */
 bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* packed, const size_t* packed_bytes,
                                   const float* const* w_scale, const int64_t* N, int64_t K, const float* x,

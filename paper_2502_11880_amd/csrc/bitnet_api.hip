@@ -60,6 +60,15 @@ bitnet::FusedLinears one_linear(const void* packed, const float* w_scale, int64_
     return L;
 }
 
+// TL2 at M > 16 runs the I2_S prefill GEMM on its weights rewritten in the I2_S layout (in the workspace), where
+// the I2_S limits hold.
+bool tl2_via_i2s(int64_t M, int64_t N, int64_t K) {
+    return M > kDecodeMaxTokens && (uint64_t)N * (uint64_t)K < ((uint64_t)1 << 32) &&
+           (uint64_t)M * (uint64_t)K < ((uint64_t)1 << 32);
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
 }  // namespace
 
 extern "C" {
@@ -109,6 +118,9 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
     if (!layout_ok(layout) || !weight_shape_ok(N, K) || M < 1) return 0;
     if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens)
         return bitnet::prefill_workspace_bytes(one_linear(nullptr, nullptr, N, nullptr, nullptr), M, K);
+    if (layout == BITNET_LAYOUT_TL2 && tl2_via_i2s(M, N, K))
+        return align256((size_t)N * (size_t)K / 4) +
+               bitnet::prefill_workspace_bytes(one_linear(nullptr, nullptr, N, nullptr, nullptr), M, K);
     return 0;
 }
 
@@ -121,12 +133,19 @@ size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int6
         const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
         need = w > need ? w : need;
     }
-    if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens) {
+    const bool tl2_gemm = layout == BITNET_LAYOUT_TL2 && M > kDecodeMaxTokens;
+    bool via = tl2_gemm;
+    for (int i = 0; i < n_linears; ++i) via = via && tl2_via_i2s(M, N[i], K);
+    if ((layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens) || via) {
         bitnet::FusedLinears L{};
         L.count = n_linears;
-        for (int i = 0; i < n_linears; ++i) L.N[i] = (int)N[i];
+        size_t words = 0;
+        for (int i = 0; i < n_linears; ++i) {
+            L.N[i] = (int)N[i];
+            if (via) words += align256((size_t)N[i] * (size_t)K / 4);
+        }
         bitnet::seal_fused(L);
-        const size_t split = bitnet::prefill_workspace_bytes(L, M, K);
+        const size_t split = words + bitnet::prefill_workspace_bytes(L, M, K);
         need = split > need ? split : need;
     }
     return need;
@@ -167,6 +186,15 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
         return hip_status(bitnet::launch_tl2_stream(one_linear(packed, w_scale, N, y, acc), nullptr, (int)K,
                                                     const_cast<int8_t*>(xq), const_cast<float*>(x_scale), nullptr, s),
                           "bitnet_mpgemm launch");
+    if (tl2_via_i2s(M, N, K)) {
+        // the weights in the I2_S layout at the start of the workspace, the GEMM's split-K slices after them
+        const size_t wbytes = align256((size_t)N * (size_t)K / 4);
+        hipError_t e = bitnet::launch_tl2_to_i2s(packed, (int)N, (int)K, ws, s);
+        if (e == hipSuccess)
+            e = bitnet::launch_i2s_prefill(one_linear(ws, w_scale, N, y, acc), xq, x_scale, x_rowsum, (int)M, (int)K,
+                                           static_cast<uint8_t*>(ws) + wbytes, ws_bytes - wbytes, s);
+        return hip_status(e, "bitnet_mpgemm launch");
+    }
     if (bitnet::tl2_mfma_max_tokens((int)K) > 0)
         return hip_status(bitnet::launch_tl2_mfma_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, (int)M,
                                                          (int)K, s),
@@ -267,7 +295,29 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     }
     hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
     if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm_fused launch");
-    if (bitnet::tl2_mfma_max_tokens((int)K) > 0)
+    // more than 16 tokens: every weight rewritten in the I2_S layout, then one prefill launch for all of them, where
+    // the workspace holds all the rewritten weights (else one bitnet_mpgemm per weight, below)
+    bool via = M > kDecodeMaxTokens;
+    size_t words = 0;
+    for (int i = 0; i < n_linears; ++i) {
+        via = via && tl2_via_i2s(M, N[i], K);
+        words += align256((size_t)N[i] * (size_t)K / 4);
+    }
+    if (via && ws_bytes >= words) {
+        bitnet::FusedLinears T = L;
+        size_t off = 0;
+        for (int i = 0; i < n_linears && e == hipSuccess; ++i) {
+            uint8_t* dst = static_cast<uint8_t*>(ws) + off;
+            e = bitnet::launch_tl2_to_i2s(packed[i], (int)N[i], (int)K, dst, s);
+            T.packed[i] = dst;
+            off += align256((size_t)N[i] * (size_t)K / 4);
+        }
+        if (e == hipSuccess)
+            e = bitnet::launch_i2s_prefill(T, xq, x_scale, x_rowsum, (int)M, (int)K, static_cast<uint8_t*>(ws) + words,
+                                           ws_bytes - words, s);
+        return hip_status(e, "bitnet_mpgemm_fused launch");
+    }
+    if (M <= kDecodeMaxTokens && bitnet::tl2_mfma_max_tokens((int)K) > 0)
         return hip_status(bitnet::launch_tl2_mfma_decode(L, xq, x_scale, (int)M, (int)K, s),
                           "bitnet_mpgemm_fused launch");
     for (int i = 0; i < n_linears; ++i) {

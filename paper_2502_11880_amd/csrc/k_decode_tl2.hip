@@ -744,6 +744,67 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
     else run(std::true_type{});
 }
 
+// TL2 -> I2_S transcoding, for the prefill GEMM (M > 16): the I2_S MFMA GEMM then runs on the same ternary
+// weights.  A lane expands its 32 triples (one row, 96 consecutive k of a 384-k block) through the expansion
+// tables as the MFMA decode kernel does and writes them as six I2_S words: the word of row n and k0 (a multiple
+// of 16) holds code t + 1 of k = k0 + 4f + b in bits 2f + 8b, at word R K + 256 s + l T + j of the I2_S array
+// (R = n / 16, block s = k0 / 256, sub-tile j = (k0 mod 256) / 64, lane chunk l = 16 ((k0 mod 64) / 16) + n mod 16,
+// T = the block's sub-tiles).  Tail units (TL1 pairs, Table 5) give one word per lane each.
+__device__ __forceinline__ uint32_t i2s_word_of(const uint32_t* d) {
+    // t in {-1, 0, 1} per byte -> code t + 1 in the low two bits of each byte
+    uint32_t w = 0;
+#pragma unroll
+    for (int f = 0; f < 4; ++f) w |= (((d[f] & 0x03030303u) + 0x01010101u) & 0x03030303u) << (2 * f);
+    return w;
+}
+
+__device__ __forceinline__ size_t i2s_word_index(int n, int k0, int K) {
+    const int R = n / kRowsPerGroup, r = n % kRowsPerGroup;
+    const int sb = k0 / kI2sBlockK, rem = k0 % kI2sBlockK;
+    const int j = rem / kSubK, q = (rem % kSubK) / 16;
+    const int T = min(4, K / kSubK - 4 * sb);
+    return (size_t)R * K + (size_t)kI2sBlockK * sb + (size_t)(16 * q + r) * T + j;
+}
+
+__global__ __launch_bounds__(256) void tl2_to_i2s_kernel(const uint8_t* __restrict__ packed, int N, int K,
+                                                         uint32_t* __restrict__ out) {
+    __shared__ __align__(16) uint8_t tab[kTl2MfmaTables];
+    for (int c = threadIdx.x; c < kTableChunks; c += 256)
+        reinterpret_cast<v4u*>(tab)[c] = reinterpret_cast<const v4u*>(kExpandTables.w)[c];
+    __syncthreads();
+    const int three = (K / kTl2BlockK) * kTl2BlockK;
+    const int nblk = three / kTl2BlockK;
+    const int units = (K - three) / kSubK;
+    const uint8_t* idx_plane = packed;
+    const uint8_t* sign_plane = packed + (size_t)N * (three / 6);
+    const uint8_t* tail_plane = sign_plane + (size_t)N * (three / 24);
+    const size_t main_items = (size_t)(N / kRowsPerGroup) * nblk * 64;     // lane chunks of the TL2 blocks
+    const size_t tail_items = (size_t)(N / kRowsPerGroup) * 64 * units;    // tail words
+    const size_t c = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (c < main_items) {
+        const size_t tile = c >> 6;                       // (row group, block)
+        const int l = (int)(c & 63), q = l >> 4, r = l & 15;
+        const int R = (int)(tile / nblk), blk = (int)(tile - (size_t)R * nblk);
+        const v4u iw = *reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * l);
+        const uint32_t sw = *reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * l);
+        uint32_t wd[24];
+        expand_triples(iw, sw, reinterpret_cast<const uint2*>(tab), wd);
+        const int n = R * kRowsPerGroup + r;
+        const int base = blk * kTl2BlockK + 96 * q;
+#pragma unroll
+        for (int g = 0; g < 6; ++g) out[i2s_word_index(n, base + 16 * g, K)] = i2s_word_of(wd + 4 * g);
+    } else if (c < main_items + tail_items) {
+        const size_t t = c - main_items;                  // (row group, lane, unit), as the tail plane
+        const int u = (int)(t % units);
+        const int l = (int)((t / units) & 63), q = l >> 4, r = l & 15;
+        const int R = (int)(t / ((size_t)64 * units));
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(tail_plane + t * 4);
+        const uint32_t* ptab = reinterpret_cast<const uint32_t*>(tab + kIdxTableBytes);
+        const uint32_t d[4] = {ptab[w & 0xFFu], ptab[(w >> 8) & 0xFFu], ptab[(w >> 16) & 0xFFu], ptab[w >> 24]};
+        out[i2s_word_index(R * kRowsPerGroup + r, three + kSubK * u + 16 * q, K)] = i2s_word_of(d);
+    }
+}
+
 // Standalone table precompute: the same tables, written to global memory for inspection.
 __global__ __launch_bounds__(256) void elut_tables_kernel(const int8_t* __restrict__ xq, int M, int K,
                                                           int16_t* __restrict__ lut, int16_t* __restrict__ lut1) {
@@ -957,6 +1018,14 @@ hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_tl2_to_i2s(const void* packed, int N, int K, void* i2s_out, hipStream_t stream) {
+    const int three = (K / kTl2BlockK) * kTl2BlockK;
+    const size_t items = (size_t)(N / kRowsPerGroup) * 64 * ((three / kTl2BlockK) + (K - three) / kSubK);
+    hipLaunchKernelGGL(tl2_to_i2s_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, stream,
+                       static_cast<const uint8_t*>(packed), N, K, static_cast<uint32_t*>(i2s_out));
+    return hipGetLastError();
 }
 
 hipError_t launch_elut_tables(const int8_t* xq, int M, int K, int16_t* lut, int16_t* lut1, hipStream_t stream) {

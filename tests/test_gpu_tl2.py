@@ -157,3 +157,47 @@ def test_tl2_mfma_fused(K, Ns):
     _announce("tl2 mfma fused", 8, K, Ns)
     from tests.test_gpu_fused import _fused_case
     _fused_case("tl2", 8, K, Ns, seed=inputs.seed_for(8, 1500 + K + len(Ns)))
+
+
+# More than 16 tokens: the TL2 weights rewritten in the I2_S layout (in the workspace), then the I2_S prefill GEMM
+# on them; TL1 tails of 0 to 5 units (K = 320 has no 384-k block at all), ragged token tiles, with and without
+# the token sums given (split-K needs them).
+@pytest.mark.parametrize("M,N,K", [(17, 48, 448), (40, 48, 832), (33, 16, 320), (64, 96, 1536), (129, 208, 3200),
+                                   (300, 512, 4096), (200, 64, 6080)])
+@pytest.mark.parametrize("rowsum", [False, True])
+def test_tl2_prefill(M, N, K, rowsum):
+    _announce("tl2 prefill", M, N, K, rowsum)
+    W = inputs.weight_f32(N, K, seed=inputs.seed_for(8, 1700 + M + N + K))
+    x = inputs.activation_f32(M, K, seed=inputs.seed_for(8, 1800 + M + K))
+    packed, w_scale = H.pack(W, "tl2")
+    xq, s, rs = H.quantize(x, with_rowsum=True)
+    y, acc = H.mpgemm("tl2", packed, w_scale, N, K, xq, s, x_rowsum=rs if rowsum else None)
+    y_ref, acc_ref, *_ = O.mpgemm_reference(x.numpy(), W.numpy())
+    assert np.array_equal(H.to_np(acc), acc_ref)
+    H.check_y(H.to_np(y), y_ref, acc_ref)
+
+
+# The 8B-class shapes at 2048 tokens (sampled rows) and a fused group (one prefill launch for all weights).
+def test_tl2_prefill_workload():
+    _announce("tl2 prefill workload", 2048, 14336, 4096)
+    M, N, K = 2048, 14336, 4096
+    W = inputs.weight_f32(N, K, seed=inputs.seed_for(8, 1900))
+    x = inputs.activation_f32(M, K, seed=inputs.seed_for(8, 1901))
+    packed, w_scale = H.pack(W, "tl2")
+    xq, s, rs = H.quantize(x, with_rowsum=True)
+    y, acc = H.mpgemm("tl2", packed, w_scale, N, K, xq, s, x_rowsum=rs)
+    xq_ref, s_ref = O.quantize_act(x.numpy())
+    t_ref, beta = O.ternarize(W.numpy())
+    rows = np.unique(np.r_[0, M - 1, np.random.default_rng(3).choice(M, 6, False)])
+    acc_ref = O.mad_gemm(xq_ref[rows], t_ref)
+    assert np.array_equal(H.to_np(acc)[rows], acc_ref)
+    H.check_y(H.to_np(y)[rows], O.epilogue(acc_ref, beta, s_ref[rows]), acc_ref)
+
+
+@pytest.mark.parametrize("M,K,Ns,split_ws", [(600, 1536, [512, 1024, 2048], True), (40, 832, [48, 16, 64], False),
+                                             (2048, 4096, [4096, 1024, 1024], True)])
+def test_tl2_prefill_fused(M, K, Ns, split_ws):
+    _announce("tl2 prefill fused", M, K, Ns, split_ws)
+    from tests.test_gpu_fused import _fused_case
+    _fused_case("tl2", M, K, Ns, seed=inputs.seed_for(8, 2000 + M + K), split_ws=split_ws,
+                sample_rows=6 if M >= 2048 else None)
