@@ -379,28 +379,43 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     }
 }
 
-// Sum of the split-K slices of one weight (its M x N block in every slice of `slice` words), then the epilogue:
-// y = (sum - sum_k xq[m, k]) * (beta / s_m).  Four outputs of one row per thread.
-__global__ __launch_bounds__(256) void prefill_splitk_finish(const int32_t* __restrict__ part, int64_t slice,
-                                                             int splits, int M, int N,
+// Sum of the split-K slices, then the epilogue y = (sum - sum_k xq[m, k]) * (beta / s_m), for every weight of the
+// launch in one pass: output quad i4 belongs to the weight whose run of M N / 4 quads holds it (a scalar-free
+// compare chain over the fixed maximum).  Each weight's block in a slice starts at its part offset; slices are
+// `slice` words apart.
+struct FinishLinears {
+    float* y[kMaxFused];
+    int32_t* acc[kMaxFused];
+    const float* w_scale[kMaxFused];
+    long long part_off[kMaxFused];
+    long long start4[kMaxFused];      // first output quad of each weight; LLONG_MAX past the last
+    int N[kMaxFused];
+    long long total4;
+};
+
+__global__ __launch_bounds__(256) void prefill_splitk_finish(FinishLinears F, const int32_t* __restrict__ part,
+                                                             int64_t slice, int splits, int M,
                                                              const int32_t* __restrict__ x_rowsum,
-                                                             const float* __restrict__ x_scale,
-                                                             const float* __restrict__ w_scale, float* __restrict__ y,
-                                                             int32_t* __restrict__ acc_out) {
-    const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;      // index of 4 outputs
-    const int n4 = N >> 2;
-    if (i4 >= (int64_t)M * n4) return;
-    const int m = (int)(i4 / n4);
-    const size_t off = (size_t)i4 * 4;
+                                                             const float* __restrict__ x_scale) {
+    const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i4 >= F.total4) return;
+    int li = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxFused; ++i) li = i4 >= F.start4[i] ? i : li;
+    const int64_t local = i4 - pick_linear(F.start4, li);
+    const int N = pick_linear(F.N, li);
+    const int m = (int)(local / (N >> 2));
+    const size_t off = (size_t)pick_linear(F.part_off, li) + (size_t)local * 4;
     v4i t = *reinterpret_cast<const v4i*>(part + off);
     for (int sp = 1; sp < splits; ++sp) t += *reinterpret_cast<const v4i*>(part + (size_t)sp * slice + off);
     const int rs = x_rowsum[m];
     t -= (v4i){rs, rs, rs, rs};
-    const float sc = *w_scale / x_scale[m];
+    const float sc = *pick_linear(F.w_scale, li) / x_scale[m];
     typedef float v4f __attribute__((ext_vector_type(4)));
     const v4f o = {(float)t.x * sc, (float)t.y * sc, (float)t.z * sc, (float)t.w * sc};
-    __builtin_nontemporal_store(o, reinterpret_cast<v4f*>(y + off));
-    if (acc_out) *reinterpret_cast<v4i*>(acc_out + off) = t;
+    __builtin_nontemporal_store(o, reinterpret_cast<v4f*>(pick_linear(F.y, li) + (size_t)local * 4));
+    int32_t* acc_out = pick_linear(F.acc, li);
+    if (acc_out) *reinterpret_cast<v4i*>(acc_out + (size_t)local * 4) = t;
 }
 
 // Tile width and split-K factor for the weight tiles of a launch.  Whichever of the 128 x 512 and 128 x 256 tiles
@@ -500,14 +515,24 @@ hipError_t launch_i2s_prefill(const FusedLinears& L, const int8_t* xq, const flo
     else
         launch_wn<2>(L, xq, x_scale, x_rowsum, M, K, splits, part, stream);
     if (splits > 1) {
-        int64_t off = 0;
-        for (int i = 0; i < L.count; ++i) {
-            const int64_t n4 = (int64_t)M * (L.N[i] / 4);
-            hipLaunchKernelGGL(prefill_splitk_finish, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream,
-                               part + off, (int64_t)M * ntot, splits, M, L.N[i], x_rowsum, x_scale, L.w_scale[i],
-                               L.y[i], L.acc[i]);
-            off += (int64_t)M * L.N[i];
+        FinishLinears F{};
+        int64_t off = 0, q4 = 0;
+        for (int i = 0; i < kMaxFused; ++i) {
+            const bool live = i < L.count;
+            F.y[i] = L.y[live ? i : 0];
+            F.acc[i] = L.acc[live ? i : 0];
+            F.w_scale[i] = L.w_scale[live ? i : 0];
+            F.N[i] = L.N[live ? i : 0];
+            F.part_off[i] = live ? off : 0;
+            F.start4[i] = live ? q4 : 0x7fffffffffffffffLL;
+            if (live) {
+                off += (int64_t)M * L.N[i];
+                q4 += (int64_t)M * (L.N[i] / 4);
+            }
         }
+        F.total4 = q4;
+        hipLaunchKernelGGL(prefill_splitk_finish, dim3((unsigned)((q4 + 255) / 256)), dim3(256), 0, stream, F, part,
+                           (int64_t)M * ntot, splits, M, x_rowsum, x_scale);
     }
     return hipGetLastError();
 }
