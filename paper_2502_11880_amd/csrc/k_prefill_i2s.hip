@@ -29,7 +29,9 @@
 // token tiles so that the work groups resident on one XCD share activation and weight tiles in its L2.
 //
 // The codes are t + 1: sum_k xq[m, k] is subtracted in the epilogue, either from x_rowsum (written by the
-// quantiser) or summed here from the activation operands.
+// quantiser) or summed here from the activation operands.  The epilogue goes through LDS in two passes of 64
+// token rows, so every wave stores 1 KiB runs of one output row (16 bytes per lane, streaming hint) instead of
+// 128-byte pieces of two rows per scalar store.
 #include "bitnet_internal.hpp"
 
 namespace bitnet {
@@ -289,8 +291,8 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     }
 
     // The K-groups past the first hand their partial tiles to the first through LDS (the staging buffers are free
-    // once every wave has passed the barrier below); every wave passes every barrier, and only the first K-group
-    // stores.  Token sums: from x_rowsum, or each K-group's partial from its activation operands.
+    // once every wave has passed the barrier below).  Token sums: from x_rowsum, or each K-group's partial from its
+    // activation operands.  Every wave passes every barrier up to the split-K return.
     __syncthreads();
     v4i* red = reinterpret_cast<v4i*>(smem);                      // [wave tile][mi][ni][4 words][lane]
     const int slot = (wm * WN + wn) * (MT * NT * 4);
@@ -315,8 +317,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
         }
     }
     __syncthreads();
-    if (wk != 0) return;                                          // no barrier follows
-    if (WK > 1) {
+    if (WK > 1 && wk == 0) {
 #pragma unroll
         for (int mi = 0; mi < MT; ++mi)
 #pragma unroll
@@ -334,6 +335,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
     if (part) {
         // split-K: this slice's exact partial sums (the code offset and the scales are applied when the slices
         // are summed)
+        if (wk != 0) return;
         int32_t* pp = part + (size_t)split * M * P.n_total;
 #pragma unroll
         for (int mi = 0; mi < MT; ++mi)
@@ -350,30 +352,51 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
         return;
     }
 
+    // Epilogue in two passes of 64 token rows (MFMA row tile mi of both wave rows): the waves holding the sums
+    // write y = (acc - sum_k xq) * beta / s_m into LDS (row stride kBN + 8 floats: the two half-waves of a write
+    // land on different banks), then every thread copies whole 16-byte runs of rows out, so a wave's store is
+    // 1 KiB of one output row.  The stores carry the streaming hint: nothing here reads y again.
     // D element v of lane (j, h): row 8 (v / 4) + 4 h + v % 4, column j (weight row n0 + 128 wn + 32 ni + j).
-    // The fp32 outputs are written with the streaming hint: nothing here reads them again, and the activation
-    // and weight tiles other work groups still read stay in L2 (6% off the 2048-token step).
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    constexpr int kYRow = kBN + 8;
+    static_assert(64 * kYRow * 4 <= kSmem, "one pass of the output tile fits the staging LDS");
+    float* ybuf = reinterpret_cast<float*>(smem);
     const float beta = *w_scale;
+    constexpr int kQuads = 64 * kBN / 4, kQPerRow = kBN / 4;
 #pragma unroll
     for (int mi = 0; mi < MT; ++mi) {
+        __syncthreads();                                          // LDS free: partial tiles or the previous pass read
+        if (wk == 0) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int ml = 64 * wm + 32 * mi + 8 * (v >> 2) + 4 * h + (v & 3);
-            const int m = m0 + ml;
-            if (m >= M) continue;
-            int rsum = rowsum_s[0][ml];
-            if (!HAS_RS) {
+            for (int v = 0; v < 16; ++v) {
+                const int rr = 8 * (v >> 2) + 4 * h + (v & 3);
+                const int ml = 64 * wm + 32 * mi + rr;
+                const int m = min(m0 + ml, M - 1);
+                int rsum = rowsum_s[0][ml];
+                if (!HAS_RS) {
 #pragma unroll
-                for (int g = 1; g < WK; ++g) rsum += rowsum_s[g][ml];
+                    for (int g = 1; g < WK; ++g) rsum += rowsum_s[g][ml];
+                }
+                const float sc = beta / x_scale[m];
+#pragma unroll
+                for (int ni = 0; ni < NT; ++ni) {
+                    const int nl = 128 * wn + 32 * ni + j32;
+                    const int val = acc[mi][ni][v] - rsum;
+                    ybuf[(32 * wm + rr) * kYRow + nl] = (float)val * sc;
+                    if (acc_out && m0 + ml < M && n0 + nl < N) acc_out[(size_t)(m0 + ml) * N + n0 + nl] = val;
+                }
             }
-            const float sc = beta / x_scale[m];
+        }
+        __syncthreads();
 #pragma unroll
-            for (int ni = 0; ni < NT; ++ni) {
-                const int n = n0 + 128 * wn + 32 * ni + j32;
-                if (n >= N) continue;
-                const int val = acc[mi][ni][v] - rsum;
-                __builtin_nontemporal_store((float)val * sc, &y[(size_t)m * N + n]);
-                if (acc_out) acc_out[(size_t)m * N + n] = val;
+        for (int i = 0; i < kQuads / kThreads; ++i) {
+            const int f = tid + i * kThreads;
+            const int lr = f / kQPerRow, c4 = f - lr * kQPerRow;
+            const int m = m0 + 64 * (lr >> 5) + 32 * mi + (lr & 31);
+            const int n = n0 + 4 * c4;
+            if (m < M && n < N) {
+                const v4f o = *reinterpret_cast<const v4f*>(ybuf + lr * kYRow + 4 * c4);
+                __builtin_nontemporal_store(o, reinterpret_cast<v4f*>(y + (size_t)m * N + n));
             }
         }
     }
