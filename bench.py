@@ -210,7 +210,7 @@ def main():
         else:
             kernel = "bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_stream_kernel per group"
         default_workload = (args.workload, M, layout) == (1, 1, "i2s")
-        traffic = measured_traffic() if default_workload else None
+        traffic = measured_traffic(*TRAFFIC["decode"]) if default_workload else None
         roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                     "traffic_unit": "bytes per launch (FETCH_SIZE x copy factor + WRITE_SIZE)" if traffic else None,
@@ -225,9 +225,11 @@ def main():
         kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
         if layout != "i2s":
             kernel = "tl2_to_i2s_kernel per weight + " + kernel
+        traffic = measured_traffic(*TRAFFIC["prefill"]) if (args.workload, M, layout) == (3, 2048, "i2s") else None
         roofline = {"bound": "mfma", "kernel": kernel,
                     "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-                    "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": None,
+                    "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": traffic,
+                    "traffic_unit": "bytes per launch (FETCH_SIZE x copy factor + WRITE_SIZE)" if traffic else None,
                     "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_ops": int(flops / launches),
                     "launches_per_step": launches}
     tokens_per_s = M / (ms_per_step * 1e-3)
@@ -270,8 +272,13 @@ def main():
 
 
 SPREAD_REPLAYS = 10
-TRAFFIC_PROFILE = "profiles/decode_i2s_bitnet3b_m1_hbm_traffic.md"
-TRAFFIC_SOURCES = ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")
+# committed counter summaries (HBM bytes per launch) and the kernel sources they were taken on
+TRAFFIC = {
+    "decode": ("profiles/decode_i2s_bitnet3b_m1_hbm_traffic.md",
+               ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")),
+    "prefill": ("profiles/prefill_i2s_llama8b_m2048_hbm_traffic.md",
+                ("paper_2502_11880_amd/csrc/k_prefill_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")),
+}
 
 
 def code_only(text):
@@ -280,17 +287,17 @@ def code_only(text):
     return "\n".join(line for line in lines if line)
 
 
-def measured_traffic():
-    """HBM bytes per launch of the default decode workload from the committed counter summary, or None when
-    the kernel sources no longer hash to the ones the counters were taken on."""
+def measured_traffic(profile, sources):
+    """HBM bytes per launch from a committed counter summary, or None when the kernel sources no longer hash to
+    the ones the counters were taken on."""
     import hashlib
     import os
 
     root = os.path.dirname(os.path.abspath(__file__))
     try:
-        text = open(os.path.join(root, TRAFFIC_PROFILE)).read()
+        text = open(os.path.join(root, profile)).read()
         h = hashlib.sha256()
-        for f in TRAFFIC_SOURCES:
+        for f in sources:
             h.update(code_only(open(os.path.join(root, f)).read()).encode())
     except OSError:
         return None
