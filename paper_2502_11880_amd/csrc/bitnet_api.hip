@@ -189,7 +189,9 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
     if (tl2_via_i2s(M, N, K)) {
         // the weights in the I2_S layout at the start of the workspace, the GEMM's split-K slices after them
         const size_t wbytes = align256((size_t)N * (size_t)K / 4);
-        hipError_t e = bitnet::launch_tl2_to_i2s(packed, (int)N, (int)K, ws, s);
+        const int n1 = (int)N;
+        void* dst = ws;
+        hipError_t e = bitnet::launch_tl2_to_i2s(&packed, &n1, &dst, 1, (int)K, s);
         if (e == hipSuccess)
             e = bitnet::launch_i2s_prefill(one_linear(ws, w_scale, N, y, acc), xq, x_scale, x_rowsum, (int)M, (int)K,
                                            static_cast<uint8_t*>(ws) + wbytes, ws_bytes - wbytes, s);
@@ -306,12 +308,15 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (via && ws_bytes >= words) {
         bitnet::FusedLinears T = L;
         size_t off = 0;
-        for (int i = 0; i < n_linears && e == hipSuccess; ++i) {
-            uint8_t* dst = static_cast<uint8_t*>(ws) + off;
-            e = bitnet::launch_tl2_to_i2s(packed[i], (int)N[i], (int)K, dst, s);
-            T.packed[i] = dst;
+        void* dst[bitnet::kMaxFused];
+        int n32[bitnet::kMaxFused];
+        for (int i = 0; i < n_linears; ++i) {
+            dst[i] = static_cast<uint8_t*>(ws) + off;
+            n32[i] = (int)N[i];
+            T.packed[i] = static_cast<const uint8_t*>(dst[i]);
             off += align256((size_t)N[i] * (size_t)K / 4);
         }
+        e = bitnet::launch_tl2_to_i2s(packed, n32, dst, n_linears, (int)K, s);
         if (e == hipSuccess)
             e = bitnet::launch_i2s_prefill(T, xq, x_scale, x_rowsum, (int)M, (int)K, static_cast<uint8_t*>(ws) + words,
                                            ws_bytes - words, s);

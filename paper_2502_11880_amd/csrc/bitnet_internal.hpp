@@ -188,8 +188,10 @@ hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const
                                   hipStream_t stream);
 hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                                  int32_t* x_rowsum, hipStream_t stream);
-// The TL2 weights of an N x K tensor rewritten in the I2_S layout (N K / 4 bytes at i2s_out), for the prefill GEMM.
-hipError_t launch_tl2_to_i2s(const void* packed, int N, int K, void* i2s_out, hipStream_t stream);
+// The TL2 weights of `count` (1..kMaxFused) N[i] x K tensors rewritten in the I2_S layout (N[i] K / 4 bytes at
+// i2s_out[i]), for the prefill GEMM; one launch.
+hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* const* i2s_out, int count, int K,
+                             hipStream_t stream);
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                              int32_t* x_rowsum, hipStream_t stream);
 

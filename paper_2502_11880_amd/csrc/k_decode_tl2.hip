@@ -744,6 +744,15 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
     else run(std::true_type{});
 }
 
+// The weights of one transcoding launch: item runs start at start[i] (LLONG_MAX past the last weight).
+struct TranscodeLinears {
+    const uint8_t* packed[kMaxFused];
+    uint32_t* out[kMaxFused];
+    int N[kMaxFused];
+    long long start[kMaxFused];
+    long long total;
+};
+
 // TL2 -> I2_S transcoding, for the prefill GEMM (M > 16): the I2_S MFMA GEMM then runs on the same ternary
 // weights.  A lane expands its 32 triples (one row, 96 consecutive k of a 384-k block) through the expansion
 // tables as the MFMA decode kernel does and writes them as six I2_S words: the word of row n and k0 (a multiple
@@ -766,41 +775,57 @@ __device__ __forceinline__ size_t i2s_word_index(int n, int k0, int K) {
     return (size_t)R * K + (size_t)kI2sBlockK * sb + (size_t)(16 * q + r) * T + j;
 }
 
-__global__ __launch_bounds__(256) void tl2_to_i2s_kernel(const uint8_t* __restrict__ packed, int N, int K,
-                                                         uint32_t* __restrict__ out) {
+// One launch rewrites every weight of a fused group: item c belongs to the weight whose run of items holds it (a
+// compare chain over the fixed maximum; runs are whole waves).  A thread's packed words are loaded before the
+// table image is copied into LDS, so the two loads overlap instead of following each other.
+__global__ __launch_bounds__(256) void tl2_to_i2s_kernel(TranscodeLinears T, int K) {
     __shared__ __align__(16) uint8_t tab[kTl2MfmaTables];
-    for (int c = threadIdx.x; c < kTableChunks; c += 256)
-        reinterpret_cast<v4u*>(tab)[c] = reinterpret_cast<const v4u*>(kExpandTables.w)[c];
-    __syncthreads();
     const int three = (K / kTl2BlockK) * kTl2BlockK;
     const int nblk = three / kTl2BlockK;
     const int units = (K - three) / kSubK;
+    const long long c_all = (long long)blockIdx.x * 256 + threadIdx.x;
+    int li = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxFused; ++i) li = c_all >= T.start[i] ? i : li;
+    const int N = T.N[li];
+    const uint8_t* packed = T.packed[li];
+    uint32_t* __restrict__ out = T.out[li];
     const uint8_t* idx_plane = packed;
     const uint8_t* sign_plane = packed + (size_t)N * (three / 6);
     const uint8_t* tail_plane = sign_plane + (size_t)N * (three / 24);
     const size_t main_items = (size_t)(N / kRowsPerGroup) * nblk * 64;     // lane chunks of the TL2 blocks
     const size_t tail_items = (size_t)(N / kRowsPerGroup) * 64 * units;    // tail words
-    const size_t c = (size_t)blockIdx.x * 256 + threadIdx.x;
-    if (c < main_items) {
+    const size_t c = (size_t)(c_all - T.start[li]);
+    const bool is_main = c_all < T.total && c < main_items;
+    const bool is_tail = c_all < T.total && !is_main && c < main_items + tail_items;
+    v4u iw = {0u, 0u, 0u, 0u};
+    uint32_t sw = 0u, tw = 0u;
+    if (is_main) {
+        iw = *reinterpret_cast<const v4u*>(idx_plane + (c >> 6) * 1024 + 16 * (c & 63));
+        sw = *reinterpret_cast<const uint32_t*>(sign_plane + (c >> 6) * 256 + 4 * (c & 63));
+    } else if (is_tail) {
+        tw = *reinterpret_cast<const uint32_t*>(tail_plane + (c - main_items) * 4);
+    }
+    for (int i = threadIdx.x; i < kTableChunks; i += 256)
+        reinterpret_cast<v4u*>(tab)[i] = reinterpret_cast<const v4u*>(kExpandTables.w)[i];
+    __syncthreads();
+    if (is_main) {
         const size_t tile = c >> 6;                       // (row group, block)
         const int l = (int)(c & 63), q = l >> 4, r = l & 15;
         const int R = (int)(tile / nblk), blk = (int)(tile - (size_t)R * nblk);
-        const v4u iw = *reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * l);
-        const uint32_t sw = *reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * l);
         uint32_t wd[24];
         expand_triples(iw, sw, reinterpret_cast<const uint2*>(tab), wd);
         const int n = R * kRowsPerGroup + r;
         const int base = blk * kTl2BlockK + 96 * q;
 #pragma unroll
         for (int g = 0; g < 6; ++g) out[i2s_word_index(n, base + 16 * g, K)] = i2s_word_of(wd + 4 * g);
-    } else if (c < main_items + tail_items) {
+    } else if (is_tail) {
         const size_t t = c - main_items;                  // (row group, lane, unit), as the tail plane
         const int u = (int)(t % units);
         const int l = (int)((t / units) & 63), q = l >> 4, r = l & 15;
         const int R = (int)(t / ((size_t)64 * units));
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(tail_plane + t * 4);
         const uint32_t* ptab = reinterpret_cast<const uint32_t*>(tab + kIdxTableBytes);
-        const uint32_t d[4] = {ptab[w & 0xFFu], ptab[(w >> 8) & 0xFFu], ptab[(w >> 16) & 0xFFu], ptab[w >> 24]};
+        const uint32_t d[4] = {ptab[tw & 0xFFu], ptab[(tw >> 8) & 0xFFu], ptab[(tw >> 16) & 0xFFu], ptab[tw >> 24]};
         out[i2s_word_index(R * kRowsPerGroup + r, three + kSubK * u + 16 * q, K)] = i2s_word_of(d);
     }
 }
@@ -1020,11 +1045,26 @@ hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const
     return hipSuccess;
 }
 
-hipError_t launch_tl2_to_i2s(const void* packed, int N, int K, void* i2s_out, hipStream_t stream) {
+size_t tl2_to_i2s_items(int N, int K) {
     const int three = (K / kTl2BlockK) * kTl2BlockK;
-    const size_t items = (size_t)(N / kRowsPerGroup) * 64 * ((three / kTl2BlockK) + (K - three) / kSubK);
-    hipLaunchKernelGGL(tl2_to_i2s_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, stream,
-                       static_cast<const uint8_t*>(packed), N, K, static_cast<uint32_t*>(i2s_out));
+    return (size_t)(N / kRowsPerGroup) * 64 * ((three / kTl2BlockK) + (K - three) / kSubK);
+}
+
+hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* const* i2s_out, int count, int K,
+                             hipStream_t stream) {
+    if (count < 1 || count > kMaxFused) return hipErrorInvalidValue;
+    TranscodeLinears T{};
+    long long items = 0;
+    for (int i = 0; i < kMaxFused; ++i) {
+        const int j = i < count ? i : 0;
+        T.packed[i] = static_cast<const uint8_t*>(packed[j]);
+        T.out[i] = static_cast<uint32_t*>(i2s_out[j]);
+        T.N[i] = N[j];
+        T.start[i] = i < count ? items : 0x7fffffffffffffffLL;
+        if (i < count) items += (long long)tl2_to_i2s_items(N[i], K);
+    }
+    T.total = items;
+    hipLaunchKernelGGL(tl2_to_i2s_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, stream, T, K);
     return hipGetLastError();
 }
 
