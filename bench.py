@@ -202,7 +202,7 @@ def main():
         avg_launch_ms = ms_per_step / launches
         achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
         if layout != "i2s" and M == 1:
-            kernel = "tl2_stream_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
+            kernel = "tl2_mfma_decode_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
         elif layout != "i2s":
             kernel = "bitnet_mpgemm_fused on TL2: quantize_rows_reg + tl2_mfma_decode_kernel per group"
         elif M == 1:
