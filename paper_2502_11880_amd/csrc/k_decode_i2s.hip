@@ -663,8 +663,9 @@ hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K,
                                    int32_t* x_rowsum, hipStream_t stream) {
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int cus = device_cus();
-    if (L.total > 2 * cus && L.total <= 8 * cus && nkb <= 16) {
-        // every row group in flight at once: one per 4-wave work group, up to eight such groups per CU
+    if (L.total > cus / 2 && L.total <= 8 * cus && nkb <= 16) {
+        // every row group in flight at once: one per 4-wave work group, from half a group per CU up to eight per
+        // CU (a 16-wave group waits on its slowest wave at the quantisation and at the reduction)
         const int u = (nkb + 3) / 4;
         if (u <= 1) return launch_stream_xv<4, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
         if (u <= 2) return launch_stream_xv<4, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
