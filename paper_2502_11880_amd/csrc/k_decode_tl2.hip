@@ -1013,7 +1013,8 @@ hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, i
     const int nblk = K / kTl2BlockK;
     if (tl2_mfma_max_tokens(K) < 1) return hipErrorInvalidValue;
     if (nblk <= 4) return launch_mfma_quant<4, 1>(L, x, xq, x_scale, x_rowsum, K, stream);
-    if (nblk <= 8) return launch_mfma_quant<8, 1>(L, x, xq, x_scale, x_rowsum, K, stream);
+    if (nblk <= 8) return launch_mfma_quant<4, 2>(L, x, xq, x_scale, x_rowsum, K, stream);
+    if (nblk <= 12) return launch_mfma_quant<4, 3>(L, x, xq, x_scale, x_rowsum, K, stream);
     if (nblk <= 16) return launch_mfma_quant<8, 2>(L, x, xq, x_scale, x_rowsum, K, stream);
     if (nblk <= 32) return launch_mfma_quant<16, 2>(L, x, xq, x_scale, x_rowsum, K, stream);
     return launch_mfma_quant<16, 3>(L, x, xq, x_scale, x_rowsum, K, stream);

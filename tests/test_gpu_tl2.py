@@ -124,7 +124,8 @@ def test_tl2_stream_one_token(N, K):
 # kernel with the row converted in each work group): every wave configuration, 1 to 8 float4 of the row per
 # thread (K = 16512: five, rounded up to eight), with and without a TL1 tail.
 @pytest.mark.parametrize("K,Ns", [(3200, [3200, 3200, 3200]), (4096, [4096, 1024, 1024]), (8640, [3200, 16]),
-                                  (14336, [4096]), (1536, [64, 48]), (16512, [32]), (448, [2400])])
+                                  (14336, [4096]), (1536, [64, 48]), (16512, [32]), (448, [2400]),
+                                  (2304, [48]), (4480, [64, 32])])
 def test_tl2_one_token_fused(K, Ns):
     _announce("tl2 one token fused", K, Ns)
     from tests.test_gpu_fused import _fused_case
