@@ -580,10 +580,9 @@ hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t
     return launch_stream<WAVES, U, 16>(L, x, K, xq, s, rs, stream);
 }
 
-template <int U, int MG>
+template <int W, int U, int MG>
 hipError_t launch_mstream(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                           int M, int K, hipStream_t stream) {
-    constexpr int W = 16;
     const void* kern = reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true>);
     const size_t lds = (size_t)M * (K + 16);
     int occ = 0;
@@ -596,13 +595,13 @@ hipError_t launch_mstream(const FusedLinears& L, const int8_t* xq, const float* 
     return hipGetLastError();
 }
 
-template <int U>
+template <int W, int U>
 hipError_t launch_mstream_m(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                             int M, int K, hipStream_t stream) {
-    if (M <= 4) return launch_mstream<U, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-    if (M <= 8) return launch_mstream<U, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-    if (M <= 12) return launch_mstream<U, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
-    return launch_mstream<U, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 4) return launch_mstream<W, U, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 8) return launch_mstream<W, U, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 12) return launch_mstream<W, U, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
+    return launch_mstream<W, U, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
 }
 
 }  // namespace
@@ -640,14 +639,22 @@ hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const floa
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int cus = device_cus();
     const bool fits = (int64_t)M * (K + 16) <= kDecodeStageBytes;   // the tokens' codes fit in LDS
-    (void)cus;
+    if (x_rowsum && fits && nkb <= 16 && L.total > cus / 2) {
+        // 4-wave work groups (K <= 4096) where the launch has more row groups than half the CUs: each group stages
+        // the codes once as the 16-wave groups do, without waiting on the slowest of 16 waves at each barrier
+        const int u4 = (nkb + 3) / 4;
+        if (u4 <= 1) return launch_mstream_m<4, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u4 <= 2) return launch_mstream_m<4, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u4 <= 3) return launch_mstream_m<4, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
+        return launch_mstream_m<4, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+    }
     if (x_rowsum && fits && nkb <= 64) {
         // 16-wave work groups, all of a row group's blocks in one batch; past what fits on the chip they stream
         const int u16 = (nkb + 15) / 16;
-        if (u16 <= 1) return launch_mstream_m<1>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u16 <= 2) return launch_mstream_m<2>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u16 <= 3) return launch_mstream_m<3>(L, xq, x_scale, x_rowsum, M, K, stream);
-        return launch_mstream_m<4>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 1) return launch_mstream_m<16, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 2) return launch_mstream_m<16, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 3) return launch_mstream_m<16, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
+        return launch_mstream_m<16, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
     }
     int waves, u;
     decode_shape(L.total, K, 4, 4, waves, u);
