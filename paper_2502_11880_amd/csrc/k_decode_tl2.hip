@@ -744,13 +744,16 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
     else run(std::true_type{});
 }
 
-// The weights of one transcoding launch: item runs start at start[i] (LLONG_MAX past the last weight).
+// The weights of one transcoding launch.  Pair items (two TL2 blocks of one row group) of weight i are numbered
+// from pstart[i], its work groups of single items from rstart[i] (LLONG_MAX past the last weight).
 struct TranscodeLinears {
     const uint8_t* packed[kMaxFused];
     uint32_t* out[kMaxFused];
     int N[kMaxFused];
-    long long start[kMaxFused];
-    long long total;
+    long long pstart[kMaxFused];
+    long long rstart[kMaxFused];
+    long long pairs;                  // pair items of the launch
+    int pair_groups;                  // persistent work groups that walk them
 };
 
 // TL2 -> I2_S transcoding, for the prefill GEMM (M > 16): the I2_S MFMA GEMM then runs on the same ternary
@@ -775,58 +778,145 @@ __device__ __forceinline__ size_t i2s_word_index(int n, int k0, int K) {
     return (size_t)R * K + (size_t)kI2sBlockK * sb + (size_t)(16 * q + r) * T + j;
 }
 
-// One launch rewrites every weight of a fused group: item c belongs to the weight whose run of items holds it (a
-// compare chain over the fixed maximum; runs are whole waves).  A thread's packed words are loaded before the
-// table image is copied into LDS, so the two loads overlap instead of following each other.
-__global__ __launch_bounds__(256) void tl2_to_i2s_kernel(TranscodeLinears T, int K) {
+// Work groups of 192 threads.  The first T.pair_groups groups walk the pair items p = blockIdx.x, + gridDim, ...: a
+// pair is two TL2 blocks of one row group, 768 k, exactly three full I2_S blocks (one contiguous 3 KiB run of the
+// I2_S array).  Two waves expand its 128 lane chunks into LDS at the words' places in that run, then the three
+// waves store the run with one 16-byte store per thread, while the next pair's packed words are already in
+// flight.  The other groups take one item per thread: the lane chunks of an odd last TL2 block and the tail
+// words, written word by word.  The packed words are loaded before the table image is copied into LDS.
+constexpr int kTcThreads = 192;
+
+__device__ __forceinline__ void tc_counts(int N, int K, long long& pairs, long long& odd_items,
+                                          long long& rest_items) {
+    const int three = (K / kTl2BlockK) * kTl2BlockK;
+    const int nblk = three / kTl2BlockK, units = (K - three) / kSubK;
+    const long long rgs = N / kRowsPerGroup;
+    pairs = rgs * (nblk / 2);
+    odd_items = rgs * 64 * (nblk & 1);
+    rest_items = odd_items + rgs * 64 * units;
+}
+
+__global__ __launch_bounds__(kTcThreads) void tl2_to_i2s_kernel(TranscodeLinears T, int K) {
     __shared__ __align__(16) uint8_t tab[kTl2MfmaTables];
+    __shared__ __align__(16) uint32_t run[3 * kI2sBlockK];     // one pair's three I2_S blocks, as in HBM
+    const int tid = threadIdx.x;
     const int three = (K / kTl2BlockK) * kTl2BlockK;
     const int nblk = three / kTl2BlockK;
     const int units = (K - three) / kSubK;
-    const long long c_all = (long long)blockIdx.x * 256 + threadIdx.x;
+    const int l = tid & 63, q = l >> 4, r = l & 15;
+    auto planes = [&](int li, const uint8_t*& idx_plane, const uint8_t*& sign_plane, const uint8_t*& tail_plane) {
+        const size_t N = (size_t)T.N[li];
+        idx_plane = T.packed[li];
+        sign_plane = idx_plane + N * (three / 6);
+        tail_plane = sign_plane + N * (three / 24);
+    };
+    auto copy_tables = [&]() {
+        for (int i = tid; i < kTableChunks; i += kTcThreads)
+            reinterpret_cast<v4u*>(tab)[i] = reinterpret_cast<const v4u*>(kExpandTables.w)[i];
+    };
+
+    if ((int)blockIdx.x < T.pair_groups) {
+        const int pairs_rg = nblk / 2;
+        // pair p: weight li, row group R, pair pp within the row group
+        auto locate_pair = [&](long long p, int& li, int& R, int& pp) {
+            li = 0;
+#pragma unroll
+            for (int i = 1; i < kMaxFused; ++i) li = p >= T.pstart[i] ? i : li;
+            const long long b = p - T.pstart[li];
+            R = (int)(b / pairs_rg);
+            pp = (int)(b - (long long)R * pairs_rg);
+        };
+        // this lane's packed words of pair p (waves 0 and 1: blocks 2 pp and 2 pp + 1; wave 2 loads nothing)
+        auto load_pair = [&](long long p, v4u& iw, uint32_t& sw) {
+            int li, R, pp;
+            locate_pair(p, li, R, pp);
+            const uint8_t *ip, *sp, *tp;
+            planes(li, ip, sp, tp);
+            const size_t tile = (size_t)R * nblk + 2 * pp + (tid >> 6);
+            iw = *reinterpret_cast<const v4u*>(ip + tile * 1024 + 16 * l);
+            sw = *reinterpret_cast<const uint32_t*>(sp + tile * 256 + 4 * l);
+        };
+        long long p = blockIdx.x;
+        const long long G = T.pair_groups;
+        v4u iw = {0u, 0u, 0u, 0u};
+        uint32_t sw = 0u;
+        if (tid < 128 && p < T.pairs) load_pair(p, iw, sw);
+        copy_tables();
+        __syncthreads();
+        for (; p < T.pairs; p += G) {
+            v4u iw_n = {0u, 0u, 0u, 0u};
+            uint32_t sw_n = 0u;
+            if (tid < 128 && p + G < T.pairs) load_pair(p + G, iw_n, sw_n);
+            int li, R, pp;
+            locate_pair(p, li, R, pp);
+            if (tid < 128) {
+                uint32_t wd[24];
+                expand_triples(iw, sw, reinterpret_cast<const uint2*>(tab), wd);
+                // word (block s, lane chunk 16 qq + r, sub-tile j) of the run, relative to its first k (768 pp)
+                const int base = (tid >> 6) * kTl2BlockK + 96 * q;
+#pragma unroll
+                for (int g = 0; g < 6; ++g) {
+                    const int kk = base + 16 * g;
+                    const int s_l = kk / kI2sBlockK, rem = kk % kI2sBlockK;
+                    run[kI2sBlockK * s_l + (16 * ((rem % kSubK) / 16) + r) * 4 + rem / kSubK] = i2s_word_of(wd + 4 * g);
+                }
+            }
+            __syncthreads();
+            const size_t first = (size_t)R * K + (size_t)pp * 2 * kTl2BlockK;   // words: 768 pp of row group R
+            reinterpret_cast<v4u*>(T.out[li] + first)[tid] = reinterpret_cast<const v4u*>(run)[tid];
+            __syncthreads();                                   // the run is rewritten by the next pair
+            iw = iw_n;
+            sw = sw_n;
+        }
+        return;
+    }
+
+    // single items: group rb of weight li
+    const long long rb_all = (long long)blockIdx.x - T.pair_groups;
     int li = 0;
 #pragma unroll
-    for (int i = 1; i < kMaxFused; ++i) li = c_all >= T.start[i] ? i : li;
-    const int N = T.N[li];
-    const uint8_t* packed = T.packed[li];
+    for (int i = 1; i < kMaxFused; ++i) li = rb_all >= T.rstart[i] ? i : li;
+    long long pairs, odd_items, rest_items;
+    tc_counts(T.N[li], K, pairs, odd_items, rest_items);
+    const uint8_t *idx_plane, *sign_plane, *tail_plane;
+    planes(li, idx_plane, sign_plane, tail_plane);
     uint32_t* __restrict__ out = T.out[li];
-    const uint8_t* idx_plane = packed;
-    const uint8_t* sign_plane = packed + (size_t)N * (three / 6);
-    const uint8_t* tail_plane = sign_plane + (size_t)N * (three / 24);
-    const size_t main_items = (size_t)(N / kRowsPerGroup) * nblk * 64;     // lane chunks of the TL2 blocks
-    const size_t tail_items = (size_t)(N / kRowsPerGroup) * 64 * units;    // tail words
-    const size_t c = (size_t)(c_all - T.start[li]);
-    const bool is_main = c_all < T.total && c < main_items;
-    const bool is_tail = c_all < T.total && !is_main && c < main_items + tail_items;
+    const long long c = (rb_all - T.rstart[li]) * kTcThreads + tid;
+    int R = 0, lc = 0, u = 0;
+    bool expand = false, tail = false;
+    if (c < odd_items) {
+        R = (int)(c >> 6);
+        lc = (int)(c & 63);
+        expand = true;
+    } else if (c < rest_items) {
+        const long long t = c - odd_items;                     // (row group, lane, unit), as the tail plane
+        u = (int)(t % units);
+        lc = (int)((t / units) & 63);
+        R = (int)(t / ((long long)64 * units));
+        tail = true;
+    }
     v4u iw = {0u, 0u, 0u, 0u};
     uint32_t sw = 0u, tw = 0u;
-    if (is_main) {
-        iw = *reinterpret_cast<const v4u*>(idx_plane + (c >> 6) * 1024 + 16 * (c & 63));
-        sw = *reinterpret_cast<const uint32_t*>(sign_plane + (c >> 6) * 256 + 4 * (c & 63));
-    } else if (is_tail) {
-        tw = *reinterpret_cast<const uint32_t*>(tail_plane + (c - main_items) * 4);
+    if (expand) {
+        const size_t tile = (size_t)R * nblk + nblk - 1;
+        iw = *reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * lc);
+        sw = *reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * lc);
+    } else if (tail) {
+        tw = *reinterpret_cast<const uint32_t*>(tail_plane + ((size_t)R * 64 * units + (size_t)lc * units + u) * 4);
     }
-    for (int i = threadIdx.x; i < kTableChunks; i += 256)
-        reinterpret_cast<v4u*>(tab)[i] = reinterpret_cast<const v4u*>(kExpandTables.w)[i];
+    copy_tables();
     __syncthreads();
-    if (is_main) {
-        const size_t tile = c >> 6;                       // (row group, block)
-        const int l = (int)(c & 63), q = l >> 4, r = l & 15;
-        const int R = (int)(tile / nblk), blk = (int)(tile - (size_t)R * nblk);
+    const int qc = lc >> 4, n = R * kRowsPerGroup + (lc & 15);
+    if (expand) {
         uint32_t wd[24];
         expand_triples(iw, sw, reinterpret_cast<const uint2*>(tab), wd);
-        const int n = R * kRowsPerGroup + r;
-        const int base = blk * kTl2BlockK + 96 * q;
+        const int base = (nblk - 1) * kTl2BlockK + 96 * qc;
 #pragma unroll
         for (int g = 0; g < 6; ++g) out[i2s_word_index(n, base + 16 * g, K)] = i2s_word_of(wd + 4 * g);
-    } else if (is_tail) {
-        const size_t t = c - main_items;                  // (row group, lane, unit), as the tail plane
-        const int u = (int)(t % units);
-        const int l = (int)((t / units) & 63), q = l >> 4, r = l & 15;
-        const int R = (int)(t / ((size_t)64 * units));
+    } else if (tail) {
         const uint32_t* ptab = reinterpret_cast<const uint32_t*>(tab + kIdxTableBytes);
         const uint32_t d[4] = {ptab[tw & 0xFFu], ptab[(tw >> 8) & 0xFFu], ptab[(tw >> 16) & 0xFFu], ptab[tw >> 24]};
-        out[i2s_word_index(R * kRowsPerGroup + r, three + kSubK * u + 16 * q, K)] = i2s_word_of(d);
+        out[i2s_word_index(n, three + kSubK * u + 16 * qc, K)] = i2s_word_of(d);
     }
 }
 
@@ -1046,26 +1136,33 @@ hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const
     return hipSuccess;
 }
 
-size_t tl2_to_i2s_items(int N, int K) {
-    const int three = (K / kTl2BlockK) * kTl2BlockK;
-    return (size_t)(N / kRowsPerGroup) * 64 * ((three / kTl2BlockK) + (K - three) / kSubK);
-}
-
 hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* const* i2s_out, int count, int K,
                              hipStream_t stream) {
     if (count < 1 || count > kMaxFused) return hipErrorInvalidValue;
+    const int three = (K / kTl2BlockK) * kTl2BlockK;
+    const int nblk = three / kTl2BlockK, units = (K - three) / kSubK;
     TranscodeLinears T{};
-    long long items = 0;
+    long long pairs = 0, rest_groups = 0;
     for (int i = 0; i < kMaxFused; ++i) {
         const int j = i < count ? i : 0;
         T.packed[i] = static_cast<const uint8_t*>(packed[j]);
         T.out[i] = static_cast<uint32_t*>(i2s_out[j]);
         T.N[i] = N[j];
-        T.start[i] = i < count ? items : 0x7fffffffffffffffLL;
-        if (i < count) items += (long long)tl2_to_i2s_items(N[i], K);
+        T.pstart[i] = i < count ? pairs : 0x7fffffffffffffffLL;
+        T.rstart[i] = i < count ? rest_groups : 0x7fffffffffffffffLL;
+        if (i < count) {
+            const long long rgs = N[i] / kRowsPerGroup;
+            pairs += rgs * (nblk / 2);
+            rest_groups += (rgs * 64 * ((nblk & 1) + units) + kTcThreads - 1) / kTcThreads;
+        }
     }
-    T.total = items;
-    hipLaunchKernelGGL(tl2_to_i2s_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, stream, T, K);
+    T.pairs = pairs;
+    // persistent pair groups: as many as fit at once (eight per CU), no more than there are pairs
+    const long long cap = (long long)device_cus() * 8;
+    T.pair_groups = (int)(pairs < cap ? pairs : cap);
+    const long long groups = T.pair_groups + rest_groups;
+    if (groups < 1) return hipSuccess;
+    hipLaunchKernelGGL(tl2_to_i2s_kernel, dim3((unsigned)groups), dim3(kTcThreads), 0, stream, T, K);
     return hipGetLastError();
 }
 
