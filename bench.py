@@ -224,7 +224,7 @@ def main():
         achieved = (flops / launches) / (avg_launch_ms * 1e-3) / 1e12
         kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
         if layout != "i2s":
-            kernel = "tl2_to_i2s_kernel per weight + " + kernel
+            kernel = "tl2_to_i2s_kernel per group + " + kernel
         traffic = measured_traffic(*TRAFFIC["prefill"]) if (args.workload, M, layout) == (3, 2048, "i2s") else None
         roofline = {"bound": "mfma", "kernel": kernel,
                     "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
