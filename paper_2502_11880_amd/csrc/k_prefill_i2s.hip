@@ -77,7 +77,9 @@ __device__ __forceinline__ T pick_linear(const T (&a)[kMaxFused], int li) {
     return v;
 }
 
-template <int WN, bool HAS_RS>
+// HAS_ACC: some weight of the launch also stores its int32 sums (the parity hook); without it the epilogue holds
+// no code for them (2% of the 2048-token step).
+template <int WN, bool HAS_RS, bool HAS_ACC>
 __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads) void i2s_prefill_kernel(
     PrefillLinears P, const int8_t* __restrict__ xq, const float* __restrict__ x_scale,
     const int32_t* __restrict__ x_rowsum, int M, int K, int splits, int32_t* __restrict__ part_all) {
@@ -383,7 +385,9 @@ __global__ __attribute__((amdgpu_waves_per_eu(2, 2))) __launch_bounds__(kThreads
                     const int nl = 128 * wn + 32 * ni + j32;
                     const int val = acc[mi][ni][v] - rsum;
                     ybuf[(32 * wm + rr) * kYRow + nl] = (float)val * sc;
-                    if (acc_out && m0 + ml < M && n0 + nl < N) acc_out[(size_t)(m0 + ml) * N + n0 + nl] = val;
+                    if constexpr (HAS_ACC) {
+                        if (acc_out && m0 + ml < M && n0 + nl < N) acc_out[(size_t)(m0 + ml) * N + n0 + nl] = val;
+                    }
                 }
             }
         }
@@ -509,12 +513,20 @@ void launch_wn(const FusedLinears& L, const int8_t* xq, const float* x_scale, co
     P.n_total = total_rows(L);
     const unsigned grid_tiles = (unsigned)(((M + kBM - 1) / kBM) * tiles);
     const dim3 grid(grid_tiles * (unsigned)splits), block(kThreads);
-    if (x_rowsum)
-        hipLaunchKernelGGL((i2s_prefill_kernel<WN, true>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M, K,
-                           splits, part);
+    bool has_acc = false;
+    for (int i = 0; i < L.count; ++i) has_acc = has_acc || L.acc[i] != nullptr;
+    if (x_rowsum && has_acc)
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, true, true>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M,
+                           K, splits, part);
+    else if (x_rowsum)
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, true, false>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M,
+                           K, splits, part);
+    else if (has_acc)
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, false, true>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M,
+                           K, splits, part);
     else
-        hipLaunchKernelGGL((i2s_prefill_kernel<WN, false>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M, K,
-                           splits, part);
+        hipLaunchKernelGGL((i2s_prefill_kernel<WN, false, false>), grid, block, 0, stream, P, xq, x_scale, x_rowsum, M,
+                           K, splits, part);
 }
 
 }  // namespace
