@@ -155,7 +155,9 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
 // the 16 token rows of one MFMA operand fall in different banks); they are the MFMA A operands (row = token;
 // rows past M repeat token 0 and are not stored) of every row group it multiplies, and no other wave reads
 // them.  The work group then walks row groups as the single-token kernel does, two batches of weights in flight.
-template <int WAVES, int U, int MG, bool HAS_RS>
+// HAS_ACC: some weight of the launch also stores its int32 sums (the parity hook); the other instance holds no
+// code for them (2% of the eight-token step).
+template <int WAVES, int U, int MG, bool HAS_RS, bool HAS_ACC>
 __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLinears L, const int8_t* __restrict__ xq,
                                                                        const float* __restrict__ x_scale,
                                                                        const int32_t* __restrict__ x_rowsum, int M,
@@ -299,7 +301,9 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
                 if (m < M) {
                     const int val = tot[v] - rs_m[v];
                     y[(size_t)m * N + n] = (float)val * (bw / xs_m[v]);
-                    if (acc_out) acc_out[(size_t)m * N + n] = val;
+                    if constexpr (HAS_ACC) {
+                        if (acc_out) acc_out[(size_t)m * N + n] = val;
+                    }
                 }
             }
         }
@@ -583,15 +587,22 @@ hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t
 template <int W, int U, int MG>
 hipError_t launch_mstream(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                           int M, int K, hipStream_t stream) {
-    const void* kern = reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true>);
+    bool has_acc = false;
+    for (int i = 0; i < L.count; ++i) has_acc = has_acc || L.acc[i] != nullptr;
+    const void* kern = has_acc ? reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, true>)
+                               : reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, false>);
     const size_t lds = (size_t)M * (K + 16);
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * W, lds) != hipSuccess || occ <= 0) occ = 1;
     const int64_t max_g = (int64_t)device_cus() * occ;
     const int64_t rounds = (L.total + max_g - 1) / max_g;
     const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * W);
-    hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true>), grid, block, lds, stream, L, xq, x_scale, x_rowsum,
-                       M, K);
+    if (has_acc)
+        hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, true>), grid, block, lds, stream, L, xq, x_scale,
+                           x_rowsum, M, K);
+    else
+        hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, false>), grid, block, lds, stream, L, xq, x_scale,
+                           x_rowsum, M, K);
     return hipGetLastError();
 }
 
