@@ -107,7 +107,8 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *   x_rowsum                        as written by bitnet_quantize_act, or NULL (then computed here).
  *   y      device fp32 [M, N]: y[m, n] = fp32(acc[m, n]) * fp32(w_scale / x_scale[m]).
  *   acc    device int32 [M, N] or NULL: when given, also receives acc[m, n] = sum_k xq[m, k] * t[n, k]
- *          exactly (the same integers for every tiling and launch shape).
+ *          exactly (the same integers for every tiling and launch shape).  A parity output: with it the
+ *          prefill and multi-token kernels run an instance that also stores the sums, a few percent slower.
  *   ws     device workspace of at least bitnet_mpgemm_workspace_bytes(layout, M, N, K) bytes, or NULL when
  *          that is 0 (else BITNET_E_WORKSPACE).  It holds the exact int32 partial sums of a prefill GEMM split
  *          along K (M > 16, small grids; only when x_rowsum is given) and, for TL2 with M > 16, the weights
