@@ -1,6 +1,7 @@
 """Build the HIP library in-tree: ``python -m paper_2502_11880_amd.build``.
 
-Compiles every ``csrc/*.hip`` source for gfx950 into ``paper_2502_11880_amd/libbitnet_mi355x.so``.
+Compiles every ``csrc/*.hip`` source for gfx950 into its own object (in parallel), then links them into
+``paper_2502_11880_amd/libbitnet_mi355x.so``.
 """
 from __future__ import annotations
 
@@ -9,6 +10,8 @@ import os
 import shutil
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -20,7 +23,6 @@ HIPCC_FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     # IEEE fp32 semantics for the quantisers and the epilogue: no contraction, correctly rounded divide,
     # denormals kept.
     "-ffp-contract=off",
@@ -43,16 +45,29 @@ def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(PKG, "csrc", "*.hip")))
 
 
-def build(verbose: bool = False, out: str = LIB_PATH, defines: tuple = ()) -> str:
-    tmp = out + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *[f"-D{d}" for d in defines], "-I", os.path.join(ROOT, "include"),
-           "-I", os.path.join(PKG, "csrc"), *sources(), "-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
+        raise RuntimeError(f"hipcc failed with exit code {res.returncode}: {' '.join(cmd[-3:])}")
+
+
+def build(verbose: bool = False, out: str = LIB_PATH, defines: tuple = (), jobs: int | None = None) -> str:
+    cc = hipcc()
+    incs = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc")]
+    defs = [f"-D{d}" for d in defines]
+    srcs = sources()
+    jobs = jobs or min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
+    with tempfile.TemporaryDirectory(prefix="bitnet_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, os.path.basename(s) + ".o") for s in srcs]
+        cmds = [[cc, *HIPCC_FLAGS, *defs, *incs, "-c", s, "-o", o] for s, o in zip(srcs, objs)]
+        with ThreadPoolExecutor(max_workers=jobs) as ex:
+            for f in [ex.submit(_run, c, verbose) for c in cmds]:
+                f.result()
+        tmp = out + ".tmp"
+        _run([cc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, out)
     return out
 
