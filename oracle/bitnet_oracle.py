@@ -354,13 +354,24 @@ def unpack_tl2(packed: np.ndarray, N: int, K: int) -> np.ndarray:
 # ----------------------------------------------------------------------------------------------
 # a5/a6: MAD accumulation (Eq. 1, Algorithm "MAD-based mpGEMM")
 # ----------------------------------------------------------------------------------------------
+F64_EXACT = 1 << 53       # every integer of magnitude up to 2^53 is a float64
+
+
 def mad_gemm(xq: np.ndarray, t: np.ndarray) -> np.ndarray:
-    """acc[m, n] = sum_k xq[m, k] * t[n, k] in exact integer arithmetic (int64, checked to fit int32)."""
-    a = np.asarray(xq, dtype=np.int64)
-    w = np.asarray(t, dtype=np.int64)
-    if a.shape[1] != w.shape[1]:
+    """acc[m, n] = sum_k xq[m, k] * t[n, k] in exact integer arithmetic (checked to fit int32).
+
+    Every term is an integer of magnitude at most 128, so every partial sum of a row is an integer of
+    magnitude at most 128 K.  While 128 K < 2^53 each of them is a float64, so a float64 matrix product gives
+    the exact sum whatever order it adds in; beyond that bound the product is taken in int64.
+    """
+    a = np.asarray(xq)
+    w = np.asarray(t)
+    if a.ndim != 2 or w.ndim != 2 or a.shape[1] != w.shape[1]:
         raise ValueError("K mismatch")
-    acc = a @ w.T
+    if 128 * max(1, a.shape[1]) < F64_EXACT:
+        acc = np.rint(a.astype(np.float64) @ w.astype(np.float64).T).astype(np.int64)
+    else:
+        acc = a.astype(np.int64) @ w.astype(np.int64).T
     if acc.size and (acc.max() > np.iinfo(np.int32).max or acc.min() < np.iinfo(np.int32).min):
         raise OverflowError("accumulator exceeds int32")
     return acc.astype(np.int32)

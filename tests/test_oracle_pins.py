@@ -117,6 +117,22 @@ def test_mad_brute_force_all_ternary_rows(K):
             assert int(acc[m, n]) == ref
 
 
+def test_mad_largest_k_against_python_integers():
+    # the longest rows the library accepts, with the extreme codes -128 and 127: exact sums of Python integers
+    rng = np.random.default_rng(11)
+    K = 132096
+    xq = rng.choice(np.array([-128, 127, -1, 0, 1], dtype=np.int8), size=(2, K))
+    t = np.stack([np.ones(K, np.int8), -np.ones(K, np.int8), rng.integers(-1, 2, size=K).astype(np.int8),
+                  np.sign(xq[0]).astype(np.int8)])
+    acc = O.mad_gemm(xq, t)
+    for m in range(2):
+        a = [int(v) for v in xq[m]]
+        for n in range(t.shape[0]):
+            w = [int(v) for v in t[n]]
+            assert int(acc[m, n]) == sum(p * q for p, q in zip(a, w))
+    assert int(acc[0, 3]) == sum(abs(int(v)) for v in xq[0])
+
+
 def test_mad_closed_forms():
     rng = np.random.default_rng(7)
     M, N, K = 4, 32, 320
