@@ -62,6 +62,16 @@ __device__ __forceinline__ int wave_sum_all(int v) {
            __builtin_amdgcn_readlane(v, 48);
 }
 
+// Lanes of one wave hand data to other lanes of the same wave through LDS: the writes are ordered before the
+// reads by a release/acquire pair at work-group scope restricted to LDS (it waits for the wave's LDS operations
+// only, never for its global loads in flight) around a wave barrier, which also keeps the compiler from moving
+// the reads above the writes.  No other wave reads the data, so no work-group barrier is needed.
+__device__ __forceinline__ void wave_lds_handoff() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // int8 codes of four activations, packed little-endian: clamp(rint(fp32(x * s)), -128, 127) (Sec. 2.1).
 // rint gives an integer-valued float; + 128 is exact; v_cvt_pk_u8_f32 then converts it exactly (saturating
 // to [0, 255], which is the clamp) into its byte, and XOR 0x80 turns the offset byte into two's complement.

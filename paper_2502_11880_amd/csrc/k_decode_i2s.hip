@@ -245,6 +245,8 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
                 if (c16 == 0 && 4 * mg + (lane >> 4) < 16) tsum[wave][4 * mg + (lane >> 4)] = t;
             }
         }
+        // the codes a lane wrote are MFMA operands of other lanes of this wave (tsum is read after a barrier)
+        wave_lds_handoff();
     };
 
     const v4i zero = {0, 0, 0, 0};
@@ -445,8 +447,10 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
             }
         }
         // Codes 4e .. 4e+3 (e = tid + 64 WAVES i) lie in block e / 64, and e / 64 = wave (mod WAVES): every
-        // wave quantised exactly the blocks it multiplies, so no barrier is needed before the stream.  The
-        // waves' code sums meet in the first epilogue, which follows a barrier.
+        // wave quantised exactly the blocks it multiplies, so only the lanes of one wave exchange codes (an
+        // LDS hand-off inside the wave, no work-group barrier).  The waves' code sums meet in the first
+        // epilogue, which follows a barrier.
+        wave_lds_handoff();
         sum = wave_sum_all(sum);
         if (lane == 0) redi[wave] = sum;
         if (bid == 0 && tid == 0) s_out[0] = sx;
