@@ -13,11 +13,14 @@ once before timing (offline preprocessing); packed copies rotate so every step s
 rather than from the 256 MB Infinity Cache.
 
 The K timed steps are captured once in a HIP graph and replayed, so the GPU runs them back to back.
-Prints one JSON line.  Decode: `value` = packed weight bytes per step / step time (GB/s), `roofline` bound
-"hbm".  Prefill: `value` = int8 TOP/s of the step (2*M*N*K per linear), `roofline` bound "mfma".
+The default workload is the largest single-GPU one: the 56-layer 100B-class stack (hidden 12288, FFN 33024) at one
+token, I2_S.  Prints one JSON line.  Decode: `value` = packed weight bytes per step / step time (GB/s), `roofline`
+bound "hbm".  Prefill: `value` = int8 TOP/s of the step (2*M*N*K per linear), `roofline` bound "mfma".
 `gweights_per_s` counts ternary weights per second (I2_S and TL2 on one scale); `ms_per_step_spread` gives the
 10th/50th/90th percentile of the per-step time over ten replays of the same graph (the first is the timed one).
-`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload, with every host thread and with one.
+`parity` checks the timed launches themselves (the first activation group's fused call, in the first, middle and
+last layer) on every output against the oracle.
 """
 from __future__ import annotations
 
@@ -41,13 +44,18 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--workload", type=int, default=1)
+    p.add_argument("--workload", type=int, default=4)
     p.add_argument("--tokens", type=int, default=None)
     p.add_argument("--layout", default="i2s", choices=["i2s", "tl2"])
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-parity", action="store_true")
     return p.parse_args()
+
+
+def log(msg):
+    """A progress line on stderr (the JSON result is the only line on stdout)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
 def activation_groups(by_name, inputs):
@@ -84,6 +92,7 @@ def main():
         args.warmup = max(1, min(args.warmup, 3))
 
     # ---- offline: generate, ternarise and pack every weight on the GPU ----
+    log(f"workload {args.workload} ({spec['name']}), {M} token(s), {layout}: packing {len(linears)} weights")
     packed, scales = {}, {}
     for i, (name, K, N) in enumerate(linears):
         W = inputs.weight_f32(N, K, seed=inputs.seed_for(args.workload, i)).to(dev)
@@ -101,6 +110,7 @@ def main():
     rot = [[packed if (c, l) == (0, 0) else {k: v.clone() for k, v in packed.items()} for l in range(n_layers)]
            for c in range(copies)]
 
+    log(f"{copies} rotating copies of {n_layers} layer(s), {step_weight_bytes / 1e9:.2f} GB of packed weights per step")
     groups = activation_groups(by_name, inputs)
     xs, xqs, sxs, rss = [], [], [], []
     for gi, g in enumerate(groups):
@@ -146,6 +156,7 @@ def main():
         return g
 
     main_path = "fused"
+    log(f"warm-up ({args.warmup} steps), then {args.steps} steps captured in a graph")
     with torch.cuda.stream(stream):
         for i in range(args.warmup):
             step(i, main_path)
@@ -164,6 +175,7 @@ def main():
     torch.cuda.synchronize()
 
     # ---- timed region ----
+    log("timed replay")
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     w0 = time.perf_counter()
     with torch.cuda.stream(stream):
@@ -209,8 +221,7 @@ def main():
             kernel = "i2s_gemv1_stream_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
         else:
             kernel = "bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_stream_kernel per group"
-        default_workload = (args.workload, M, layout) == (1, 1, "i2s")
-        traffic = measured_traffic(*TRAFFIC["decode"]) if default_workload else None
+        traffic = measured_traffic(*TRAFFIC[key]) if (key := (args.workload, M, layout)) in TRAFFIC else None
         roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                     "traffic_unit": "bytes per launch (FETCH_SIZE x copy factor + WRITE_SIZE)" if traffic else None,
@@ -225,7 +236,7 @@ def main():
         kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
         if layout != "i2s":
             kernel = "tl2_to_i2s_kernel per group + " + kernel
-        traffic = measured_traffic(*TRAFFIC["prefill"]) if (args.workload, M, layout) == (3, 2048, "i2s") else None
+        traffic = measured_traffic(*TRAFFIC[key]) if (key := (args.workload, M, layout)) in TRAFFIC else None
         roofline = {"bound": "mfma", "kernel": kernel,
                     "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": traffic,
@@ -235,10 +246,12 @@ def main():
     tokens_per_s = M / (ms_per_step * 1e-3)
 
     parity = None
+    log(f"{ms_per_step:.5f} ms per step; parity of the timed launches against the oracle")
     if not args.no_parity:
-        parity = parity_spot_check(args, layout, M, linears, packed, scales, xs, dev)
+        parity = parity_check(args, layout, M, linears, groups, by_name, xs, ys, fargs, n_layers, ws, stream)
     cpu = None
     if not args.no_cpu_baseline:
+        log("CPU oracle timing")
         cpu = cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, decode)
 
     out = {
@@ -273,11 +286,14 @@ def main():
 
 SPREAD_REPLAYS = 10
 # committed counter summaries (HBM bytes per launch) and the kernel sources they were taken on
+# (workload, tokens, layout) -> (summary, kernel sources)
 TRAFFIC = {
-    "decode": ("profiles/decode_i2s_bitnet3b_m1_hbm_traffic.md",
-               ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")),
-    "prefill": ("profiles/prefill_i2s_llama8b_m2048_hbm_traffic.md",
-                ("paper_2502_11880_amd/csrc/k_prefill_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")),
+    (4, 1, "i2s"): ("profiles/decode_i2s_100b_m1_hbm_traffic.md",
+                    ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")),
+    (1, 1, "i2s"): ("profiles/decode_i2s_bitnet3b_m1_hbm_traffic.md",
+                    ("paper_2502_11880_amd/csrc/k_decode_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")),
+    (3, 2048, "i2s"): ("profiles/prefill_i2s_llama8b_m2048_hbm_traffic.md",
+                       ("paper_2502_11880_amd/csrc/k_prefill_i2s.hip", "paper_2502_11880_amd/csrc/bitnet_internal.hpp")),
 }
 
 
@@ -307,8 +323,9 @@ def measured_traffic(profile, sources):
     return int(fields["traffic_bytes_per_launch"])
 
 
-def parity_spot_check(args, layout, M, linears, packed, scales, xs, dev):
-    """Bit-exact check of the benchmark's own first linear against the oracle (sampled rows for prefill)."""
+def parity_check(args, layout, M, linears, groups, by_name, xs, ys, fargs, n_layers, ws, stream):
+    """Every output of the first activation group's fused call -- the launch the timed step makes, with the same
+    arguments -- against the oracle, in the first, middle and last layer (rotating copy 0)."""
     import numpy as np
     import torch
 
@@ -316,28 +333,46 @@ def parity_spot_check(args, layout, M, linears, packed, scales, xs, dev):
     from oracle import bitnet_oracle as O
     from paper_2502_11880_amd import inputs
 
-    name, K, N = linears[0]
-    W = inputs.weight_f32(N, K, seed=inputs.seed_for(args.workload, 0))
-    x = xs[0].cpu()
+    g = groups[0]
+    K = by_name[g[0]][0]
+    index = {name: i for i, (name, _, _) in enumerate(linears)}
+    xq_ref, s_ref = O.quantize_act(xs[0].cpu().numpy())
+    refs = {}
+    for n in g:
+        N = by_name[n][1]
+        t_ref, beta = O.ternarize(inputs.weight_f32(N, K, seed=inputs.seed_for(args.workload, index[n])).numpy())
+        acc_ref = O.mad_gemm(xq_ref, t_ref)
+        refs[n] = (acc_ref, O.epilogue(acc_ref, beta, s_ref))
+        del t_ref
+    dev = xs[0].device
     xq = torch.empty((M, K), dtype=torch.int8, device=dev)
     s = torch.empty(M, dtype=torch.float32, device=dev)
     rs = torch.empty(M, dtype=torch.int32, device=dev)
-    B.bitnet_quantize_act(xs[0], xq, s, rs)
-    y = torch.empty((M, N), dtype=torch.float32, device=dev)
-    acc = torch.empty((M, N), dtype=torch.int32, device=dev)
-    ws = torch.zeros(max(16, B.bitnet_mpgemm_workspace_bytes(layout, M, N, K)), dtype=torch.uint8, device=dev)
-    B.bitnet_mpgemm(layout, packed[name], scales[name], N, K, xq, s, y, acc, ws, x_rowsum=rs)
-    torch.cuda.synchronize()
-    rows = np.arange(M) if M <= 16 else np.unique(np.r_[0, M - 1, np.random.default_rng(0).choice(M, 6, False)])
-    xq_ref, s_ref = O.quantize_act(x.numpy())
-    t_ref, beta = O.ternarize(W.numpy())
-    acc_ref = O.mad_gemm(xq_ref[rows], t_ref)
-    y_ref = O.epilogue(acc_ref, beta, s_ref[rows])
-    exact = bool(np.array_equal(acc.cpu().numpy()[rows], acc_ref))
-    yg = y.cpu().numpy()[rows].astype(np.float64)
-    rel = float(np.max(np.abs(yg - y_ref) / np.maximum(np.abs(y_ref), 1e-30)))
-    return {"linear": f"{name}:{K}x{N}", "rows_checked": int(len(rows)), "acc_bit_exact": exact,
-            "y_max_rel_err": rel}
+    layers = sorted({0, n_layers // 2, n_layers - 1})
+    codes_ok, zeros_ok, worst, outputs = True, True, 0.0, 0
+    for l in layers:
+        for n in g:
+            ys[n].fill_(float("nan"))
+        with torch.cuda.stream(stream):
+            B.bitnet_mpgemm_fused(layout, None, None, xs[0], xq, s, rs, None, ws, stream.cuda_stream,
+                                  args=fargs[0][l][0])
+        torch.cuda.synchronize()
+        codes_ok = codes_ok and bool(np.array_equal(xq.cpu().numpy(), xq_ref)) and bool(
+            np.array_equal(s.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))) and bool(
+            np.array_equal(rs.cpu().numpy(), xq_ref.astype(np.int64).sum(1)))
+        for n in g:
+            acc_ref, y_ref = refs[n]
+            yg = ys[n].cpu().numpy().astype(np.float64)
+            err = np.abs(yg - y_ref) / np.maximum(np.abs(y_ref), 1e-30)
+            err[acc_ref == 0] = 0.0
+            worst = max(worst, float(np.nan_to_num(err, nan=np.inf).max()))
+            zeros_ok = zeros_ok and bool(np.all(yg[acc_ref == 0] == 0.0))
+            outputs += yg.size
+    return {"group": ",".join(g) + f":{K}x[" + ",".join(str(by_name[n][1]) for n in g) + "]",
+            "call": "bitnet_mpgemm_fused, the timed launch and arguments", "layers_checked": layers,
+            "rows_checked": M, "outputs_checked": outputs, "codes_bit_exact": codes_ok,
+            "y_max_rel_err": worst, "zeros_exact": zeros_ok,
+            "pass": bool(codes_ok and zeros_ok and worst <= 1e-5)}
 
 
 def cpu_model():
@@ -351,14 +386,23 @@ def cpu_model():
     return None
 
 
+def host_threads():
+    """Threads this process may run on (its CPU affinity), else the host's CPU count."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        return os.cpu_count() or 1
+
+
 def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, decode):
-    """Time the oracle (quantise + exact integer accumulation + epilogue) on the host for ~cpu_seconds."""
+    """Time the oracle (quantise + exact integer accumulation + epilogue) on the host for ~cpu_seconds, once with
+    every host thread and once with one (the oracle's matrix product is a BLAS call; the rest is numpy)."""
     import torch
+    from threadpoolctl import threadpool_limits
 
     from oracle import bitnet_oracle as O
     from paper_2502_11880_amd import inputs
 
-    torch.set_num_threads(1)
     n_layers = inputs.WORKLOADS[args.workload].get("layers", 1)
     # very large layers: the first CPU_ROWS output rows of each weight stand in for all of them
     row_cap = CPU_ROWS if n_layers > 1 else None
@@ -373,32 +417,46 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
     Mc = M if decode else min(M, 4)
     xs = [inputs.activation_f32(M, by_name[g[0]][0], seed=inputs.seed_for(args.workload, 100 + gi)).numpy()[:Mc]
           for gi, g in enumerate(groups)]
-    t0 = time.perf_counter()
-    steps = 0
-    while True:
-        for gi, g in enumerate(groups):
-            xq, s = O.quantize_act(xs[gi])
-            for n in g:
-                O.epilogue(O.mad_gemm(xq, ts[n]), betas[n], s)
-        steps += 1
-        el = time.perf_counter() - t0
-        if el >= args.cpu_seconds:
-            break
-    per_step = el / steps
-    host = {"cpu_model": cpu_model(), "host_threads": os.cpu_count()}
-    if decode and row_cap is not None:
-        rate = sample_bytes / per_step            # packed-equivalent weight bytes per second
-        return {"value": round(rate / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-                "sample": f"{steps} passes over the first {row_cap} output rows of each of the {len(linears)} "
-                          f"linears of one layer (M={M}) in {el:.1f} s; numpy int64 matmul, one thread",
-                "tokens_per_s": round(M * rate / step_weight_bytes, 6), **host}
-    if decode:
-        return {"value": round(step_weight_bytes / per_step / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-                "sample": f"{steps} full steps of the same workload (all {len(linears)} linears, M={M}) in {el:.1f} s; "
-                          "numpy int64 matmul, one thread", "tokens_per_s": round(M / per_step, 3), **host}
-    return {"value": round(flops * Mc / M / per_step / 1e12, 6), "unit": "TOP/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} steps of the same linears on {Mc} of the {M} token rows in {el:.1f} s; "
-                      "numpy int64 matmul, one thread", "tokens_per_s": round(Mc / per_step, 3), **host}
+
+    def timed(threads):
+        torch.set_num_threads(threads)
+        with threadpool_limits(limits=threads):
+            t0 = time.perf_counter()
+            steps = 0
+            while True:
+                for gi, g in enumerate(groups):
+                    xq, s = O.quantize_act(xs[gi])
+                    for n in g:
+                        O.epilogue(O.mad_gemm(xq, ts[n]), betas[n], s)
+                steps += 1
+                el = time.perf_counter() - t0
+                if el >= args.cpu_seconds / 2:
+                    return steps, el
+
+    legs = {}
+    for threads in (host_threads(), 1):
+        steps, el = timed(threads)
+        per_step = el / steps
+        if decode and row_cap is not None:
+            rate = sample_bytes / per_step            # packed-equivalent weight bytes per second
+            legs[threads] = {"value": round(rate / 1e9, 4), "unit": "GB/s", "cores": threads,
+                             "sample": f"{steps} passes over the first {row_cap} output rows of each of the "
+                                       f"{len(linears)} linears of one layer (M={M}) in {el:.1f} s",
+                             "tokens_per_s": round(M * rate / step_weight_bytes, 6)}
+        elif decode:
+            legs[threads] = {"value": round(step_weight_bytes / per_step / 1e9, 4), "unit": "GB/s", "cores": threads,
+                             "sample": f"{steps} full steps of the same workload (all {len(linears)} linears, M={M}) "
+                                       f"in {el:.1f} s", "tokens_per_s": round(M / per_step, 3)}
+        else:
+            legs[threads] = {"value": round(flops * Mc / M / per_step / 1e12, 6), "unit": "TOP/s", "cores": threads,
+                             "sample": f"{steps} steps of the same linears on {Mc} of the {M} token rows in {el:.1f} s",
+                             "tokens_per_s": round(Mc / per_step, 3)}
+    allc = legs[host_threads()]
+    one = legs[1]
+    how = "; numpy quantiser and epilogue, float64 BLAS matrix product (exact for these integers)"
+    return {**allc, "kind": "oracle", "sample": allc["sample"] + how, "cpu_model": cpu_model(),
+            "host_threads": host_threads(),
+            "single_thread": {k: one[k] for k in ("value", "unit", "cores", "sample", "tokens_per_s")}}
 
 
 if __name__ == "__main__":

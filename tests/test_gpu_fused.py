@@ -17,36 +17,45 @@ def _announce(*what):
 
 
 def _fused_case(layout, M, K, Ns, seed, split_ws=False, sample_rows=None):
+    """One fused call per layout in `layout` (a name or a tuple of names) on the same seeded weights and
+    activation, every output (or every output of a seeded sample of token rows) against the oracle, and
+    bit-identical to the separate quantise + bitnet_mpgemm calls and to the fused call on the quantised input."""
+    layouts = (layout,) if isinstance(layout, str) else tuple(layout)
     Ws = [inputs.weight_f32(N, K, seed=seed + i) for i, N in enumerate(Ns)]
     x = inputs.activation_f32(M, K, seed=seed + 100)
-    packs = [H.pack(W, layout) for W in Ws]
-    xd = x.to(H.DEV)
-    xq = torch.empty((M, K), dtype=torch.int8, device=H.DEV)
-    s = torch.empty(M, dtype=torch.float32, device=H.DEV)
-    rs = torch.empty(M, dtype=torch.int32, device=H.DEV)
-    ys = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
-    need = max(B.bitnet_mpgemm_workspace_bytes(layout, M, N, K) for N in Ns)
-    if split_ws:
-        need = max(need, B.bitnet_mpgemm_fused_workspace_bytes(layout, Ns, K, M))
-    ws = torch.zeros(max(16, need), dtype=torch.uint8, device=H.DEV)
-    B.bitnet_mpgemm_fused(layout, [p for p, _ in packs], [b for _, b in packs], xd, xq, s, rs, ys, ws)
     xq_ref, s_ref = O.quantize_act(x.numpy())
-    assert np.array_equal(H.to_np(xq), xq_ref)
-    assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
-    assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
+    refs = [O.ternarize(W.numpy()) for W in Ws]
     rows = np.arange(M) if sample_rows is None else np.unique(
         np.concatenate([[0, M - 1], np.random.default_rng(seed).choice(M, size=sample_rows, replace=False)]))
-    for i, (W, (p, b), y) in enumerate(zip(Ws, packs, ys)):
-        t_ref, beta_ref = O.ternarize(W.numpy())
-        acc_ref = O.mad_gemm(xq_ref[rows], t_ref)
-        H.check_y(H.to_np(y)[rows], O.epilogue(acc_ref, beta_ref, s_ref[rows]), acc_ref)
-        y_sep, _ = H.mpgemm(layout, p, b, Ns[i], K, xq, s, x_rowsum=rs)
-        assert np.array_equal(H.to_np(y), H.to_np(y_sep))      # identical to the separate calls
-    # the products alone, on the activation quantised above (x = NULL)
-    ys2 = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
-    B.bitnet_mpgemm_fused(layout, [p for p, _ in packs], [b for _, b in packs], None, xq, s, rs, ys2, ws)
-    for y, y2 in zip(ys, ys2):
-        assert np.array_equal(H.to_np(y), H.to_np(y2))
+    acc_refs = [O.mad_gemm(xq_ref[rows], t_ref) for t_ref, _ in refs]
+    xd = x.to(H.DEV)
+    for lay in layouts:
+        _announce("  layout", lay)
+        packs = [H.pack(W, lay) for W in Ws]
+        xq = torch.empty((M, K), dtype=torch.int8, device=H.DEV)
+        s = torch.empty(M, dtype=torch.float32, device=H.DEV)
+        rs = torch.empty(M, dtype=torch.int32, device=H.DEV)
+        ys = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
+        need = max(B.bitnet_mpgemm_workspace_bytes(lay, M, N, K) for N in Ns)
+        if split_ws:
+            need = max(need, B.bitnet_mpgemm_fused_workspace_bytes(lay, Ns, K, M))
+        ws = torch.zeros(max(16, need), dtype=torch.uint8, device=H.DEV)
+        B.bitnet_mpgemm_fused(lay, [p for p, _ in packs], [b for _, b in packs], xd, xq, s, rs, ys, ws)
+        assert np.array_equal(H.to_np(xq), xq_ref)
+        assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
+        assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
+        for i, ((p, b), y, (_, beta_ref), acc_ref) in enumerate(zip(packs, ys, refs, acc_refs)):
+            H.check_y(H.to_np(y)[rows], O.epilogue(acc_ref, beta_ref, s_ref[rows]), acc_ref)
+            y_sep, _ = H.mpgemm(lay, p, b, Ns[i], K, xq, s, x_rowsum=rs)
+            assert np.array_equal(H.to_np(y), H.to_np(y_sep))      # identical to the separate calls
+            del y_sep
+        # the products alone, on the activation quantised above (x = NULL)
+        ys2 = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
+        B.bitnet_mpgemm_fused(lay, [p for p, _ in packs], [b for _, b in packs], None, xq, s, rs, ys2, ws)
+        for y, y2 in zip(ys, ys2):
+            assert np.array_equal(H.to_np(y), H.to_np(y2))
+        del packs, ys, ys2, ws
+        torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("M,K,Ns", [(1, 64, [16]), (1, 320, [16, 48, 32]), (2, 832, [64, 16]),
@@ -86,15 +95,51 @@ def test_fused_i2s_prefill(M, K, Ns, split_ws):
     _fused_case("i2s", M, K, Ns, seed=inputs.seed_for(2, 900 + M + K + len(Ns)), split_ws=split_ws)
 
 
-# The 8B-class q/k/v and gate/up groups at 2048 tokens (sampled rows against the oracle; every output against the
-# separate calls).
+# The 8B-class q/k/v and gate/up groups at 2048 tokens: every output against the oracle (these groups take the
+# 128 x 512 tile, four 32 x 32 tiles per wave column) and against the separate calls.
 @pytest.mark.parametrize("Ns", [[4096, 1024, 1024], [14336, 14336]])
 def test_fused_i2s_prefill_workload(Ns):
     _announce("fused i2s prefill workload", 2048, 4096, Ns)
-    _fused_case("i2s", 2048, 4096, Ns, seed=inputs.seed_for(3, 50 + len(Ns)), split_ws=True, sample_rows=6)
+    _fused_case("i2s", 2048, 4096, Ns, seed=inputs.seed_for(3, 50 + len(Ns)), split_ws=True)
 
 
 @pytest.mark.parametrize("M,K,Ns", [(1, 448, [16, 32]), (3, 4096, [64, 48])])
 def test_fused_tl2(M, K, Ns):
     _announce("fused tl2", M, K, Ns)
     _fused_case("tl2", M, K, Ns, seed=inputs.seed_for(2, 99 + M + K))
+
+
+# One token through the fused call (one launch that also quantises) on the exact linear groups the benchmark times,
+# and one shape for each remaining instance of the single-token streaming kernel.  Instance (waves, 256-k blocks
+# per wave per batch, float4 of the row per thread) that each shape selects on a 256-CU MI355X, I2_S:
+ONE_TOKEN_GROUPS = [
+    (1536, [4096]),                  # the 1536 x 4096 linear: <4, 2, 2>
+    (3200, [3200]),                  # 3B-class o: <4, 4, 4>
+    (4096, [4096, 1024, 1024]),      # 8B-class q/k/v: <4, 4, 4>
+    (4096, [4096]),                  # 8B-class o: <4, 4, 4>
+    (4096, [14336, 14336]),          # 8B-class gate/up: <4, 4, 4>
+    (14336, [4096]),                 # 8B-class down: <16, 4, 4>
+    (1024, [4096]),                  # <4, 1, 1>
+    (2560, [4096]),                  # <4, 3, 4>
+    (6144, [1024]),                  # <16, 2, 2>
+    (28672, [1024]),                 # <16, 4, 8>, two batches per row group
+    (40960, [512]),                  # <16, 4, 16>, three batches per row group
+]
+
+
+@pytest.mark.parametrize("K,Ns", ONE_TOKEN_GROUPS)
+def test_fused_one_token_workload_groups(K, Ns):
+    _announce("fused one token", K, Ns)
+    _fused_case(("i2s", "tl2"), 1, K, Ns, seed=inputs.seed_for(2, 3000 + K + len(Ns)))
+
+
+# The 100B-class layer's groups at one token (the launches of the stack benchmark), both layouts.  I2_S: q/k/v
+# (2304 row groups: 256 work groups of <16, 3, 4> walking nine row groups each), o and down (768 row groups:
+# three per work group; down <16, 3, 16> with three batches per row group), gate/up (4128 row groups).  TL2:
+# q/k/v, o and gate/up on the MFMA expansion with the row quantised inside; down (K = 33024, 86 blocks) through
+# the quantiser and the table-lookup kernel.
+@pytest.mark.parametrize("K,Ns", [(12288, [12288, 12288, 12288]), (12288, [12288]), (12288, [33024, 33024]),
+                                  (33024, [12288])])
+def test_fused_one_token_100b_groups(K, Ns):
+    _announce("fused one token 100B-class", K, Ns)
+    _fused_case(("i2s", "tl2"), 1, K, Ns, seed=inputs.seed_for(4, 10 * len(Ns) + K % 7))

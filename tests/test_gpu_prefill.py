@@ -1,7 +1,6 @@
 """GPU parity of the prefill path (M > 16 tokens, int8-MFMA GEMM) against the oracle.
 
-Small shapes compare every output; the 8B-class prefill shapes (M = 512 and 2048) compare every output of a
-seeded sample of token rows, which the oracle computes exactly.
+Every test compares every output with the oracle, including the 8B-class prefill shapes (M = 512 and 2048).
 """
 import numpy as np
 import pytest
@@ -48,7 +47,7 @@ def test_i2s_prefill_parity(M, N, K, rowsum):
 def test_i2s_prefill_wide_tiles(M, N, K, rowsum):
     # grids of at least one 128 x 512 tile per CU take the widest tile; K = 320 ends in a short block
     _announce("i2s prefill wide tiles", M, N, K, rowsum)
-    _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(4, 7 * M + N + K), sample_rows=12, rowsum=rowsum)
+    _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(4, 7 * M + N + K), rowsum=rowsum)
 
 
 def test_i2s_prefill_extreme_values():
@@ -75,4 +74,4 @@ def test_i2s_prefill_workload_shapes(M):
         if name in ("k", "v", "up"):        # same shapes as q / gate; keep the suite short
             continue
         _announce("prefill workload", name, M, N, K)
-        _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(3, i), sample_rows=6)
+        _prefill_vs_oracle(M, N, K, seed=inputs.seed_for(3, i))
