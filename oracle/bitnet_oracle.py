@@ -19,9 +19,12 @@ What it computes, with the part of the paper each step follows:
   each weight triple becomes a 4-bit index plus a 1-bit sign held in separate planes (signed-unsigned
   weight splitting, Sec. 3.1.2); the K remainder that does not fill a TL2 block uses TL1 pair codes
   (Table 5), as block-fitting weight splitting prescribes (Sec. 3.1.2).
+* ``pack_tl1`` / ``unpack_tl1`` -- the TL1 format on its own (Table 1 "TL1_1", Algorithm TL1, Table 5): every
+  weight pair is its 4-bit Table 5 code, 2 bits per weight, tiled like I2_S (see ``tl1_pair_position``).
 * ``mad_gemm`` -- Eq. 1 / Algorithm "MAD-based mpGEMM": acc[m, n] = sum_k xq[m, k] * t[n, k], exact.
 * ``elut_tables`` / ``elut_gemm`` -- Eq. 3 / Algorithm "ELUT mpGEMM" with mirror consolidation
-  (Sec. 3.1.1) and the 1-bit sign operation of Eq. 5: an independent second route to the same integers.
+  (Sec. 3.1.1) and the 1-bit sign operation of Eq. 5: an independent second route to the same integers;
+  ``tl1_tables`` / ``elut_gemm_tl1`` the same for the TL1 format (Algorithm TL1: 9-entry pair tables).
 * ``epilogue`` -- y = acc * beta / s_m in float64 (the dequantisation the quantisers above imply).
 
 All floating-point decisions that produce integers (the weight divide and round, the activation multiply
@@ -352,6 +355,73 @@ def unpack_tl2(packed: np.ndarray, N: int, K: int) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------------------------
+# a2: TL1 packing on its own (Table 1 "TL1_1", Algorithm TL1, Table 5).  Layout definition.
+# ----------------------------------------------------------------------------------------------
+def tl1_packed_bytes(N: int, K: int) -> int:
+    """4 bits per pair of weights: 2 bits per weight, like I2_S."""
+    check_shape(N, K)
+    return N * K // 4
+
+
+def tl1_pair_position(n, p, N: int, K: int):
+    """(byte, nibble shift) of pair p of row n, the weights k = 2p and 2p + 1.
+
+    The tiling is that of I2_S (``i2s_position``): 16-row groups, 256-k blocks, lane l = 16*q + r owning one
+    32-bit word per 64-k sub-tile j of a block, and that word holding the 16 weights k = 64*(4*s + j) + 16*q + e
+    (e = 0..15) of row 16R + r.  Inside the word the 8 pair codes sit as: pair e // 2 = i of the 16 in byte
+    i % 4, low nibble for i < 4 and high nibble for i >= 4.
+    """
+    n = np.asarray(n, dtype=np.int64)
+    p = np.asarray(p, dtype=np.int64)
+    k = 2 * p
+    R, r = n // 16, n % 16
+    u = k // 64
+    s, j = u // 4, u % 4
+    kk = k % 64
+    q = kk // 16
+    i = (kk % 16) // 2
+    T = np.minimum(4, K // 64 - 4 * s)
+    lane = 16 * q + r
+    byte = R * (4 * K) + s * 1024 + 4 * T * lane + 4 * j + i % 4
+    return byte, 4 * (i // 4)
+
+
+def pack_tl1(t: np.ndarray) -> np.ndarray:
+    t = np.asarray(t)
+    N, K = t.shape
+    check_shape(N, K)
+    if t.min(initial=0) < -1 or t.max(initial=0) > 1:
+        raise ValueError("weights must be ternary")
+    out = np.zeros(tl1_packed_bytes(N, K), dtype=np.uint8)
+    P = K // 2
+    nn, pp = np.meshgrid(np.arange(N), np.arange(P), indexing="ij")
+    tp = t.astype(np.int64).reshape(N, P, 2)
+    code = tl1_code(tp[..., 0], tp[..., 1])
+    byte, shift = tl1_pair_position(nn, pp, N, K)
+    np.bitwise_or.at(out, byte.ravel(), (code << shift).ravel().astype(np.uint8))
+    return out
+
+
+def tl1_decode_codes(packed: np.ndarray, N: int, K: int) -> np.ndarray:
+    """The Table 5 code of every pair, [N, K/2]."""
+    check_shape(N, K)
+    packed = np.asarray(packed, dtype=np.uint8)
+    if packed.size != tl1_packed_bytes(N, K):
+        raise ValueError("TL1 buffer has the wrong size")
+    nn, pp = np.meshgrid(np.arange(N), np.arange(K // 2), indexing="ij")
+    byte, shift = tl1_pair_position(nn, pp, N, K)
+    return (packed[byte].astype(np.int64) >> shift) & 0xF
+
+
+def unpack_tl1(packed: np.ndarray, N: int, K: int) -> np.ndarray:
+    code = tl1_decode_codes(packed, N, K)
+    if np.any(code > 8):
+        raise ValueError("TL1 codes above 8 never occur in a valid buffer")
+    pair = np.stack([code // 3 - 1, code % 3 - 1], axis=-1)
+    return pair.reshape(N, K).astype(np.int8)
+
+
+# ----------------------------------------------------------------------------------------------
 # a5/a6: MAD accumulation (Eq. 1, Algorithm "MAD-based mpGEMM")
 # ----------------------------------------------------------------------------------------------
 F64_EXACT = 1 << 53       # every integer of magnitude up to 2^53 is a float64
@@ -424,6 +494,31 @@ def elut_gemm(xq: np.ndarray, packed_tl2: np.ndarray, N: int, K: int) -> np.ndar
         if lut1.shape[1]:
             vals1 = np.take_along_axis(lut1[m][None, :, :], tail[:, :, None], axis=2)[..., 0]
             acc[m] += vals1.sum(axis=1)
+    return acc.astype(np.int32)
+
+
+def tl1_tables(xq: np.ndarray) -> np.ndarray:
+    """Per token, the 9-entry table of every weight pair (PreCompute of Algorithm TL1):
+    lut[m, p, i] = (i//3 - 1)*a0 + (i%3 - 1)*a1 with (a0, a1) = xq[m, 2p:2p+2], i the Table 5 code."""
+    a = np.asarray(xq, dtype=np.int64)
+    M, K = a.shape
+    pair = a.reshape(M, K // 2, 2)
+    lut = np.zeros((M, K // 2, 9), dtype=np.int64)
+    for i in range(9):
+        lut[:, :, i] = (i // 3 - 1) * pair[..., 0] + (i % 3 - 1) * pair[..., 1]
+    return lut
+
+
+def elut_gemm_tl1(xq: np.ndarray, packed_tl1: np.ndarray, N: int, K: int) -> np.ndarray:
+    """acc via one table lookup per weight pair on the packed TL1 buffer (Algorithm TL1, Eq. 3 with g = 2).
+    Shares nothing with ``mad_gemm``."""
+    code = tl1_decode_codes(packed_tl1, N, K)            # [N, K/2]
+    lut = tl1_tables(xq)                                  # [M, K/2, 9]
+    M = lut.shape[0]
+    acc = np.zeros((M, N), dtype=np.int64)
+    for m in range(M):
+        vals = np.take_along_axis(lut[m][None, :, :], code[:, :, None], axis=2)[..., 0]   # [N, K/2]
+        acc[m] = vals.sum(axis=1)
     return acc.astype(np.int32)
 
 

@@ -178,6 +178,32 @@ def test_tl2_positions_hand_computed():
     assert tuple(int(v) for v in O.tl1_tail_position(1, 9, N, K)) == (1348, 4)
 
 
+def test_tl1_positions_hand_computed():
+    N, K = 32, 320      # one full 256-k block and a 64-k block
+    cases = {           # (n, pair): (byte, shift), worked out by hand from the layout definition
+        (0, 0): (0, 0), (0, 1): (1, 0), (0, 4): (0, 4), (0, 7): (3, 4), (1, 0): (16, 0), (0, 8): (256, 0),
+        (0, 32): (4, 0), (0, 128): (1024, 0), (3, 150): (1166, 4), (16, 0): (1280, 0), (17, 0): (1296, 0),
+    }
+    for (n, pr), (byte, shift) in cases.items():
+        b, sh = O.tl1_pair_position(n, pr, N, K)
+        assert (int(b), int(sh)) == (byte, shift), (n, pr)
+
+
+@pytest.mark.parametrize("N,K", [(16, 64), (32, 320), (16, 1600)])
+def test_tl1_round_trip_every_nibble_once(N, K):
+    rng = np.random.default_rng(N + 13 * K)
+    t = rng.integers(-1, 2, size=(N, K)).astype(np.int8)
+    p = O.pack_tl1(t)
+    assert p.size * 8 == 2 * N * K                    # 4 bits per pair: 2 bits per weight (Table 1, TL1)
+    assert np.array_equal(O.unpack_tl1(p, N, K), t)
+    nn, pp = np.meshgrid(np.arange(N), np.arange(K // 2), indexing="ij")
+    b, sh = O.tl1_pair_position(nn, pp, N, K)
+    nib = b.ravel() * 2 + sh.ravel() // 4
+    assert np.unique(nib).size == N * K // 2 and nib.max() == N * K // 2 - 1
+    codes = O.tl1_decode_codes(p, N, K)
+    assert np.array_equal(codes, O.tl1_code(t[:, 0::2], t[:, 1::2]))   # Table 5 code of every pair
+
+
 @pytest.mark.parametrize("N,K", [(16, 64), (16, 128), (32, 192), (16, 256), (48, 320), (16, 384),
                                  (32, 448), (16, 832), (32, 1600)])
 def test_pack_round_trips_and_sizes(N, K):
@@ -240,6 +266,26 @@ def test_elut_equals_mad(M, N, K):
     xq = rng.integers(-127, 128, size=(M, K)).astype(np.int8)
     packed = O.pack_tl2(t)
     assert np.array_equal(O.elut_gemm(xq, packed, N, K), O.mad_gemm(xq, t))
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 16, 64), (3, 32, 320), (2, 16, 1600)])
+def test_elut_tl1_equals_mad(M, N, K):
+    rng = np.random.default_rng(M * 17 + N * 5 + K)
+    t = rng.integers(-1, 2, size=(N, K)).astype(np.int8)
+    xq = rng.integers(-128, 128, size=(M, K)).astype(np.int8)
+    assert np.array_equal(O.elut_gemm_tl1(xq, O.pack_tl1(t), N, K), O.mad_gemm(xq, t))
+
+
+def test_tl1_tables_are_enumerations():
+    rng = np.random.default_rng(5)
+    xq = rng.integers(-128, 128, size=(2, 64)).astype(np.int8)
+    lut = O.tl1_tables(xq)
+    assert lut.shape == (2, 32, 9)
+    for m in range(2):
+        for p in (0, 17, 31):
+            b = [int(v) for v in xq[m, 2 * p:2 * p + 2]]
+            for t in itertools.product((-1, 0, 1), repeat=2):
+                assert int(lut[m, p, int(O.tl1_code(*t))]) == b[0] * t[0] + b[1] * t[1]
 
 
 def test_elut_tables_are_enumerations():
