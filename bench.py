@@ -50,6 +50,7 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-parity", action="store_true")
+    p.add_argument("--replays", type=int, default=10, help="replays of the timed graph for the spread figure")
     return p.parse_args()
 
 
@@ -191,7 +192,7 @@ def main():
     # spread: the same K steps replayed again, each replay timed on its own (outside the timed region above)
     reps = [ms_per_step]
     with torch.cuda.stream(stream):
-        for _ in range(SPREAD_REPLAYS - 1):
+        for _ in range(max(1, args.replays) - 1):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             g_main.replay()
@@ -284,7 +285,6 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-SPREAD_REPLAYS = 10
 # committed counter summaries (HBM bytes per launch) and the kernel sources they were taken on
 # (workload, tokens, layout) -> (summary, kernel sources)
 TRAFFIC = {
