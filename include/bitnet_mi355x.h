@@ -128,6 +128,22 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
                             size_t ws_bytes, void* stream);
 
 /*
+ * bitnet_mpgemm_noalloc -- bitnet_mpgemm without a workspace argument, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ *   Arguments, results, shapes and statuses as bitnet_mpgemm.  The workspace bitnet_mpgemm would take (split-K
+ *   slices of the prefill GEMM, TL2 weights rewritten for it) comes from a static device array of
+ *   BITNET_NOALLOC_SCRATCH_BYTES (32 MiB) that each GPU the library runs on holds until the process ends.  A shape
+ *   whose bitnet_mpgemm_workspace_bytes exceeds it returns BITNET_E_WORKSPACE before anything is enqueued.
+ *   Every call on one GPU shares that GPU's array and leaves its contents behind (nothing in it has to start at
+ *   zero): calls on one stream are ordered, but calls that overlap on one GPU (other streams, other threads) race.
+ *   The call allocates and frees nothing; on its first use on a device it looks the array's address up once.
+ */
+#define BITNET_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+bitnet_status bitnet_mpgemm_noalloc(int layout, const void* packed, size_t packed_bytes, const float* w_scale,
+                                    int64_t N, int64_t K, const int8_t* xq, const float* x_scale,
+                                    const int32_t* x_rowsum, int64_t M, float* y, int32_t* acc, void* stream);
+
+/*
  * Workspace bytes with which bitnet_mpgemm_fused runs every split it can use for these n_linears weights (host
  * array N of rows, shared K, M tokens; 0 is a valid answer and 0 is also returned for invalid arguments): at
  * least the largest bitnet_mpgemm_workspace_bytes of the weights (the minimum the call accepts), and for a fused

@@ -37,6 +37,10 @@ _SIGNATURES = [
      [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    ("bitnet_mpgemm_noalloc", ctypes.c_int,
+     [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+      ctypes.c_void_p]),
     ("bitnet_mpgemm_fused_workspace_bytes", ctypes.c_size_t,
      [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
     ("bitnet_mpgemm_fused", ctypes.c_int,
@@ -162,6 +166,22 @@ def bitnet_mpgemm(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=N
                              _ptr(y, "y", torch.float32),
                              _ptr(acc, "acc", torch.int32), ws_ptr, ws_bytes, _stream(stream))
     _check("bitnet_mpgemm", st)
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20     # BITNET_NOALLOC_SCRATCH_BYTES
+
+
+def bitnet_mpgemm_noalloc(layout, packed, w_scale, N: int, K: int, xq, x_scale, y, acc=None, stream=None,
+                          x_rowsum=None) -> None:
+    """bitnet_mpgemm with its workspace taken from the library's static per-GPU scratch (no allocation)."""
+    import torch
+    M = xq.shape[0]
+    st = lib().bitnet_mpgemm_noalloc(_layout(layout), _ptr(packed, "packed", torch.uint8), packed.numel(),
+                                     _ptr(w_scale, "w_scale", torch.float32), N, K, _ptr(xq, "xq", torch.int8),
+                                     _ptr(x_scale, "x_scale", torch.float32),
+                                     _ptr(x_rowsum, "x_rowsum", torch.int32), M, _ptr(y, "y", torch.float32),
+                                     _ptr(acc, "acc", torch.int32), _stream(stream))
+    _check("bitnet_mpgemm_noalloc", st)
 
 
 def bitnet_mpgemm_fused_workspace_bytes(layout, Ns, K: int, M: int) -> int:

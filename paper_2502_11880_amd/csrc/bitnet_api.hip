@@ -6,6 +6,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 
 namespace {
 
@@ -151,16 +152,21 @@ size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int6
     return need;
 }
 
-bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale, int64_t N,
-                            int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
-                            float* y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks of bitnet_mpgemm's arguments other than the workspace; sets *need to its workspace bytes.
+bitnet_status mpgemm_check(int layout, const void* packed, size_t packed_bytes, const float* w_scale, int64_t N,
+                           int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
+                           float* y, int32_t* acc, size_t* need) {
     if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
     if (!packed || !w_scale || !xq || !x_scale || !y) return fail(BITNET_E_INVALID, "null pointer argument");
     if (!weight_shape_ok(N, K)) return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
                                             (long long)kMaxK, (long long)N, (long long)K);
     if (M < 1 || M > ((int64_t)1 << 24)) return fail(BITNET_E_SHAPE, "need 1 <= M <= 2^24; got M=%lld", (long long)M);
     if (!aligned(packed, 16) || !aligned(xq, 16) || !aligned(y, 16) || (acc && !aligned(acc, 16)) ||
-        !aligned(ws, 16) || !aligned(w_scale, 4) || !aligned(x_scale, 4) || !aligned(x_rowsum, 4))
+        !aligned(w_scale, 4) || !aligned(x_scale, 4) || !aligned(x_rowsum, 4))
         return fail(BITNET_E_ALIGN, "packed, xq, y, acc and ws need 16-byte alignment, scales and x_rowsum 4-byte");
     if (packed_bytes < packed_bytes_of(layout, N, K))
         return fail(BITNET_E_INVALID, "packed buffer holds %zu bytes, %zu needed", packed_bytes,
@@ -169,11 +175,15 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
                                         (uint64_t)M * (uint64_t)K >= ((uint64_t)1 << 32)))
         return fail(BITNET_E_SHAPE, "I2_S needs N*K and M*K below 2^32; got M=%lld N=%lld K=%lld", (long long)M,
                     (long long)N, (long long)K);
-    // the workspace holds split-K slices of the prefill GEMM (used when x_rowsum is given)
-    const size_t need = bitnet_mpgemm_workspace_bytes(layout, M, N, K);
-    if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
+    *need = bitnet_mpgemm_workspace_bytes(layout, M, N, K);
+    return BITNET_OK;
+}
 
-    hipStream_t s = (hipStream_t)stream;
+// The launches of bitnet_mpgemm once its arguments are checked (ws holds at least the workspace it needs).
+bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, const float* w_scale, int64_t N,
+                         int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
+                         float* y, int32_t* acc, void* ws, size_t ws_bytes, hipStream_t s) {
+    (void)packed_bytes;
     if (layout == BITNET_LAYOUT_I2S && M <= kDecodeMaxTokens)
         return hip_status(bitnet::launch_i2s_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
                                                     (int)M, (int)K, s),
@@ -209,6 +219,76 @@ bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes,
         if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
     }
     return ok();
+}
+
+// Scratch of bitnet_mpgemm_noalloc: one copy of this array on every GPU the library runs on, held until the
+// process ends.  In host code its name is only a handle; the device address of each GPU's copy comes from
+// hipGetSymbolAddress (once per device, with that device current) and is the only form passed to kernels.
+constexpr size_t kNoallocScratchBytes = BITNET_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+
+namespace {
+
+// The current device's copy of `scratch`.
+bitnet_status scratch_on_current_device(void** out) {
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(BITNET_E_HIP, "device %d outside the supported range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t g = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (g != hipSuccess || !p) return hip_status(g != hipSuccess ? g : hipErrorInvalidSymbol,
+                                                     "hipGetSymbolAddress of the no-allocation scratch");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return BITNET_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+bitnet_status bitnet_mpgemm(int layout, const void* packed, size_t packed_bytes, const float* w_scale, int64_t N,
+                            int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
+                            float* y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
+    size_t need = 0;
+    const bitnet_status st = mpgemm_check(layout, packed, packed_bytes, w_scale, N, K, xq, x_scale, x_rowsum, M, y,
+                                          acc, &need);
+    if (st != BITNET_OK) return st;
+    if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
+    // the workspace holds split-K slices of the prefill GEMM (used when x_rowsum is given) and TL2 weights
+    // rewritten for it
+    if (need && (!ws || ws_bytes < need)) return fail(BITNET_E_WORKSPACE, "mpgemm workspace needs %zu bytes", need);
+    return mpgemm_run(layout, packed, packed_bytes, w_scale, N, K, xq, x_scale, x_rowsum, M, y, acc, ws, ws_bytes,
+                      (hipStream_t)stream);
+}
+
+bitnet_status bitnet_mpgemm_noalloc(int layout, const void* packed, size_t packed_bytes, const float* w_scale,
+                                    int64_t N, int64_t K, const int8_t* xq, const float* x_scale,
+                                    const int32_t* x_rowsum, int64_t M, float* y, int32_t* acc, void* stream) {
+    size_t need = 0;
+    bitnet_status st = mpgemm_check(layout, packed, packed_bytes, w_scale, N, K, xq, x_scale, x_rowsum, M, y, acc,
+                                    &need);
+    if (st != BITNET_OK) return st;
+    if (need > kNoallocScratchBytes)
+        return fail(BITNET_E_WORKSPACE, "this shape needs %zu bytes of workspace; the no-allocation scratch holds %zu",
+                    need, kNoallocScratchBytes);
+    void* ws = nullptr;
+    if (need) {
+        st = scratch_on_current_device(&ws);
+        if (st != BITNET_OK) return st;
+    }
+    return mpgemm_run(layout, packed, packed_bytes, w_scale, N, K, xq, x_scale, x_rowsum, M, y, acc, ws,
+                      need ? kNoallocScratchBytes : 0, (hipStream_t)stream);
 }
 
 bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* packed, const size_t* packed_bytes,

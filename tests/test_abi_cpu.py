@@ -88,6 +88,26 @@ def test_mpgemm_validation_statuses():
 
 
 @cpu_only
+def test_mpgemm_noalloc_validation_statuses():
+    lib = B.lib()
+
+    def call(**kw):
+        a = dict(layout=1, packed=FAKE, packed_bytes=1 << 30, w_scale=FAKE, N=16384, K=16384, xq=FAKE, x_scale=FAKE,
+                 x_rowsum=None, M=64, y=FAKE, acc=None, stream=None)
+        a.update(kw)
+        return lib.bitnet_mpgemm_noalloc(a["layout"], a["packed"], a["packed_bytes"], a["w_scale"], a["N"], a["K"],
+                                         a["xq"], a["x_scale"], a["x_rowsum"], a["M"], a["y"], a["acc"], a["stream"])
+
+    assert call(packed=None) == 1
+    assert call(layout=9) == 4
+    assert call(K=100) == 2
+    assert call(xq=FAKE + 4) == 3
+    # TL2 prefill at 16384 x 16384 rewrites 64 MiB of weights: more than the static scratch holds
+    assert B.bitnet_mpgemm_workspace_bytes("tl2", 64, 16384, 16384) > B.NOALLOC_SCRATCH_BYTES
+    assert call() == 5 and "scratch" in B.bitnet_last_error()
+
+
+@cpu_only
 def test_quantize_and_pack_validation_statuses():
     lib = B.lib()
     assert lib.bitnet_quantize_act(None, 1, 64, FAKE, FAKE, None, None) == 1
