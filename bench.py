@@ -46,7 +46,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", type=int, default=4)
     p.add_argument("--tokens", type=int, default=None)
-    p.add_argument("--layout", default="i2s", choices=["i2s", "tl2"])
+    p.add_argument("--layout", default="i2s", choices=["i2s", "tl2", "tl1"])
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-parity", action="store_true")
@@ -214,14 +214,15 @@ def main():
         avg_bytes = sum(grp_bytes) * n_layers / launches
         avg_launch_ms = ms_per_step / launches
         achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
-        if layout != "i2s" and M == 1:
+        words = " on TL1 words" if layout == "tl1" else ""
+        if layout == "tl2" and M == 1:
             kernel = "tl2_mfma_decode_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
-        elif layout != "i2s":
+        elif layout == "tl2":
             kernel = "bitnet_mpgemm_fused on TL2: quantize_rows_reg + tl2_mfma_decode_kernel per group"
         elif M == 1:
-            kernel = "i2s_gemv1_stream_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
+            kernel = f"i2s_gemv1_stream_kernel{words} (bitnet_mpgemm_fused, one token: quantiser fused)"
         else:
-            kernel = "bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_stream_kernel per group"
+            kernel = f"bitnet_mpgemm_fused: quantize_rows_reg + i2s_decode_stream_kernel{words} per group"
         traffic = measured_traffic(*TRAFFIC[key]) if (key := (args.workload, M, layout)) in TRAFFIC else None
         roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
@@ -236,7 +237,7 @@ def main():
         achieved = (flops / launches) / (avg_launch_ms * 1e-3) / 1e12
         kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
         if layout != "i2s":
-            kernel = "tl2_to_i2s_kernel per group + " + kernel
+            kernel = f"{layout}_to_i2s transcoding per group + " + kernel
         traffic = measured_traffic(*TRAFFIC[key]) if (key := (args.workload, M, layout)) in TRAFFIC else None
         roofline = {"bound": "mfma", "kernel": kernel,
                     "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",

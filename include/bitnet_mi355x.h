@@ -40,7 +40,7 @@ typedef enum {
 } bitnet_status;
 
 /*
- * Weight layouts.  Both need N % 16 == 0 and K % 64 == 0 (rows are tiled by 16, K by 64).
+ * Weight layouts.  All need N % 16 == 0 and K % 64 == 0 (rows are tiled by 16, K by 64).
  *
  * BITNET_LAYOUT_I2S ("Int2 with a Scale", Table 1, Sec. 3.2.2): 2 bits per weight, code = t + 1.
  *   16-row groups; K in blocks of up to 256 (four 64-k sub-tiles; only the last block may be shorter).
@@ -58,10 +58,16 @@ typedef enum {
  *   in byte i/2, low nibble first) and 4 sign bytes (triple i at bit i%8 of byte i/8).  The tail is cut
  *   into 64-k units; lane (r, q) owns one 32-bit word per unit holding pairs 32u + 8q + i (byte i/2, low
  *   nibble first), with each lane's words contiguous.
+ *
+ * BITNET_LAYOUT_TL1 (Table 1 "TL1_1", Algorithm TL1, Table 5): 2 bits per weight.  Every pair of weights is its
+ *   4-bit Table 5 code 3(t0+1) + (t1+1), in the tiling of I2_S: a 32-bit word of lane (r, q) in sub-tile j of
+ *   block s holds the 16 weights k = 64*(4*s + j) + 16*q + e of row 16R + r as 8 pair codes, pair i (weights
+ *   e = 2i, 2i+1) in byte i % 4, low nibble for i < 4 and high nibble for i >= 4.  Size N*K/4 bytes.
  */
 typedef enum {
     BITNET_LAYOUT_I2S = 0,
-    BITNET_LAYOUT_TL2 = 1
+    BITNET_LAYOUT_TL2 = 1,
+    BITNET_LAYOUT_TL1 = 2
 } bitnet_layout;
 
 /* Bytes of the packed buffer for an N x K weight in `layout`; 0 if the shape or layout is unsupported. */
@@ -115,7 +121,9 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *          rewritten in the I2_S layout (N * K / 4 bytes) that the prefill GEMM reads; any contents on entry,
  *          nothing kept between calls.  Calls that run concurrently must not share it.
  *   Shapes: M >= 1, N % 16 == 0, K % 64 == 0, K <= 132096 (127 * K < 2^24 keeps acc exact in fp32);
- *   I2_S also needs N * K and M * K below 2^32.  I2_S: M <= 16 runs the decode GEMV, larger M the prefill GEMM.
+ *   I2_S and TL1 also need N * K and M * K below 2^32.  I2_S: M <= 16 runs the decode GEMV, larger M the prefill
+ *   GEMM.  TL1: M <= 16 runs the same decode GEMV, which expands the pair codes to int8 in registers; larger M
+ *   rewrites the weights in the I2_S layout in the workspace (N * K / 4 bytes) and runs the prefill GEMM.
  *   TL2: one token runs the table lookups of Eq. 3 (tables built in LDS) where the row's tables fit (K <= 14336);
  *   otherwise, up to 16 tokens with 384 <= K < 18816, the packed triples are expanded to int8 weights and
  *   multiplied on int8 MFMA; more than 16 tokens (with N * K and M * K below 2^32) rewrite the weights in the
@@ -173,7 +181,8 @@ size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int6
  *   row quantised in every work group, the triples expanded for MFMA); other TL2 cases run the quantiser and
  *   then one launch for all weights (the MFMA expansion for M <= 16 and K < 18816; for M > 16, every weight
  *   rewritten in the I2_S layout and one prefill launch, where ws holds all of them) or one bitnet_mpgemm call
- *   per weight.
+ *   per weight.  TL1 runs as I2_S up to 16 tokens (the same launches, the pair codes expanded in registers) and
+ *   as TL2 above (every weight rewritten in the I2_S layout, one prefill launch).
  */
 bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* packed, const size_t* packed_bytes,
                                   const float* const* w_scale, const int64_t* N, int64_t K, const float* x,

@@ -16,7 +16,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
 
 BITNET_LAYOUT_I2S = 0
 BITNET_LAYOUT_TL2 = 1
-LAYOUTS = {"i2s": BITNET_LAYOUT_I2S, "tl2": BITNET_LAYOUT_TL2}
+BITNET_LAYOUT_TL1 = 2
+LAYOUTS = {"i2s": BITNET_LAYOUT_I2S, "tl2": BITNET_LAYOUT_TL2, "tl1": BITNET_LAYOUT_TL1}
 
 BITNET_OK = 0
 STATUS_NAMES = {0: "BITNET_OK", 1: "BITNET_E_INVALID", 2: "BITNET_E_SHAPE", 3: "BITNET_E_ALIGN",

@@ -40,10 +40,16 @@ bool weight_shape_ok(int64_t N, int64_t K) {
            N <= (int64_t)1 << 30;
 }
 
-bool layout_ok(int layout) { return layout == BITNET_LAYOUT_I2S || layout == BITNET_LAYOUT_TL2; }
+bool layout_ok(int layout) {
+    return layout == BITNET_LAYOUT_I2S || layout == BITNET_LAYOUT_TL2 || layout == BITNET_LAYOUT_TL1;
+}
+
+// I2_S and TL1 share the tiling, the decode kernels (which read the word format as a template) and their limits.
+bool i2s_tiled(int layout) { return layout == BITNET_LAYOUT_I2S || layout == BITNET_LAYOUT_TL1; }
+int word_format(int layout) { return layout == BITNET_LAYOUT_TL1 ? bitnet::kFmtTl1 : bitnet::kFmtI2s; }
 
 size_t packed_bytes_of(int layout, int64_t N, int64_t K) {
-    if (layout == BITNET_LAYOUT_I2S) return (size_t)N * (size_t)K / 4;
+    if (i2s_tiled(layout)) return (size_t)N * (size_t)K / 4;
     const int64_t three = (K / bitnet::kTl2BlockK) * bitnet::kTl2BlockK;
     const int64_t two = K - three;
     return (size_t)N * three / 6 + (size_t)N * three / 24 + (size_t)N * two / 4;
@@ -61,8 +67,8 @@ bitnet::FusedLinears one_linear(const void* packed, const float* w_scale, int64_
     return L;
 }
 
-// TL2 at M > 16 runs the I2_S prefill GEMM on its weights rewritten in the I2_S layout (in the workspace), where
-// the I2_S limits hold.
+// TL2 and TL1 at M > 16 run the I2_S prefill GEMM on their weights rewritten in the I2_S layout (in the workspace),
+// where the I2_S limits hold.
 bool tl2_via_i2s(int64_t M, int64_t N, int64_t K) {
     return M > kDecodeMaxTokens && (uint64_t)N * (uint64_t)K < ((uint64_t)1 << 32) &&
            (uint64_t)M * (uint64_t)K < ((uint64_t)1 << 32);
@@ -119,7 +125,7 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
     if (!layout_ok(layout) || !weight_shape_ok(N, K) || M < 1) return 0;
     if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens)
         return bitnet::prefill_workspace_bytes(one_linear(nullptr, nullptr, N, nullptr, nullptr), M, K);
-    if (layout == BITNET_LAYOUT_TL2 && tl2_via_i2s(M, N, K))
+    if ((layout == BITNET_LAYOUT_TL2 || layout == BITNET_LAYOUT_TL1) && tl2_via_i2s(M, N, K))
         return align256((size_t)N * (size_t)K / 4) +
                bitnet::prefill_workspace_bytes(one_linear(nullptr, nullptr, N, nullptr, nullptr), M, K);
     return 0;
@@ -134,7 +140,7 @@ size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int6
         const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
         need = w > need ? w : need;
     }
-    const bool tl2_gemm = layout == BITNET_LAYOUT_TL2 && M > kDecodeMaxTokens;
+    const bool tl2_gemm = (layout == BITNET_LAYOUT_TL2 || layout == BITNET_LAYOUT_TL1) && M > kDecodeMaxTokens;
     bool via = tl2_gemm;
     for (int i = 0; i < n_linears; ++i) via = via && tl2_via_i2s(M, N[i], K);
     if ((layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens) || via) {
@@ -171,10 +177,10 @@ bitnet_status mpgemm_check(int layout, const void* packed, size_t packed_bytes, 
     if (packed_bytes < packed_bytes_of(layout, N, K))
         return fail(BITNET_E_INVALID, "packed buffer holds %zu bytes, %zu needed", packed_bytes,
                     packed_bytes_of(layout, N, K));
-    if (layout == BITNET_LAYOUT_I2S && ((uint64_t)N * (uint64_t)K >= ((uint64_t)1 << 32) ||
-                                        (uint64_t)M * (uint64_t)K >= ((uint64_t)1 << 32)))
-        return fail(BITNET_E_SHAPE, "I2_S needs N*K and M*K below 2^32; got M=%lld N=%lld K=%lld", (long long)M,
-                    (long long)N, (long long)K);
+    if (i2s_tiled(layout) && ((uint64_t)N * (uint64_t)K >= ((uint64_t)1 << 32) ||
+                              (uint64_t)M * (uint64_t)K >= ((uint64_t)1 << 32)))
+        return fail(BITNET_E_SHAPE, "I2_S and TL1 need N*K and M*K below 2^32; got M=%lld N=%lld K=%lld",
+                    (long long)M, (long long)N, (long long)K);
     *need = bitnet_mpgemm_workspace_bytes(layout, M, N, K);
     return BITNET_OK;
 }
@@ -184,10 +190,21 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
                          int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
                          float* y, int32_t* acc, void* ws, size_t ws_bytes, hipStream_t s) {
     (void)packed_bytes;
-    if (layout == BITNET_LAYOUT_I2S && M <= kDecodeMaxTokens)
+    if (i2s_tiled(layout) && M <= kDecodeMaxTokens)
         return hip_status(bitnet::launch_i2s_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
-                                                    (int)M, (int)K, s),
+                                                    (int)M, (int)K, s, word_format(layout)),
                           "bitnet_mpgemm launch");
+    if (layout == BITNET_LAYOUT_TL1) {
+        // the TL1 words rewritten as I2_S words at the start of the workspace, the GEMM's split-K slices after them
+        const size_t wbytes = align256((size_t)N * (size_t)K / 4);
+        const int n1 = (int)N;
+        void* dst = ws;
+        hipError_t e = bitnet::launch_tl1_to_i2s(&packed, &n1, &dst, 1, (int)K, s);
+        if (e == hipSuccess)
+            e = bitnet::launch_i2s_prefill(one_linear(ws, w_scale, N, y, acc), xq, x_scale, x_rowsum, (int)M, (int)K,
+                                           static_cast<uint8_t*>(ws) + wbytes, ws_bytes - wbytes, s);
+        return hip_status(e, "bitnet_mpgemm launch");
+    }
     if (layout == BITNET_LAYOUT_I2S)
         return hip_status(bitnet::launch_i2s_prefill(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
                                                      (int)M, (int)K, ws, ws_bytes, s),
@@ -314,9 +331,9 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
         if (packed_bytes[i] < packed_bytes_of(layout, N[i], K))
             return fail(BITNET_E_INVALID, "weight %d: packed buffer holds %zu bytes, %zu needed", i, packed_bytes[i],
                         packed_bytes_of(layout, N[i], K));
-        if (layout == BITNET_LAYOUT_I2S && ((uint64_t)N[i] * (uint64_t)K >= ((uint64_t)1 << 32) ||
-                                            (uint64_t)M * (uint64_t)K >= ((uint64_t)1 << 32)))
-            return fail(BITNET_E_SHAPE, "weight %d: I2_S needs N*K and M*K below 2^32", i);
+        if (i2s_tiled(layout) && ((uint64_t)N[i] * (uint64_t)K >= ((uint64_t)1 << 32) ||
+                                  (uint64_t)M * (uint64_t)K >= ((uint64_t)1 << 32)))
+            return fail(BITNET_E_SHAPE, "weight %d: I2_S and TL1 need N*K and M*K below 2^32", i);
         const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
         need = w > need ? w : need;
     }
@@ -326,7 +343,8 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
 
     hipStream_t s = (hipStream_t)stream;
-    if (layout == BITNET_LAYOUT_I2S) {
+    if (layout == BITNET_LAYOUT_I2S || (layout == BITNET_LAYOUT_TL1 && M <= kDecodeMaxTokens)) {
+        const int fmt = word_format(layout);
         bitnet::FusedLinears L{};
         L.count = n_linears;
         int64_t rgs = 0;
@@ -341,18 +359,19 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
         if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
         bitnet::seal_fused(L);
         if (quantise && M == 1 && K <= bitnet::kFusedMaxK)   // one launch: quantise inside every work group
-            return hip_status(bitnet::launch_i2s_gemv1_stream(L, x, (int)K, xq, x_scale, x_rowsum, s),
+            return hip_status(bitnet::launch_i2s_gemv1_stream(L, x, (int)K, xq, x_scale, x_rowsum, s, fmt),
                               "bitnet_mpgemm_fused launch");
         hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
         if (e == hipSuccess)
             e = M <= kDecodeMaxTokens
-                    ? bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s)
+                    ? bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s, fmt)
                     : bitnet::launch_i2s_prefill(L, xq, x_scale, x_rowsum, (int)M, (int)K, ws, ws_bytes, s);
         return hip_status(e, "bitnet_mpgemm_fused launch");
     }
-    // TL2: one token whose tables fit in LDS: one streaming launch for every weight (quantising inside).  Otherwise
-    // the quantiser once, then one MFMA launch for every weight (token slices that fit in LDS) or, where that path
-    // does not cover K, one table-lookup launch per weight.
+    // TL2: one token: one launch for every weight that quantises inside (the MFMA expansion, or the table lookups
+    // where the whole row's tables fit in LDS).  Otherwise the quantiser once, then one MFMA launch for every weight
+    // (token slices that fit in LDS) or, where that path does not cover K, one table-lookup launch per weight.
+    // TL2 and TL1 past 16 tokens: the quantiser, every weight rewritten in the I2_S layout, one prefill launch.
     bitnet::FusedLinears L{};
     L.count = n_linears;
     int64_t rgs = 0;
@@ -366,10 +385,11 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     }
     if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
     bitnet::seal_fused(L);
-    if (M == 1 && quantise && bitnet::tl2_mfma_max_tokens((int)K) > 0)
+    const bool tl2 = layout == BITNET_LAYOUT_TL2;
+    if (tl2 && M == 1 && quantise && bitnet::tl2_mfma_max_tokens((int)K) > 0)
         return hip_status(bitnet::launch_tl2_mfma_quant(L, x, (int)K, xq, x_scale, x_rowsum, s),
                           "bitnet_mpgemm_fused launch");
-    if (M == 1 && bitnet::tl2_stream_fits((int)K)) {
+    if (tl2 && M == 1 && bitnet::tl2_stream_fits((int)K)) {
         if (!quantise) return hip_status(bitnet::launch_tl2_stream(L, nullptr, (int)K, xq, x_scale, x_rowsum, s),
                                          "bitnet_mpgemm_fused launch");
         return hip_status(bitnet::launch_tl2_stream(L, x, (int)K, xq, x_scale, x_rowsum, s),
@@ -396,13 +416,14 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
             T.packed[i] = static_cast<const uint8_t*>(dst[i]);
             off += align256((size_t)N[i] * (size_t)K / 4);
         }
-        e = bitnet::launch_tl2_to_i2s(packed, n32, dst, n_linears, (int)K, s);
+        e = tl2 ? bitnet::launch_tl2_to_i2s(packed, n32, dst, n_linears, (int)K, s)
+                : bitnet::launch_tl1_to_i2s(packed, n32, dst, n_linears, (int)K, s);
         if (e == hipSuccess)
             e = bitnet::launch_i2s_prefill(T, xq, x_scale, x_rowsum, (int)M, (int)K, static_cast<uint8_t*>(ws) + words,
                                            ws_bytes - words, s);
         return hip_status(e, "bitnet_mpgemm_fused launch");
     }
-    if (M <= kDecodeMaxTokens && bitnet::tl2_mfma_max_tokens((int)K) > 0)
+    if (tl2 && M <= kDecodeMaxTokens && bitnet::tl2_mfma_max_tokens((int)K) > 0)
         return hip_status(bitnet::launch_tl2_mfma_decode(L, xq, x_scale, (int)M, (int)K, s),
                           "bitnet_mpgemm_fused launch");
     for (int i = 0; i < n_linears; ++i) {

@@ -98,6 +98,50 @@ __device__ __forceinline__ v4i unpack_codes(uint32_t w) {
     return b;
 }
 
+// Weight formats that share the I2_S tiling (one 32-bit word = 16 weights of one row, k = 16 q + e, e = 0..15):
+// I2_S words hold 2-bit codes t + 1; TL1 words hold the Table 5 codes c = 3 (t0 + 1) + (t1 + 1) of 8 pairs, pair i
+// (weights e = 2i, 2i + 1) in byte i % 4, low nibble for i < 4 and high nibble for i >= 4.
+constexpr int kFmtI2s = 0;
+constexpr int kFmtTl1 = 1;
+
+// A TL1 word as the offset codes t + 1 of its 16 weights, in four int8 words:
+// [t0 + 1 of pairs 0..3, t1 + 1 of pairs 0..3, t0 + 1 of pairs 4..7, t1 + 1 of pairs 4..7], which are the weights
+// e = 0,2,4,6 | 1,3,5,7 | 8,10,12,14 | 9,11,13,15.  floor(c / 3) = (11 c) >> 5 for c <= 8, and every byte of the
+// word products stays below 256, so the word arithmetic never carries from one byte into the next.
+__device__ __forceinline__ v4i tl1_codes(uint32_t w) {
+    const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;
+    const uint32_t qlo = ((lo * 11u) >> 5) & 0x07070707u, qhi = ((hi * 11u) >> 5) & 0x07070707u;
+    v4i b;
+    b.x = (int)qlo;
+    b.y = (int)(lo - 3u * qlo);
+    b.z = (int)qhi;
+    b.w = (int)(hi - 3u * qhi);
+    return b;
+}
+
+// The 16 activation codes of k = 16 q .. 16 q + 15 (natural order in) in the order tl1_codes gives the weights.
+// v_perm_b32 picks byte s of {hi, lo} (s < 4: lo) for every selector byte s.
+__device__ __forceinline__ v4i tl1_perm16(v4i a) {
+    v4i o;
+    o.x = (int)__builtin_amdgcn_perm((uint32_t)a.y, (uint32_t)a.x, 0x06040200u);
+    o.y = (int)__builtin_amdgcn_perm((uint32_t)a.y, (uint32_t)a.x, 0x07050301u);
+    o.z = (int)__builtin_amdgcn_perm((uint32_t)a.w, (uint32_t)a.z, 0x06040200u);
+    o.w = (int)__builtin_amdgcn_perm((uint32_t)a.w, (uint32_t)a.z, 0x07050301u);
+    return o;
+}
+
+// The MFMA B operand (offset codes) of one packed word, and the A operand order that matches it.
+template <int FMT>
+__device__ __forceinline__ v4i decode_b(uint32_t w) {
+    if constexpr (FMT == kFmtTl1) return tl1_codes(w);
+    else return unpack_codes(w);
+}
+template <int FMT>
+__device__ __forceinline__ v4i order_a(v4i a) {
+    if constexpr (FMT == kFmtTl1) return tl1_perm16(a);
+    else return a;
+}
+
 __device__ __forceinline__ uint32_t word_of(const v4u& v, int j) {
     return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
 }
@@ -175,10 +219,15 @@ size_t prefill_workspace_bytes(const FusedLinears& L, int64_t M, int64_t K);
 hipError_t launch_i2s_prefill(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                               int M, int K, void* ws, size_t ws_bytes, hipStream_t stream);
 constexpr int64_t kFusedMaxK = 61440;   // single-token fused quantise+GEMV keeps the K codes in LDS
+// fmt: kFmtI2s or kFmtTl1 (the weights' word format; both formats share the I2_S tiling)
 hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
-                             int M, int K, hipStream_t stream);
+                             int M, int K, hipStream_t stream, int fmt = kFmtI2s);
 hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
-                                   int32_t* x_rowsum, hipStream_t stream);
+                                   int32_t* x_rowsum, hipStream_t stream, int fmt = kFmtI2s);
+// The TL1 weights of `count` (1..kMaxFused) N[i] x K tensors rewritten as I2_S words (same positions, N[i] K / 4
+// bytes at i2s_out[i]), for the prefill GEMM; one launch.
+hipError_t launch_tl1_to_i2s(const void* const* packed, const int* N, void* const* i2s_out, int count, int K,
+                             hipStream_t stream);
 constexpr int kElutMaxTokens = 8;     // tokens per ELUT launch
 int tl2_elut_waves(int M);
 size_t tl2_elut_lds_bytes(int M);
@@ -204,5 +253,27 @@ hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* cons
                              hipStream_t stream);
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                              int32_t* x_rowsum, hipStream_t stream);
+
+// A chain of one-token fused GEMVs in one persistent launch.  The plan is a ChainHeader followed by n_links
+// ChainLinks, built on the host and copied to the device by the caller.
+constexpr uint32_t kChainMagic = 0xB17C4A1Du;
+constexpr int kChainSpinLimit = 1 << 22;        // polls of one wait before a work group gives up
+struct ChainHeader {
+    uint32_t magic;
+    int n_links;
+    int max_k;
+    int layout;
+    int reserved[12];
+};
+struct ChainLink {
+    FusedLinears L;
+    const float* x;
+    int8_t* xq;
+    float* x_scale;
+    int32_t* x_rowsum;
+    int K;
+    int reserved[3];
+};
+hipError_t launch_chain(const void* plan, int n_links, int max_k, int fmt, void* ws, hipStream_t stream);
 
 }  // namespace bitnet

@@ -61,7 +61,7 @@ __device__ __forceinline__ uint32_t block_word(const v4u& w, int j, int T, int l
     return i == 0 ? w.x : i == 1 ? w.y : i == 2 ? w.z : w.w;
 }
 
-template <int WAVES, int U, bool HAS_RS>
+template <int WAVES, int U, bool HAS_RS, int FMT>
 __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, const int8_t* __restrict__ xq,
                                                                 const float* __restrict__ x_scale,
                                                                 const int32_t* __restrict__ x_rowsum, int M, int K) {
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int k = min(kb * kI2sBlockK + kSubK * j, K - kSubK);   // past a short block: any real k
-                av[u][j] = *reinterpret_cast<const v4i*>(arow + k);
+                av[u][j] = order_a<FMT>(*reinterpret_cast<const v4i*>(arow + k));
             }
         }
 #pragma unroll
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     if (j < T) {
-                        acc = mfma16x16x64(av[u][j], unpack_codes(block_word(wv[u], j, T, lane)), acc);
+                        acc = mfma16x16x64(av[u][j], decode_b<FMT>(block_word(wv[u], j, T, lane)), acc);
                         if (!HAS_RS) rowsum = mfma16x16x64(av[u][j], ones, rowsum);
                     }
                 }
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
 // them.  The work group then walks row groups as the single-token kernel does, two batches of weights in flight.
 // HAS_ACC: some weight of the launch also stores its int32 sums (the parity hook); the other instance holds no
 // code for them (2% of the eight-token step).
-template <int WAVES, int U, int MG, bool HAS_RS, bool HAS_ACC>
+template <int WAVES, int U, int MG, bool HAS_RS, bool HAS_ACC, int FMT>
 __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLinears L, const int8_t* __restrict__ xq,
                                                                        const float* __restrict__ x_scale,
                                                                        const int32_t* __restrict__ x_rowsum, int M,
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
                 const int m = 4 * mg + (lane >> 4);
                 const int k = (wave + WAVES * u) * kI2sBlockK + 16 * c16;
                 if (m < M && k < K) {
-                    *reinterpret_cast<v4i*>(xs + m * stride + k) = ast[u][mg];
+                    *reinterpret_cast<v4i*>(xs + m * stride + k) = order_a<FMT>(ast[u][mg]);
                     if (!HAS_RS) {
                         const v4i a4 = ast[u][mg];
                         tp[mg] = byte_sum4((uint32_t)a4.x, byte_sum4((uint32_t)a4.y,
@@ -262,7 +262,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
             if (kb < nfull) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(word_of(w[u], j)),
+                    acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), decode_b<FMT>(word_of(w[u], j)),
                                        acc);
             } else if (kb < nkb) {
 #pragma unroll
@@ -270,7 +270,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
                     if (j < Tlast) {
                         const int i = j + sh_tail;
                         const uint32_t wd = i == 0 ? w[u].x : i == 1 ? w[u].y : i == 2 ? w[u].z : w[u].w;
-                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(wd), acc);
+                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), decode_b<FMT>(wd), acc);
                     }
                 }
             }
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
 // never waits for the arithmetic.  The last batch of a row group reduces the waves' partial sums through LDS
 // (double-buffered, one barrier) and applies the epilogue.  Every A row holds the token's codes (LDS broadcast
 // reads, no lane masking); D row 0 is the one stored.
-template <int WAVES, int U, int XV>
+template <int WAVES, int U, int XV, int FMT>
 __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinears L, const float* __restrict__ x,
                                                                       int K, int8_t* __restrict__ xq_out,
                                                                       float* __restrict__ s_out,
@@ -442,7 +442,14 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
             if (e < K4) {
                 const uint32_t c = quant4(xv[i], sx);
                 sum = byte_sum4(c, sum);
-                reinterpret_cast<uint32_t*>(xs)[e] = c;
+                uint32_t cs = c;
+                if constexpr (FMT == kFmtTl1) {
+                    // the 16 codes of k = 16 (e / 4) .. + 15 in tl1_codes' order: word e % 4 of the group takes
+                    // bytes of its own word and of its neighbour e ^ 1 (the next lane of the same quad)
+                    const uint32_t nb = (uint32_t)dpp_row_step((int)c, 0);
+                    cs = (e & 1) ? __builtin_amdgcn_perm(c, nb, 0x07050301u) : __builtin_amdgcn_perm(nb, c, 0x06040200u);
+                }
+                reinterpret_cast<uint32_t*>(xs)[e] = cs;
                 if (bid == 0) reinterpret_cast<uint32_t*>(xq_out)[e] = c;
             }
         }
@@ -473,15 +480,15 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
                 if (kb < nfull) {
     #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(word_of(w[u], j)),
-                                           acc);
+                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j),
+                                           decode_b<FMT>(word_of(w[u], j)), acc);
                 } else if (kb < nkb) {
     #pragma unroll
                     for (int j = 0; j < 3; ++j) {
                         if (j < Tlast) {
                             const int i = j + sh_tail;
                             const uint32_t wd = i == 0 ? w[u].x : i == 1 ? w[u].y : i == 2 ? w[u].z : w[u].w;
-                            acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), unpack_codes(wd), acc);
+                            acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), decode_b<FMT>(wd), acc);
                         }
                     }
                 }
@@ -537,31 +544,32 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
     else run(std::true_type{});
 }
 
-template <int WAVES, int U>
+template <int FMT, int WAVES, int U>
 void launch_plain(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int M, int K,
                   hipStream_t stream) {
     const dim3 grid((unsigned)L.total), block(64 * WAVES);
     if (x_rowsum)
-        hipLaunchKernelGGL((i2s_decode_kernel<WAVES, U, true>), grid, block, 0, stream, L, xq, x_scale, x_rowsum, M, K);
+        hipLaunchKernelGGL((i2s_decode_kernel<WAVES, U, true, FMT>), grid, block, 0, stream, L, xq, x_scale, x_rowsum,
+                           M, K);
     else
-        hipLaunchKernelGGL((i2s_decode_kernel<WAVES, U, false>), grid, block, 0, stream, L, xq, x_scale, x_rowsum, M,
-                           K);
+        hipLaunchKernelGGL((i2s_decode_kernel<WAVES, U, false, FMT>), grid, block, 0, stream, L, xq, x_scale, x_rowsum,
+                           M, K);
 }
 
-template <int WAVES>
+template <int FMT, int WAVES>
 void launch_plain_u(int U, const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                     int M, int K, hipStream_t stream) {
-    if (U <= 1) launch_plain<WAVES, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-    else if (U <= 2) launch_plain<WAVES, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-    else launch_plain<WAVES, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (U <= 1) launch_plain<FMT, WAVES, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+    else if (U <= 2) launch_plain<FMT, WAVES, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+    else launch_plain<FMT, WAVES, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
 }
 
 constexpr int64_t kDecodeStageBytes = 128 * 1024;   // LDS for the tokens' codes in the multi-token stream
 
-template <int WAVES, int U, int XV>
+template <int FMT, int WAVES, int U, int XV>
 hipError_t launch_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
                          hipStream_t stream) {
-    auto kern = i2s_gemv1_stream_kernel<WAVES, U, XV>;
+    auto kern = i2s_gemv1_stream_kernel<WAVES, U, XV, FMT>;
     const size_t lds = (size_t)K;
     // as many work groups as fit on the chip at once, balanced so that every one walks the same number of
     // row groups (to within one)
@@ -577,24 +585,24 @@ hipError_t launch_stream(const FusedLinears& L, const float* x, int K, int8_t* x
     return hipGetLastError();
 }
 
-template <int WAVES, int U>
+template <int FMT, int WAVES, int U>
 hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
                             hipStream_t stream) {
     const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
-    if (xv <= 1) return launch_stream<WAVES, U, 1>(L, x, K, xq, s, rs, stream);
-    if (xv <= 2) return launch_stream<WAVES, U, 2>(L, x, K, xq, s, rs, stream);
-    if (WAVES < 16 || xv <= 4) return launch_stream<WAVES, U, 4>(L, x, K, xq, s, rs, stream);
-    if (xv <= 8) return launch_stream<WAVES, U, 8>(L, x, K, xq, s, rs, stream);
-    return launch_stream<WAVES, U, 16>(L, x, K, xq, s, rs, stream);
+    if (xv <= 1) return launch_stream<FMT, WAVES, U, 1>(L, x, K, xq, s, rs, stream);
+    if (xv <= 2) return launch_stream<FMT, WAVES, U, 2>(L, x, K, xq, s, rs, stream);
+    if (WAVES < 16 || xv <= 4) return launch_stream<FMT, WAVES, U, 4>(L, x, K, xq, s, rs, stream);
+    if (xv <= 8) return launch_stream<FMT, WAVES, U, 8>(L, x, K, xq, s, rs, stream);
+    return launch_stream<FMT, WAVES, U, 16>(L, x, K, xq, s, rs, stream);
 }
 
-template <int W, int U, int MG>
+template <int FMT, int W, int U, int MG>
 hipError_t launch_mstream(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                           int M, int K, hipStream_t stream) {
     bool has_acc = false;
     for (int i = 0; i < L.count; ++i) has_acc = has_acc || L.acc[i] != nullptr;
-    const void* kern = has_acc ? reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, true>)
-                               : reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, false>);
+    const void* kern = has_acc ? reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, true, FMT>)
+                               : reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, false, FMT>);
     const size_t lds = (size_t)M * (K + 16);
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * W, lds) != hipSuccess || occ <= 0) occ = 1;
@@ -602,21 +610,21 @@ hipError_t launch_mstream(const FusedLinears& L, const int8_t* xq, const float* 
     const int64_t rounds = (L.total + max_g - 1) / max_g;
     const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * W);
     if (has_acc)
-        hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, true>), grid, block, lds, stream, L, xq, x_scale,
-                           x_rowsum, M, K);
+        hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, true, FMT>), grid, block, lds, stream, L, xq,
+                           x_scale, x_rowsum, M, K);
     else
-        hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, false>), grid, block, lds, stream, L, xq, x_scale,
-                           x_rowsum, M, K);
+        hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, false, FMT>), grid, block, lds, stream, L, xq,
+                           x_scale, x_rowsum, M, K);
     return hipGetLastError();
 }
 
-template <int W, int U>
+template <int FMT, int W, int U>
 hipError_t launch_mstream_m(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                             int M, int K, hipStream_t stream) {
-    if (M <= 4) return launch_mstream<W, U, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-    if (M <= 8) return launch_mstream<W, U, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-    if (M <= 12) return launch_mstream<W, U, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
-    return launch_mstream<W, U, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 4) return launch_mstream<FMT, W, U, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 8) return launch_mstream<FMT, W, U, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+    if (M <= 12) return launch_mstream<FMT, W, U, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
+    return launch_mstream<FMT, W, U, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
 }
 
 }  // namespace
@@ -649,7 +657,8 @@ void decode_shape(int64_t groups, int64_t K, int max_u, int min_waves, int& wave
     if (u > max_u) u = max_u;
 }
 
-hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
+template <int FMT>
+hipError_t launch_decode_fmt(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                              int M, int K, hipStream_t stream) {
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int cus = device_cus();
@@ -658,51 +667,64 @@ hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const floa
         // 4-wave work groups (K <= 4096) where the launch has more row groups than half the CUs: each group stages
         // the codes once as the 16-wave groups do, without waiting on the slowest of 16 waves at each barrier
         const int u4 = (nkb + 3) / 4;
-        if (u4 <= 1) return launch_mstream_m<4, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u4 <= 2) return launch_mstream_m<4, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u4 <= 3) return launch_mstream_m<4, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
-        return launch_mstream_m<4, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u4 <= 1) return launch_mstream_m<FMT, 4, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u4 <= 2) return launch_mstream_m<FMT, 4, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u4 <= 3) return launch_mstream_m<FMT, 4, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
+        return launch_mstream_m<FMT, 4, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
     }
     if (x_rowsum && fits && nkb <= 64) {
         // 16-wave work groups, all of a row group's blocks in one batch; past what fits on the chip they stream
         const int u16 = (nkb + 15) / 16;
-        if (u16 <= 1) return launch_mstream_m<16, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u16 <= 2) return launch_mstream_m<16, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u16 <= 3) return launch_mstream_m<16, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
-        return launch_mstream_m<16, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 1) return launch_mstream_m<FMT, 16, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 2) return launch_mstream_m<FMT, 16, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 3) return launch_mstream_m<FMT, 16, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
+        return launch_mstream_m<FMT, 16, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
     }
     int waves, u;
     decode_shape(L.total, K, 4, 4, waves, u);
     switch (waves) {
-        case 4: launch_plain_u<4>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
-        case 8: launch_plain_u<8>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
-        default: launch_plain_u<16>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
+        case 4: launch_plain_u<FMT, 4>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
+        case 8: launch_plain_u<FMT, 8>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
+        default: launch_plain_u<FMT, 16>(u, L, xq, x_scale, x_rowsum, M, K, stream); break;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
-                                   int32_t* x_rowsum, hipStream_t stream) {
+template <int FMT>
+hipError_t launch_gemv1_fmt(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                            int32_t* x_rowsum, hipStream_t stream) {
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int cus = device_cus();
     if (L.total > cus / 2 && L.total <= 8 * cus && nkb <= 16) {
         // every row group in flight at once: one per 4-wave work group, from half a group per CU up to eight per
         // CU (a 16-wave group waits on its slowest wave at the quantisation and at the reduction)
         const int u = (nkb + 3) / 4;
-        if (u <= 1) return launch_stream_xv<4, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
-        if (u <= 2) return launch_stream_xv<4, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
-        if (u <= 3) return launch_stream_xv<4, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
-        return launch_stream_xv<4, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
+        if (u <= 1) return launch_stream_xv<FMT, 4, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+        if (u <= 2) return launch_stream_xv<FMT, 4, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
+        if (u <= 3) return launch_stream_xv<FMT, 4, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+        return launch_stream_xv<FMT, 4, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
     }
     // 16-wave work groups, up to four 256-k blocks per wave per batch, the batches of a row group balanced;
     // past what fits on the chip at once the work groups stream
     constexpr int kWaves = 16;
     const int nb = (nkb + 4 * kWaves - 1) / (4 * kWaves);
     const int u = (nkb + kWaves * nb - 1) / (kWaves * nb);
-    if (u <= 1) return launch_stream_xv<kWaves, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
-    if (u <= 2) return launch_stream_xv<kWaves, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
-    if (u <= 3) return launch_stream_xv<kWaves, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
-    return launch_stream_xv<kWaves, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (u <= 1) return launch_stream_xv<FMT, kWaves, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (u <= 2) return launch_stream_xv<FMT, kWaves, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (u <= 3) return launch_stream_xv<FMT, kWaves, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+    return launch_stream_xv<FMT, kWaves, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
+}
+
+hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
+                             int M, int K, hipStream_t stream, int fmt) {
+    return fmt == kFmtTl1 ? launch_decode_fmt<kFmtTl1>(L, xq, x_scale, x_rowsum, M, K, stream)
+                          : launch_decode_fmt<kFmtI2s>(L, xq, x_scale, x_rowsum, M, K, stream);
+}
+
+hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                                   int32_t* x_rowsum, hipStream_t stream, int fmt) {
+    return fmt == kFmtTl1 ? launch_gemv1_fmt<kFmtTl1>(L, x, K, xq, x_scale, x_rowsum, stream)
+                          : launch_gemv1_fmt<kFmtI2s>(L, x, K, xq, x_scale, x_rowsum, stream);
 }
 
 }  // namespace bitnet

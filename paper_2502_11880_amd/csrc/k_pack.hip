@@ -155,6 +155,60 @@ __global__ __launch_bounds__(256) void pack_i2s_words(const float* __restrict__ 
     out[d] = word;
 }
 
+// TL1 (Algorithm TL1, Table 5): the I2_S tiling, one thread per 32-bit word = 8 pair codes (16 weights) of one row;
+// pair i (weights k0 + 2i, k0 + 2i + 1) in byte i % 4, low nibble for i < 4, high nibble for i >= 4.
+__global__ __launch_bounds__(256) void pack_tl1_words(const float* __restrict__ W, int K, size_t nwords,
+                                                      const float* __restrict__ beta_p,
+                                                      uint32_t* __restrict__ out) {
+    const size_t d = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (d >= nwords) return;
+    const float beta = *beta_p;
+    const size_t R = d / (size_t)K;                   // a row group holds K words (4K bytes)
+    const int rem = (int)(d - R * (size_t)K);
+    const int s = rem >> 8;                           // 1 KiB blocks of 256 words
+    const int w = rem & 255;
+    const int nsub = K / kSubK;
+    const int T = min(4, nsub - 4 * s);
+    const int l = w / T, j = w - l * T;
+    const int r = l & 15, q = l >> 4;
+    const size_t n = R * kRowsPerGroup + r;
+    const int k0 = kSubK * (4 * s + j) + 16 * q;
+    const float2* src = reinterpret_cast<const float2*>(W + n * (size_t)K + k0);
+    uint32_t word = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float2 v = src[i];
+        const uint32_t c = (uint32_t)(3 * (ternary(v.x, beta) + 1) + (ternary(v.y, beta) + 1));
+        word |= c << (8 * (i & 3) + 4 * (i >> 2));
+    }
+    out[d] = word;
+}
+
+// TL1 words rewritten as I2_S words at the same positions (both formats tile a word as 16 weights of one row):
+// weight e of the word is pair e / 2, code c: t + 1 = c / 3 for even e, c % 3 for odd e; it goes to byte e % 4,
+// bits 2 (e / 4).  blockIdx.y is the weight.
+struct Tl1Transcode {
+    const uint32_t* src[kMaxFused];
+    uint32_t* dst[kMaxFused];
+    size_t nwords[kMaxFused];
+};
+
+__global__ __launch_bounds__(256) void tl1_to_i2s_words(Tl1Transcode T) {
+    const int li = blockIdx.y;
+    const size_t d = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (d >= T.nwords[li]) return;
+    const uint32_t w = T.src[li][d];
+    uint32_t o = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int i = e >> 1;
+        const uint32_t c = (w >> (8 * (i & 3) + 4 * (i >> 2))) & 0xFu;
+        const uint32_t code = (e & 1) ? c % 3u : c / 3u;
+        o |= code << (8 * (e & 3) + 2 * (e >> 2));
+    }
+    T.dst[li][d] = o;
+}
+
 // TL2 part: one thread per lane chunk = 32 triples (96 weights) of one row in one 384-k block.
 __global__ __launch_bounds__(256) void pack_tl2_chunks(const float* __restrict__ W, int K, int nblk,
                                                        size_t nchunks, const float* __restrict__ beta_p,
@@ -229,6 +283,10 @@ hipError_t launch_pack(int layout, const float* W, int64_t N, int64_t K, void* p
         const size_t nwords = n / 16;
         hipLaunchKernelGGL(pack_i2s_words, dim3(grid_for(nwords, 256)), dim3(256), 0, stream, W, (int)K,
                            nwords, w_scale, static_cast<uint32_t*>(packed));
+    } else if (layout == 2) {
+        const size_t nwords = n / 16;
+        hipLaunchKernelGGL(pack_tl1_words, dim3(grid_for(nwords, 256)), dim3(256), 0, stream, W, (int)K,
+                           nwords, w_scale, static_cast<uint32_t*>(packed));
     } else {
         const int three = (int)(K / kTl2BlockK) * kTl2BlockK;
         const int two = (int)K - three;
@@ -249,6 +307,20 @@ hipError_t launch_pack(int layout, const float* W, int64_t N, int64_t K, void* p
                                three, units, nwords, w_scale, tail);
         }
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_tl1_to_i2s(const void* const* packed, const int* N, void* const* i2s_out, int count, int K,
+                             hipStream_t stream) {
+    Tl1Transcode T{};
+    size_t most = 0;
+    for (int i = 0; i < count; ++i) {
+        T.src[i] = static_cast<const uint32_t*>(packed[i]);
+        T.dst[i] = static_cast<uint32_t*>(i2s_out[i]);
+        T.nwords[i] = (size_t)N[i] * (size_t)K / 16;
+        most = T.nwords[i] > most ? T.nwords[i] : most;
+    }
+    hipLaunchKernelGGL(tl1_to_i2s_words, dim3(grid_for(most, 256), (unsigned)count), dim3(256), 0, stream, T);
     return hipGetLastError();
 }
 

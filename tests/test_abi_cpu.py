@@ -34,10 +34,11 @@ def test_library_exports_every_declared_symbol():
 def test_packed_bytes_match_layout_definitions(N, K):
     assert B.bitnet_packed_bytes("i2s", N, K) == O.i2s_packed_bytes(N, K)
     assert B.bitnet_packed_bytes("tl2", N, K) == O.tl2_packed_bytes(N, K)
+    assert B.bitnet_packed_bytes("tl1", N, K) == O.tl1_packed_bytes(N, K)
 
 
 def test_packed_bytes_rejects_bad_shapes():
-    for layout in ("i2s", "tl2"):
+    for layout in ("i2s", "tl2", "tl1"):
         assert B.bitnet_packed_bytes(layout, 15, 64) == 0
         assert B.bitnet_packed_bytes(layout, 16, 65) == 0
         assert B.bitnet_packed_bytes(layout, 0, 64) == 0

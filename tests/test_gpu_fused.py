@@ -110,8 +110,9 @@ def test_fused_tl2(M, K, Ns):
 
 
 # One token through the fused call (one launch that also quantises) on the exact linear groups the benchmark times,
-# and one shape for each remaining instance of the single-token streaming kernel.  Instance (waves, 256-k blocks
-# per wave per batch, float4 of the row per thread) that each shape selects on a 256-CU MI355X, I2_S:
+# and one shape for each remaining instance of the single-token streaming kernel, in the three layouts (TL1 runs the
+# same instances as I2_S).  Instance (waves, 256-k blocks per wave per batch, float4 of the row per thread) that
+# each shape selects on a 256-CU MI355X, I2_S and TL1:
 ONE_TOKEN_GROUPS = [
     (1536, [4096]),                  # the 1536 x 4096 linear: <4, 2, 2>
     (3200, [3200]),                  # 3B-class o: <4, 4, 4>
@@ -130,10 +131,10 @@ ONE_TOKEN_GROUPS = [
 @pytest.mark.parametrize("K,Ns", ONE_TOKEN_GROUPS)
 def test_fused_one_token_workload_groups(K, Ns):
     _announce("fused one token", K, Ns)
-    _fused_case(("i2s", "tl2"), 1, K, Ns, seed=inputs.seed_for(2, 3000 + K + len(Ns)))
+    _fused_case(("i2s", "tl2", "tl1"), 1, K, Ns, seed=inputs.seed_for(2, 3000 + K + len(Ns)))
 
 
-# The 100B-class layer's groups at one token (the launches of the stack benchmark), both layouts.  I2_S: q/k/v
+# The 100B-class layer's groups at one token (the launches of the stack benchmark), every layout.  I2_S and TL1: q/k/v
 # (2304 row groups: 256 work groups of <16, 3, 4> walking nine row groups each), o and down (768 row groups:
 # three per work group; down <16, 3, 16> with three batches per row group), gate/up (4128 row groups).  TL2:
 # q/k/v, o and gate/up on the MFMA expansion with the row quantised inside; down (K = 33024, 86 blocks) through
@@ -142,4 +143,4 @@ def test_fused_one_token_workload_groups(K, Ns):
                                   (33024, [12288])])
 def test_fused_one_token_100b_groups(K, Ns):
     _announce("fused one token 100B-class", K, Ns)
-    _fused_case(("i2s", "tl2"), 1, K, Ns, seed=inputs.seed_for(4, 10 * len(Ns) + K % 7))
+    _fused_case(("i2s", "tl2", "tl1"), 1, K, Ns, seed=inputs.seed_for(4, 10 * len(Ns) + K % 7))

@@ -35,7 +35,8 @@ def _call_pair(layout, M, N, K, seed):
 # I2_S prefill with K split across work groups (the int32 slices in the scratch), then a smaller one; TL2 prefill
 # (weights rewritten in the I2_S layout in the scratch), then a smaller one.
 @pytest.mark.parametrize("layout,shapes", [("i2s", [(64, 1024, 4096), (40, 256, 1536)]),
-                                           ("tl2", [(300, 2048, 4096), (33, 256, 832)])])
+                                           ("tl2", [(300, 2048, 4096), (33, 256, 832)]),
+                                           ("tl1", [(300, 2048, 4096), (33, 256, 832)])])
 def test_noalloc_matches_mpgemm_twice(layout, shapes):
     for i, (M, N, K) in enumerate(shapes):
         _call_pair(layout, M, N, K, seed=inputs.seed_for(9, 40 * i + M + N + K))
