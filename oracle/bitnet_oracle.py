@@ -25,6 +25,9 @@ What it computes, with the part of the paper each step follows:
 * ``elut_tables`` / ``elut_gemm`` -- Eq. 3 / Algorithm "ELUT mpGEMM" with mirror consolidation
   (Sec. 3.1.1) and the 1-bit sign operation of Eq. 5: an independent second route to the same integers;
   ``tl1_tables`` / ``elut_gemm_tl1`` the same for the TL1 format (Algorithm TL1: 9-entry pair tables).
+* ``elut_*`` / ``pack_elut`` -- the ELUT method for integer weights of other cardinalities (Appendix "Insight",
+  Table 3, Algorithm "ELUT mpGEMM"): group codes, tables of the C^g sums (mirrored for symmetric sets) and the
+  packed formats c4g2, c5g2 and c3g5.
 * ``epilogue`` -- y = acc * beta / s_m in float64 (the dequantisation the quantisers above imply).
 
 All floating-point decisions that produce integers (the weight divide and round, the activation multiply
@@ -520,6 +523,176 @@ def elut_gemm_tl1(xq: np.ndarray, packed_tl1: np.ndarray, N: int, K: int) -> np.
         vals = np.take_along_axis(lut[m][None, :, :], code[:, :, None], axis=2)[..., 0]   # [N, K/2]
         acc[m] = vals.sum(axis=1)
     return acc.astype(np.int32)
+
+
+# ----------------------------------------------------------------------------------------------
+# ELUT beyond ternary weights (Appendix "Insight", Table 3, Algorithm "ELUT mpGEMM", Eq. 3 and Eq. 4):
+# integer weights from a set of C values, one table of the C^g sums per group of g weights
+# ----------------------------------------------------------------------------------------------
+# Formats: name -> (C, g, mirror).  C = 4 with g = 2 and C = 5 with g = 2 are rows of Table 3; C = 3 with g = 5 is
+# a group too long for a 16-entry register table (the register-length analysis of the appendix) whose 122-entry
+# mirrored table lives in GPU LDS.
+ELUT_FORMATS = {"c4g2": (4, 2, False), "c5g2": (5, 2, True), "c3g5": (3, 5, True)}
+
+
+def elut_values(C: int) -> np.ndarray:
+    """The weight set of cardinality C: the C consecutive integers -floor(C/2) .. C - 1 - floor(C/2)
+    ({-1, 0, 1} for C = 3, the two's-complement {-2, -1, 0, 1} for C = 4, {-2, .., 2} for C = 5)."""
+    return np.arange(-(C // 2), C - C // 2, dtype=np.int64)
+
+
+def elut_entries(C: int, g: int, mirror: bool) -> int:
+    """Table length: C^g, or the non-negative half (C^g + 1) / 2 with mirror consolidation (odd C only)."""
+    if mirror and C % 2 == 0:
+        raise ValueError("mirror consolidation needs a weight set symmetric about 0 (odd C)")
+    return (C ** g + 1) // 2 if mirror else C ** g
+
+
+def elut_bits(C: int, g: int, mirror: bool) -> int:
+    """Bits per group: the index of an entry, plus the sign bit with mirror consolidation."""
+    return math.ceil(math.log2(elut_entries(C, g, mirror))) + (1 if mirror else 0)
+
+
+def elut_entry_weights(C: int, g: int, mirror: bool) -> np.ndarray:
+    """[E, g] weights of table entry e: without mirroring the base-C digits of e (first weight most significant)
+    offset by the set's minimum; with mirroring the balanced base-C digits of e (so entry e is the group whose value
+    sum_j w_j C^(g-1-j) equals e)."""
+    E = elut_entries(C, g, mirror)
+    out = np.zeros((E, g), dtype=np.int64)
+    lo = int(elut_values(C)[0])
+    for e in range(E):
+        v = e
+        for j in range(g - 1, -1, -1):
+            if mirror:
+                r = v % C
+                if r > C // 2:
+                    r -= C
+                out[e, j] = r
+                v = (v - r) // C
+            else:
+                out[e, j] = v % C + lo
+                v //= C
+        if v != 0:
+            raise ValueError("entry outside the group's range")
+    return out
+
+
+def elut_group_codes(w: np.ndarray, C: int, g: int, mirror: bool):
+    """(index, sign) of every group of g weights along the rows of w [N, K] (K % g == 0); sign is 0 without
+    mirroring.  Plain: the base-C number of the digits w_j - min.  Mirrored: v = sum_j w_j C^(g-1-j),
+    index |v|, sign [v < 0] (the rule of Table 6 for any odd C)."""
+    w = np.asarray(w, dtype=np.int64)
+    N, K = w.shape
+    if K % g:
+        raise ValueError("K must be a multiple of the group size")
+    vals = elut_values(C)
+    if w.min(initial=0) < vals[0] or w.max(initial=0) > vals[-1]:
+        raise ValueError("weights outside the set")
+    grp = w.reshape(N, K // g, g)
+    if mirror:
+        v = np.zeros(grp.shape[:2], dtype=np.int64)
+        for j in range(g):
+            v = v * C + grp[..., j]
+        return np.abs(v), (v < 0).astype(np.int64)
+    code = np.zeros(grp.shape[:2], dtype=np.int64)
+    for j in range(g):
+        code = code * C + (grp[..., j] - vals[0])
+    return code, np.zeros_like(code)
+
+
+def elut_generic_tables(xq: np.ndarray, C: int, g: int, mirror: bool) -> np.ndarray:
+    """Table-setup step: lut[m, j, e] = sum_i d_i(e) * xq[m, g j + i] over the entry weights d(e)."""
+    a = np.asarray(xq, dtype=np.int64)
+    M, K = a.shape
+    d = elut_entry_weights(C, g, mirror)                 # [E, g]
+    grp = a.reshape(M, K // g, g)
+    return np.einsum("mjg,eg->mje", grp, d)
+
+
+def elut_generic_gemm(xq: np.ndarray, idx: np.ndarray, sign: np.ndarray, C: int, g: int, mirror: bool) -> np.ndarray:
+    """acc[m, n] = sum over the groups of row n of the looked-up entry, negated where the group's sign is set
+    (Eq. 5 with the sign widened to a mask).  Shares nothing with ``mad_gemm``."""
+    lut = elut_generic_tables(xq, C, g, mirror)          # [M, G, E]
+    M = lut.shape[0]
+    N = idx.shape[0]
+    acc = np.zeros((M, N), dtype=np.int64)
+    for m in range(M):
+        vals = np.take_along_axis(lut[m][None, :, :], idx[:, :, None], axis=2)[..., 0]   # [N, G]
+        acc[m] = sign_op(vals, sign).sum(axis=1)
+    return acc
+
+
+def elut_layout_check(fmt: str, N: int, K: int) -> None:
+    C, g, _ = ELUT_FORMATS[fmt]
+    step = 320 if g == 5 else 64
+    if N <= 0 or K <= 0 or N % 16 or K % step:
+        raise ValueError(f"{fmt} needs N % 16 == 0 and K % {step} == 0")
+
+
+def elut_packed_bytes(fmt: str, N: int, K: int) -> int:
+    """c4g2: a 4-bit code per pair (N K / 4 bytes); c5g2: a 4-bit index plane (N K / 4) then a sign plane of one
+    bit per pair (N K / 16); c3g5: one byte per group of five (index in bits 0-6, sign in bit 7; N K / 5)."""
+    elut_layout_check(fmt, N, K)
+    return {"c4g2": N * K // 4, "c5g2": N * K // 4 + N * K // 16, "c3g5": N * K // 5}[fmt]
+
+
+def elut_group_position(fmt: str, n, j, N: int, K: int):
+    """(byte, shift) of the index field of group j of row n, and (byte, bit) of its sign (-1 where the sign
+    shares the index byte or does not exist).  Rows are row-major in each plane; in the 4-bit planes group j
+    sits in byte j // 2, low nibble first."""
+    n = np.asarray(n, dtype=np.int64)
+    j = np.asarray(j, dtype=np.int64)
+    C, g, mirror = ELUT_FORMATS[fmt]
+    none = np.full(np.broadcast(n, j).shape, -1, dtype=np.int64)
+    if fmt == "c3g5":
+        return n * (K // 5) + j, np.zeros_like(none), none, none
+    ib, ish = n * (K // 4) + j // 2, 4 * (j % 2)
+    if fmt == "c5g2":
+        return ib, ish, N * K // 4 + n * (K // 16) + j // 8, j % 8
+    return ib, ish, none, none
+
+
+def pack_elut(w: np.ndarray, fmt: str) -> np.ndarray:
+    w = np.asarray(w)
+    N, K = w.shape
+    elut_layout_check(fmt, N, K)
+    C, g, mirror = ELUT_FORMATS[fmt]
+    idx, sign = elut_group_codes(w, C, g, mirror)
+    out = np.zeros(elut_packed_bytes(fmt, N, K), dtype=np.uint8)
+    nn, jj = np.meshgrid(np.arange(N), np.arange(K // g), indexing="ij")
+    ib, ish, sb, sbit = elut_group_position(fmt, nn, jj, N, K)
+    field = idx | (sign << 7) if fmt == "c3g5" else idx
+    np.bitwise_or.at(out, ib.ravel(), (field << ish).ravel().astype(np.uint8))
+    if fmt == "c5g2":
+        np.bitwise_or.at(out, sb.ravel(), (sign << sbit).ravel().astype(np.uint8))
+    return out
+
+
+def elut_decode_codes(packed: np.ndarray, fmt: str, N: int, K: int):
+    """(index, sign) of every group, [N, K / g] each, read back from a packed buffer."""
+    packed = np.asarray(packed, dtype=np.uint8)
+    if packed.size != elut_packed_bytes(fmt, N, K):
+        raise ValueError("buffer has the wrong size")
+    C, g, mirror = ELUT_FORMATS[fmt]
+    nn, jj = np.meshgrid(np.arange(N), np.arange(K // g), indexing="ij")
+    ib, ish, sb, sbit = elut_group_position(fmt, nn, jj, N, K)
+    if fmt == "c3g5":
+        byte = packed[ib].astype(np.int64)
+        return byte & 0x7F, byte >> 7
+    idx = (packed[ib].astype(np.int64) >> ish) & 0xF
+    sign = (packed[sb].astype(np.int64) >> sbit) & 1 if fmt == "c5g2" else np.zeros_like(idx)
+    return idx, sign
+
+
+def unpack_elut(packed: np.ndarray, fmt: str, N: int, K: int) -> np.ndarray:
+    C, g, mirror = ELUT_FORMATS[fmt]
+    idx, sign = elut_decode_codes(packed, fmt, N, K)
+    E = elut_entries(C, g, mirror)
+    if np.any(idx >= E) or (mirror and np.any((idx == 0) & (sign == 1))):
+        raise ValueError("invalid group code")
+    d = elut_entry_weights(C, g, mirror)
+    grp = d[idx] * np.where(sign == 1, -1, 1)[..., None]
+    return grp.reshape(N, K).astype(np.int8)
 
 
 # ----------------------------------------------------------------------------------------------

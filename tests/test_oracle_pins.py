@@ -436,3 +436,88 @@ def test_reference_path_small():
     # y approximates x @ W.T up to the quantisation error of both operands
     dense = x.astype(np.float64) @ (t.astype(np.float64) * float(beta)).T
     assert np.allclose(y, dense, rtol=0.05, atol=0.05 * np.abs(dense).max())
+
+
+# ---------------------------------------------------------------------------------------------
+# ELUT for other weight cardinalities (Appendix "Insight", Table 3)
+# ---------------------------------------------------------------------------------------------
+def test_elut_formats_bits_per_weight_match_table3():
+    # Table 3 rows: (C, g, bpw_b, bpw_e) = (3, 3, 2, 1.67), (4, 2, 2, 2), (5, 2, 3, 2.5)
+    for C, g, mirror, bpw_b, bpw_e in [(3, 3, True, 2, 1.67), (4, 2, False, 2, 2.0), (5, 2, True, 3, 2.5)]:
+        assert math.ceil(math.log2(C)) == bpw_b
+        assert round(O.elut_bits(C, g, mirror) / g, 2) == bpw_e
+    # the formats built beyond Table 3's rows: C = 3 with g = 5 fits a byte per group (1.6 bits per weight)
+    assert O.elut_bits(3, 5, True) / 5 == 1.6 and O.elut_entries(3, 5, True) == 122
+    assert O.elut_entries(4, 2, False) == 16 and O.elut_entries(5, 2, True) == 13
+    for fmt, (C, g, mirror) in O.ELUT_FORMATS.items():
+        N, K = 16, 640
+        assert O.elut_packed_bytes(fmt, N, K) * 8 == N * K * O.elut_bits(C, g, mirror) // g
+
+
+def test_elut_generic_reduces_to_tl1_and_tl2_codes():
+    # C = 3: g = 3 mirrored is Table 6 (TL2), g = 2 plain is Table 5 (TL1)
+    d3 = O.elut_entry_weights(3, 3, True)
+    assert [tuple(int(v) for v in r) for r in d3] == [O.balanced_ternary_digits(i) for i in range(14)]
+    for t in itertools.product((-1, 0, 1), repeat=3):
+        idx, sign = O.elut_group_codes(np.array([t]), 3, 3, True)
+        ref = O.tl2_codes(*t)
+        assert (int(idx[0, 0]), int(sign[0, 0])) == (int(ref[0]), int(ref[1]))
+    for row in _rows("tl1_table5.txt"):
+        t0, t1, code = int(row[0]), int(row[1]), int(row[2], 2)
+        idx, sign = O.elut_group_codes(np.array([[t0, t1]]), 3, 2, False)
+        assert int(idx[0, 0]) == code and int(sign[0, 0]) == 0
+        assert tuple(int(v) for v in O.elut_entry_weights(3, 2, False)[code]) == (t0, t1)
+
+
+@pytest.mark.parametrize("fmt", list(O.ELUT_FORMATS))
+def test_elut_tables_enumerate_every_group(fmt):
+    C, g, mirror = O.ELUT_FORMATS[fmt]
+    rng = np.random.default_rng(len(fmt) + C)
+    a = rng.integers(-128, 128, size=g)
+    xq = np.tile(a, (1, 4)).astype(np.int8)                        # one token, four groups of the same codes
+    lut = O.elut_generic_tables(xq, C, g, mirror)
+    vals = [int(v) for v in O.elut_values(C)]
+    seen = set()
+    for grp in itertools.product(vals, repeat=g):
+        idx, sign = O.elut_group_codes(np.array([grp]), C, g, mirror)
+        i, sg = int(idx[0, 0]), int(sign[0, 0])
+        seen.add((i, sg))
+        assert int(O.sign_op(lut[0, 0, i], sg)) == sum(int(x) * w for x, w in zip(a, grp))
+        if mirror and any(grp):
+            neg = O.elut_group_codes(np.array([[-w for w in grp]]), C, g, mirror)
+            assert (int(neg[0][0, 0]), int(neg[1][0, 0])) == (i, 1 - sg)
+    assert len(seen) == C ** g                                      # every group has its own code
+
+
+@pytest.mark.parametrize("fmt", list(O.ELUT_FORMATS))
+@pytest.mark.parametrize("M,N,K", [(1, 16, 640), (3, 32, 1280)])
+def test_elut_generic_equals_mad_and_round_trips(fmt, M, N, K):
+    C, g, mirror = O.ELUT_FORMATS[fmt]
+    rng = np.random.default_rng(M * 7 + N + K + C)
+    w = rng.choice(O.elut_values(C), size=(N, K)).astype(np.int8)
+    w[0] = O.elut_values(C)[0]                                      # extreme rows: every weight the smallest value
+    w[1] = O.elut_values(C)[-1]
+    xq = rng.integers(-128, 128, size=(M, K)).astype(np.int8)
+    xq[0, :] = -128
+    p = O.pack_elut(w, fmt)
+    assert np.array_equal(O.unpack_elut(p, fmt, N, K), w)
+    idx, sign = O.elut_decode_codes(p, fmt, N, K)
+    assert np.array_equal(O.elut_generic_gemm(xq, idx, sign, C, g, mirror), O.mad_gemm(xq, w))
+
+
+def test_elut_positions_hand_computed_and_every_field_once():
+    N, K = 32, 640
+    # c4g2 / c5g2: group j of row n in byte n*K/4 + j//2 (low nibble first); c5g2 signs after N*K/4 bytes, one bit
+    # per group; c3g5: one byte per group at n*K/5 + j
+    assert tuple(int(v) for v in O.elut_group_position("c4g2", 1, 3, N, K)[:2]) == (161, 4)
+    assert tuple(int(v) for v in O.elut_group_position("c5g2", 2, 9, N, K)) == (324, 4, 5120 + 80 + 1, 1)
+    assert int(O.elut_group_position("c3g5", 3, 7, N, K)[0]) == 3 * 128 + 7
+    for fmt, (C, g, mirror) in O.ELUT_FORMATS.items():
+        nn, jj = np.meshgrid(np.arange(N), np.arange(K // g), indexing="ij")
+        ib, ish, sb, sbit = O.elut_group_position(fmt, nn, jj, N, K)
+        width = 8 if fmt == "c3g5" else 4
+        slots = ib.ravel() * (8 // width) + ish.ravel() // width
+        assert np.unique(slots).size == slots.size
+        if fmt == "c5g2":
+            bits = sb.ravel() * 8 + sbit.ravel()
+            assert np.unique(bits).size == bits.size and bits.max() == 8 * O.elut_packed_bytes(fmt, N, K) - 1
