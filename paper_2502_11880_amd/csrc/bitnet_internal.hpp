@@ -254,26 +254,5 @@ hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* cons
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                              int32_t* x_rowsum, hipStream_t stream);
 
-// A chain of one-token fused GEMVs in one persistent launch.  The plan is a ChainHeader followed by n_links
-// ChainLinks, built on the host and copied to the device by the caller.
-constexpr uint32_t kChainMagic = 0xB17C4A1Du;
-constexpr int kChainSpinLimit = 1 << 22;        // polls of one wait before a work group gives up
-struct ChainHeader {
-    uint32_t magic;
-    int n_links;
-    int max_k;
-    int layout;
-    int reserved[12];
-};
-struct ChainLink {
-    FusedLinears L;
-    const float* x;
-    int8_t* xq;
-    float* x_scale;
-    int32_t* x_rowsum;
-    int K;
-    int reserved[3];
-};
-hipError_t launch_chain(const void* plan, int n_links, int max_k, int fmt, void* ws, hipStream_t stream);
 
 }  // namespace bitnet
