@@ -46,7 +46,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", type=int, default=4)
     p.add_argument("--tokens", type=int, default=None)
-    p.add_argument("--layout", default="i2s", choices=["i2s", "tl2", "tl1"])
+    p.add_argument("--layout", default="i2s", choices=["i2s", "tl2", "tl1", "c4g2", "c5g2", "c3g5"])
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-parity", action="store_true")
@@ -57,6 +57,23 @@ def parse():
 def log(msg):
     """A progress line on stderr (the JSON result is the only line on stdout)."""
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+INT_BETA = 0.02                  # per-tensor scale given with the integer-weight layouts' weights
+INT_C = {"c4g2": 4, "c5g2": 5, "c3g5": 3}
+
+
+def int_layout(layout):
+    return layout in INT_C
+
+
+def bench_weight(args, inputs, layout, i, N, K):
+    """The benchmark's weight i: fp32 N(0, 0.02) for the ternary layouts (ternarised by the packer), seeded integers
+    of the layout's set for the integer-weight layouts."""
+    seed = inputs.seed_for(args.workload, i)
+    if int_layout(layout):
+        return inputs.int_weights(N, K, INT_C[layout], seed=seed)
+    return inputs.weight_f32(N, K, seed=seed)
 
 
 def activation_groups(by_name, inputs):
@@ -96,11 +113,19 @@ def main():
     log(f"workload {args.workload} ({spec['name']}), {M} token(s), {layout}: packing {len(linears)} weights")
     packed, scales = {}, {}
     for i, (name, K, N) in enumerate(linears):
-        W = inputs.weight_f32(N, K, seed=inputs.seed_for(args.workload, i)).to(dev)
-        pk = torch.empty(B.bitnet_packed_bytes(layout, N, K), dtype=torch.uint8, device=dev)
-        sc = torch.empty(1, dtype=torch.float32, device=dev)
-        pws = torch.empty(B.bitnet_pack_workspace_bytes(N, K), dtype=torch.uint8, device=dev)
-        B.bitnet_pack_weights(layout, W, pk, sc, pws)
+        W = bench_weight(args, inputs, layout, i, N, K).to(dev)
+        nbytes = B.bitnet_packed_bytes(layout, N, K)
+        if nbytes == 0:
+            print(f"layout {layout} does not take a {N} x {K} weight", file=sys.stderr)
+            sys.exit(2)
+        pk = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        if int_layout(layout):
+            sc = torch.full((1,), INT_BETA, dtype=torch.float32, device=dev)
+            B.bitnet_pack_int_weights(layout, W, pk)
+        else:
+            sc = torch.empty(1, dtype=torch.float32, device=dev)
+            pws = torch.empty(B.bitnet_pack_workspace_bytes(N, K), dtype=torch.uint8, device=dev)
+            B.bitnet_pack_weights(layout, W, pk, sc, pws)
         packed[name], scales[name] = pk, sc
         del W
     torch.cuda.synchronize()
@@ -215,7 +240,9 @@ def main():
         avg_launch_ms = ms_per_step / launches
         achieved = avg_bytes / (avg_launch_ms * 1e-3) / 1e9
         words = " on TL1 words" if layout == "tl1" else ""
-        if layout == "tl2" and M == 1:
+        if int_layout(layout):
+            kernel = f"elut_generic_kernel ({layout} table lookups) per weight, after quantize_rows_reg per group"
+        elif layout == "tl2" and M == 1:
             kernel = "tl2_mfma_decode_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
         elif layout == "tl2":
             kernel = "bitnet_mpgemm_fused on TL2: quantize_rows_reg + tl2_mfma_decode_kernel per group"
@@ -341,7 +368,8 @@ def parity_check(args, layout, M, linears, groups, by_name, xs, ys, fargs, n_lay
     refs = {}
     for n in g:
         N = by_name[n][1]
-        t_ref, beta = O.ternarize(inputs.weight_f32(N, K, seed=inputs.seed_for(args.workload, index[n])).numpy())
+        W = bench_weight(args, inputs, layout, index[n], N, K).numpy()
+        t_ref, beta = (W, np.float32(INT_BETA)) if int_layout(layout) else O.ternarize(W)
         acc_ref = O.mad_gemm(xq_ref, t_ref)
         refs[n] = (acc_ref, O.epilogue(acc_ref, beta, s_ref))
         del t_ref
@@ -411,8 +439,8 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
     sample_bytes = 0
     for i, (name, K, N) in enumerate(linears):
         Ns = N if row_cap is None else min(N, row_cap)
-        W = inputs.weight_f32(Ns, K, seed=inputs.seed_for(args.workload, i)).numpy()
-        ts[name], betas[name] = O.ternarize(W)
+        W = bench_weight(args, inputs, args.layout, i, Ns, K).numpy()
+        ts[name], betas[name] = (W, INT_BETA) if int_layout(args.layout) else O.ternarize(W)
         sample_bytes += Ns * K // 4
     # prefill: a bounded sample of token rows stands in for the full M
     Mc = M if decode else min(M, 4)

@@ -63,11 +63,25 @@ typedef enum {
  *   4-bit Table 5 code 3(t0+1) + (t1+1), in the tiling of I2_S: a 32-bit word of lane (r, q) in sub-tile j of
  *   block s holds the 16 weights k = 64*(4*s + j) + 16*q + e of row 16R + r as 8 pair codes, pair i (weights
  *   e = 2i, 2i+1) in byte i % 4, low nibble for i < 4 and high nibble for i >= 4.  Size N*K/4 bytes.
+ *
+ * Integer-weight layouts (Appendix "Insight", Table 3, Algorithm "ELUT mpGEMM"): weights from a set of C consecutive
+ * integers, packed from int8 values with bitnet_pack_int_weights and multiplied by table lookups (Eq. 3, with the
+ * sign operation of Eq. 5 where the set is symmetric).  Row-major planes; group j of row n is weights g j .. g j+g-1.
+ * BITNET_LAYOUT_C4G2: C = 4 {-2, -1, 0, 1}, g = 2, code 4 (w0 + 2) + (w1 + 2) in 4 bits (group j in byte
+ *   n K/4 + j/2, low nibble first); 2 bits per weight.  Size N*K/4.
+ * BITNET_LAYOUT_C5G2: C = 5 {-2, .., 2}, g = 2, 4-bit index |5 w0 + w1| placed as C4G2's codes, then a sign plane
+ *   of one bit per group (group j of row n at byte N K/4 + n K/16 + j/8, bit j % 8); 2.5 bits per weight.
+ *   Size N*K/4 + N*K/16.
+ * BITNET_LAYOUT_C3G5: C = 3 {-1, 0, 1}, g = 5, one byte per group at n K/5 + j: index |sum_i 3^(4-i) w_i| (0..121)
+ *   in bits 0-6, sign [sum < 0] in bit 7; 1.6 bits per weight.  Needs K % 320 == 0.  Size N*K/5.
  */
 typedef enum {
     BITNET_LAYOUT_I2S = 0,
     BITNET_LAYOUT_TL2 = 1,
-    BITNET_LAYOUT_TL1 = 2
+    BITNET_LAYOUT_TL1 = 2,
+    BITNET_LAYOUT_C4G2 = 3,
+    BITNET_LAYOUT_C5G2 = 4,
+    BITNET_LAYOUT_C3G5 = 5
 } bitnet_layout;
 
 /* Bytes of the packed buffer for an N x K weight in `layout`; 0 if the shape or layout is unsupported. */
@@ -90,6 +104,16 @@ size_t bitnet_pack_workspace_bytes(int64_t N, int64_t K);
 bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t K,
                                   void* packed, size_t packed_bytes, float* w_scale,
                                   void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * bitnet_pack_int_weights -- pack integer weights for an integer-weight layout (C4G2, C5G2, C3G5; Table 3).
+ *   Wq         device int8 [N, K], values in the layout's set (a value outside it is packed as the nearest value
+ *              of the set).  The per-tensor scale is the caller's: pass it to bitnet_mpgemm as w_scale.
+ *   packed     device buffer of at least bitnet_packed_bytes(layout, N, K) bytes; fully overwritten.
+ *   Shapes: N % 16 == 0, K % 64 == 0 (C3G5: K % 320 == 0), N*K < 2^32.  Pointers 16-byte aligned.
+ */
+bitnet_status bitnet_pack_int_weights(int layout, const int8_t* Wq, int64_t N, int64_t K, void* packed,
+                                      size_t packed_bytes, void* stream);
 
 /*
  * bitnet_quantize_act -- per-token absmax int8 quantisation (Sec. 2.1, Sec. 3.2.2).
@@ -124,6 +148,8 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *   I2_S and TL1 also need N * K and M * K below 2^32.  I2_S: M <= 16 runs the decode GEMV, larger M the prefill
  *   GEMM.  TL1: M <= 16 runs the same decode GEMV, which expands the pair codes to int8 in registers; larger M
  *   rewrites the weights in the I2_S layout in the workspace (N * K / 4 bytes) and runs the prefill GEMM.
+ *   Integer-weight layouts (C4G2, C5G2, C3G5): table lookups with the tables built in LDS for 4 tokens at a time
+ *   (2 for C3G5), any M; x_rowsum is not used and no workspace is needed.
  *   TL2: one token runs the table lookups of Eq. 3 (tables built in LDS) where the row's tables fit (K <= 14336);
  *   otherwise, up to 16 tokens with 384 <= K < 18816, the packed triples are expanded to int8 weights and
  *   multiplied on int8 MFMA; more than 16 tokens (with N * K and M * K below 2^32) rewrite the weights in the
@@ -182,7 +208,8 @@ size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int6
  *   then one launch for all weights (the MFMA expansion for M <= 16 and K < 18816; for M > 16, every weight
  *   rewritten in the I2_S layout and one prefill launch, where ws holds all of them) or one bitnet_mpgemm call
  *   per weight.  TL1 runs as I2_S up to 16 tokens (the same launches, the pair codes expanded in registers) and
- *   as TL2 above (every weight rewritten in the I2_S layout, one prefill launch).
+ *   as TL2 above (every weight rewritten in the I2_S layout, one prefill launch).  The integer-weight layouts run
+ *   the quantiser and then the table lookups of each weight.
  */
 bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* packed, const size_t* packed_bytes,
                                   const float* const* w_scale, const int64_t* N, int64_t K, const float* x,

@@ -17,7 +17,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
 BITNET_LAYOUT_I2S = 0
 BITNET_LAYOUT_TL2 = 1
 BITNET_LAYOUT_TL1 = 2
-LAYOUTS = {"i2s": BITNET_LAYOUT_I2S, "tl2": BITNET_LAYOUT_TL2, "tl1": BITNET_LAYOUT_TL1}
+BITNET_LAYOUT_C4G2 = 3
+BITNET_LAYOUT_C5G2 = 4
+BITNET_LAYOUT_C3G5 = 5
+LAYOUTS = {"i2s": BITNET_LAYOUT_I2S, "tl2": BITNET_LAYOUT_TL2, "tl1": BITNET_LAYOUT_TL1, "c4g2": BITNET_LAYOUT_C4G2,
+           "c5g2": BITNET_LAYOUT_C5G2, "c3g5": BITNET_LAYOUT_C3G5}
+INT_LAYOUTS = ("c4g2", "c5g2", "c3g5")
 
 BITNET_OK = 0
 STATUS_NAMES = {0: "BITNET_OK", 1: "BITNET_E_INVALID", 2: "BITNET_E_SHAPE", 3: "BITNET_E_ALIGN",
@@ -30,6 +35,8 @@ _SIGNATURES = [
     ("bitnet_pack_weights", ctypes.c_int,
      [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t,
       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    ("bitnet_pack_int_weights", ctypes.c_int,
+     [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     ("bitnet_quantize_act", ctypes.c_int,
      [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
       ctypes.c_void_p]),
@@ -141,6 +148,15 @@ def bitnet_pack_weights(layout, W, packed, w_scale, ws, stream=None) -> None:
                                    _ptr(w_scale, "w_scale", torch.float32), _ptr(ws, "ws"),
                                    ws.numel() * ws.element_size(), _stream(stream))
     _check("bitnet_pack_weights", st)
+
+
+def bitnet_pack_int_weights(layout, Wq, packed, stream=None) -> None:
+    """Pack integer weights Wq (int8 [N, K], device) for an integer-weight layout (c4g2, c5g2, c3g5)."""
+    import torch
+    N, K = Wq.shape
+    st = lib().bitnet_pack_int_weights(_layout(layout), _ptr(Wq, "Wq", torch.int8), N, K,
+                                       _ptr(packed, "packed", torch.uint8), packed.numel(), _stream(stream))
+    _check("bitnet_pack_int_weights", st)
 
 
 def bitnet_quantize_act(x, xq, x_scale, x_rowsum=None, stream=None) -> None:

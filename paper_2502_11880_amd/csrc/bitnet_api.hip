@@ -40,8 +40,22 @@ bool weight_shape_ok(int64_t N, int64_t K) {
            N <= (int64_t)1 << 30;
 }
 
+// c3g5 groups five weights: its rows are whole 64-byte runs of groups (K % 320 == 0)
+bool layout_shape_ok(int layout, int64_t N, int64_t K) {
+    return weight_shape_ok(N, K) && (layout != BITNET_LAYOUT_C3G5 || K % 320 == 0);
+}
+
 bool layout_ok(int layout) {
-    return layout == BITNET_LAYOUT_I2S || layout == BITNET_LAYOUT_TL2 || layout == BITNET_LAYOUT_TL1;
+    return layout >= BITNET_LAYOUT_I2S && layout <= BITNET_LAYOUT_C3G5;
+}
+
+// The integer-weight ELUT layouts (packed from integer weights by bitnet_pack_int_weights)
+bool elut_layout(int layout) {
+    return layout == BITNET_LAYOUT_C4G2 || layout == BITNET_LAYOUT_C5G2 || layout == BITNET_LAYOUT_C3G5;
+}
+int elut_format(int layout) {
+    return layout == BITNET_LAYOUT_C4G2 ? bitnet::kElutC4G2
+           : layout == BITNET_LAYOUT_C5G2 ? bitnet::kElutC5G2 : bitnet::kElutC3G5;
 }
 
 // I2_S and TL1 share the tiling, the decode kernels (which read the word format as a template) and their limits.
@@ -49,7 +63,9 @@ bool i2s_tiled(int layout) { return layout == BITNET_LAYOUT_I2S || layout == BIT
 int word_format(int layout) { return layout == BITNET_LAYOUT_TL1 ? bitnet::kFmtTl1 : bitnet::kFmtI2s; }
 
 size_t packed_bytes_of(int layout, int64_t N, int64_t K) {
-    if (i2s_tiled(layout)) return (size_t)N * (size_t)K / 4;
+    if (i2s_tiled(layout) || layout == BITNET_LAYOUT_C4G2) return (size_t)N * (size_t)K / 4;
+    if (layout == BITNET_LAYOUT_C5G2) return (size_t)N * (size_t)K / 4 + (size_t)N * (size_t)K / 16;
+    if (layout == BITNET_LAYOUT_C3G5) return (size_t)N * (size_t)K / 5;
     const int64_t three = (K / bitnet::kTl2BlockK) * bitnet::kTl2BlockK;
     const int64_t two = K - three;
     return (size_t)N * three / 6 + (size_t)N * three / 24 + (size_t)N * two / 4;
@@ -81,7 +97,7 @@ size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 extern "C" {
 
 size_t bitnet_packed_bytes(int layout, int64_t N, int64_t K) {
-    if (!layout_ok(layout) || !weight_shape_ok(N, K)) return 0;
+    if (!layout_ok(layout) || !layout_shape_ok(layout, N, K)) return 0;
     return packed_bytes_of(layout, N, K);
 }
 
@@ -94,6 +110,8 @@ size_t bitnet_pack_workspace_bytes(int64_t N, int64_t K) {
 bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t K, void* packed,
                                   size_t packed_bytes, float* w_scale, void* ws, size_t ws_bytes, void* stream) {
     if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
+    if (elut_layout(layout))
+        return fail(BITNET_E_LAYOUT, "layout %d holds integer weights: pack it with bitnet_pack_int_weights", layout);
     if (!W || !packed || !w_scale) return fail(BITNET_E_INVALID, "null pointer argument");
     if (!weight_shape_ok(N, K)) return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
                                             (long long)kMaxK, (long long)N, (long long)K);
@@ -109,6 +127,21 @@ bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t
                       "bitnet_pack_weights launch");
 }
 
+bitnet_status bitnet_pack_int_weights(int layout, const int8_t* Wq, int64_t N, int64_t K, void* packed,
+                                      size_t packed_bytes, void* stream) {
+    if (!elut_layout(layout)) return fail(BITNET_E_LAYOUT, "layout %d is not an integer-weight ELUT layout", layout);
+    if (!Wq || !packed) return fail(BITNET_E_INVALID, "null pointer argument");
+    if (!layout_shape_ok(layout, N, K) || (uint64_t)N * (uint64_t)K >= ((uint64_t)1 << 32))
+        return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% %d == 0, 0 < K <= %lld, N*K < 2^32; got N=%lld K=%lld",
+                    layout == BITNET_LAYOUT_C3G5 ? 320 : 64, (long long)kMaxK, (long long)N, (long long)K);
+    if (!aligned(Wq, 16) || !aligned(packed, 16)) return fail(BITNET_E_ALIGN, "Wq and packed need 16-byte alignment");
+    if (packed_bytes < packed_bytes_of(layout, N, K))
+        return fail(BITNET_E_INVALID, "packed buffer holds %zu bytes, %zu needed", packed_bytes,
+                    packed_bytes_of(layout, N, K));
+    return hip_status(bitnet::launch_pack_elut(elut_format(layout), Wq, (int)N, (int)K, packed, (hipStream_t)stream),
+                      "bitnet_pack_int_weights launch");
+}
+
 bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* xq, float* x_scale,
                                   int32_t* x_rowsum, void* stream) {
     if (!x || !xq || !x_scale) return fail(BITNET_E_INVALID, "null pointer argument");
@@ -122,7 +155,7 @@ bitnet_status bitnet_quantize_act(const float* x, int64_t M, int64_t K, int8_t* 
 }
 
 size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K) {
-    if (!layout_ok(layout) || !weight_shape_ok(N, K) || M < 1) return 0;
+    if (!layout_ok(layout) || !layout_shape_ok(layout, N, K) || M < 1) return 0;
     if (layout == BITNET_LAYOUT_I2S && M > kDecodeMaxTokens)
         return bitnet::prefill_workspace_bytes(one_linear(nullptr, nullptr, N, nullptr, nullptr), M, K);
     if ((layout == BITNET_LAYOUT_TL2 || layout == BITNET_LAYOUT_TL1) && tl2_via_i2s(M, N, K))
@@ -134,7 +167,7 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
 size_t bitnet_mpgemm_fused_workspace_bytes(int layout, int n_linears, const int64_t* N, int64_t K, int64_t M) {
     if (!layout_ok(layout) || !N || n_linears < 1 || n_linears > bitnet::kMaxFused || M < 1) return 0;
     for (int i = 0; i < n_linears; ++i)
-        if (!weight_shape_ok(N[i], K)) return 0;
+        if (!layout_shape_ok(layout, N[i], K)) return 0;
     size_t need = 0;
     for (int i = 0; i < n_linears; ++i) {
         const size_t w = bitnet_mpgemm_workspace_bytes(layout, M, N[i], K);
@@ -168,9 +201,12 @@ bitnet_status mpgemm_check(int layout, const void* packed, size_t packed_bytes, 
                            float* y, int32_t* acc, size_t* need) {
     if (!layout_ok(layout)) return fail(BITNET_E_LAYOUT, "unknown layout %d", layout);
     if (!packed || !w_scale || !xq || !x_scale || !y) return fail(BITNET_E_INVALID, "null pointer argument");
-    if (!weight_shape_ok(N, K)) return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
-                                            (long long)kMaxK, (long long)N, (long long)K);
+    if (!layout_shape_ok(layout, N, K))
+        return fail(BITNET_E_SHAPE, "need N %% 16 == 0, K %% %d == 0, 0 < K <= %lld; got N=%lld K=%lld",
+                    layout == BITNET_LAYOUT_C3G5 ? 320 : 64, (long long)kMaxK, (long long)N, (long long)K);
     if (M < 1 || M > ((int64_t)1 << 24)) return fail(BITNET_E_SHAPE, "need 1 <= M <= 2^24; got M=%lld", (long long)M);
+    if (elut_layout(layout) && (uint64_t)N * (uint64_t)K >= ((uint64_t)1 << 32))
+        return fail(BITNET_E_SHAPE, "integer-weight layouts need N*K below 2^32");
     if (!aligned(packed, 16) || !aligned(xq, 16) || !aligned(y, 16) || (acc && !aligned(acc, 16)) ||
         !aligned(w_scale, 4) || !aligned(x_scale, 4) || !aligned(x_rowsum, 4))
         return fail(BITNET_E_ALIGN, "packed, xq, y, acc and ws need 16-byte alignment, scales and x_rowsum 4-byte");
@@ -190,6 +226,10 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
                          int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
                          float* y, int32_t* acc, void* ws, size_t ws_bytes, hipStream_t s) {
     (void)packed_bytes;
+    if (elut_layout(layout))   // table lookups of the integer-weight formats, any M (slices of 2 or 4 tokens)
+        return hip_status(bitnet::launch_elut_generic(elut_format(layout), packed, w_scale, xq, x_scale, (int)M, (int)N,
+                                                      (int)K, y, acc, s),
+                          "bitnet_mpgemm launch");
     if (i2s_tiled(layout) && M <= kDecodeMaxTokens)
         return hip_status(bitnet::launch_i2s_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
                                                     (int)M, (int)K, s, word_format(layout)),
@@ -324,8 +364,9 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     size_t need = 0;
     for (int i = 0; i < n_linears; ++i) {
         if (!packed[i] || !w_scale[i] || !y[i]) return fail(BITNET_E_INVALID, "null pointer for weight %d", i);
-        if (!weight_shape_ok(N[i], K)) return fail(BITNET_E_SHAPE, "weight %d: need N %% 16 == 0, K %% 64 == 0, 0 < K <= %lld; got N=%lld K=%lld",
-                                                   i, (long long)kMaxK, (long long)N[i], (long long)K);
+        if (!layout_shape_ok(layout, N[i], K))
+            return fail(BITNET_E_SHAPE, "weight %d: need N %% 16 == 0, K %% %d == 0, 0 < K <= %lld; got N=%lld K=%lld", i,
+                        layout == BITNET_LAYOUT_C3G5 ? 320 : 64, (long long)kMaxK, (long long)N[i], (long long)K);
         if (!aligned(packed[i], 16) || !aligned(y[i], 16) || !aligned(w_scale[i], 4))
             return fail(BITNET_E_ALIGN, "weight %d: packed and y need 16-byte alignment, w_scale 4-byte", i);
         if (packed_bytes[i] < packed_bytes_of(layout, N[i], K))
@@ -343,6 +384,14 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
 
     hipStream_t s = (hipStream_t)stream;
+    if (elut_layout(layout)) {
+        // the quantiser once, then the table lookups of each weight
+        hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
+        for (int i = 0; i < n_linears && e == hipSuccess; ++i)
+            e = bitnet::launch_elut_generic(elut_format(layout), packed[i], w_scale[i], xq, x_scale, (int)M, (int)N[i],
+                                            (int)K, y[i], nullptr, s);
+        return hip_status(e, "bitnet_mpgemm_fused launch");
+    }
     if (layout == BITNET_LAYOUT_I2S || (layout == BITNET_LAYOUT_TL1 && M <= kDecodeMaxTokens)) {
         const int fmt = word_format(layout);
         bitnet::FusedLinears L{};

@@ -254,5 +254,14 @@ hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* cons
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                              int32_t* x_rowsum, hipStream_t stream);
 
+// ELUT for integer weights of other cardinalities: formats c4g2, c5g2 and c3g5 (table lookups, up to 4 tokens per
+// launch for the 2-weight groups and 2 for c3g5; the launcher slices M).
+constexpr int kElutC4G2 = 0;
+constexpr int kElutC5G2 = 1;
+constexpr int kElutC3G5 = 2;
+hipError_t launch_elut_generic(int fmt, const void* packed, const float* w_scale, const int8_t* xq,
+                               const float* x_scale, int M, int N, int K, float* y, int32_t* acc, hipStream_t stream);
+hipError_t launch_pack_elut(int fmt, const int8_t* Wq, int N, int K, void* packed, hipStream_t stream);
+
 
 }  // namespace bitnet

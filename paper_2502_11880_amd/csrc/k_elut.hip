@@ -1,0 +1,265 @@
+// ELUT mpGEMM for integer weights of other cardinalities (Appendix "Insight", Table 3, Algorithm "ELUT mpGEMM",
+// Eq. 3): the weights come from a set of C consecutive integers, every group of g weights is one code, and the
+// accumulation looks the code up in a table of the C^g possible group sums of the token's activations (with mirror
+// consolidation for symmetric sets: the non-negative half of the table, an index and a sign, Eq. 5).
+//
+// Formats (codes as the oracle defines them):
+//   c4g2  C = 4 {-2, -1, 0, 1},  g = 2: 4-bit code = 4 (w0 + 2) + (w1 + 2), 16 entries, 2 bits per weight
+//   c5g2  C = 5 {-2, .., 2},     g = 2: 4-bit index |5 w0 + w1| (13 entries) + a sign plane, 2.5 bits per weight
+//   c3g5  C = 3 {-1, 0, 1},      g = 5: one byte per group, index |sum_j 3^(4-j) w_j| (122 entries) in bits 0-6 and
+//                                       the sign in bit 7, 1.6 bits per weight
+// A 122-entry table does not fit the 16-byte table registers of the paper's CPU kernels (its register-length
+// analysis stops ternary groups at g = 3); in GPU LDS it costs 244 bytes per group and token.
+//
+// Kernel (decode, up to 4 tokens per launch; 2 for c3g5).  A work group of 16 waves owns 16 RS consecutive weight
+// rows (RS per wave) and walks K in blocks of 64 packed words per row: each lane owns word l of a row's block, and
+// the block's tables are built in LDS by the whole group (one entry per thread at a time, from the block's
+// activation codes staged in LDS) before the lanes look their groups up.  Table entry e of group p of token t
+// sits at ((t E' + e) * GB + q) with q = (p mod GW) * 64 + p / GW, so the 64 lanes of a wave reading item i of
+// their words touch 64 consecutive entries when their codes agree.  Each lane keeps one int32 sum per row and
+// token; a wave reduction and the epilogue y = acc * beta / s_t finish each row.
+#include "bitnet_internal.hpp"
+
+namespace bitnet {
+namespace {
+
+template <int F>
+struct ElutFmt;
+template <>
+struct ElutFmt<kElutC4G2> {
+    static constexpr int C = 4, G = 2, E = 16, EP = 16, GW = 8, MT = 4;
+    static constexpr bool kMirror = false;
+};
+template <>
+struct ElutFmt<kElutC5G2> {
+    static constexpr int C = 5, G = 2, E = 13, EP = 16, GW = 8, MT = 4;
+    static constexpr bool kMirror = true;
+};
+template <>
+struct ElutFmt<kElutC3G5> {
+    static constexpr int C = 3, G = 5, E = 122, EP = 128, GW = 4, MT = 2;
+    static constexpr bool kMirror = true;
+};
+
+constexpr int kEW = 16;                  // waves per work group
+constexpr int kEThreads = 64 * kEW;
+
+// Weight j of table entry e (the oracle's elut_entry_weights): base-C digits offset by the set's minimum, or the
+// balanced base-C digits of e with mirroring; weight 0 is the most significant digit.
+template <int F>
+__device__ __forceinline__ int entry_weight(int e, int j) {
+    using T = ElutFmt<F>;
+    int v = e, d = 0;
+    for (int i = T::G - 1; i >= j; --i) {
+        if (T::kMirror) {
+            int r = v % T::C;
+            if (r > T::C / 2) r -= T::C;
+            d = r;
+            v = (v - r) / T::C;
+        } else {
+            d = v % T::C - T::C / 2;
+            v /= T::C;
+        }
+    }
+    return d;
+}
+
+template <int F, int RS>
+__global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* __restrict__ packed,
+                                                                 const float* __restrict__ w_scale,
+                                                                 const int8_t* __restrict__ xq,
+                                                                 const float* __restrict__ x_scale, int M, int N,
+                                                                 int K, float* __restrict__ y,
+                                                                 int32_t* __restrict__ acc_out) {
+    using T = ElutFmt<F>;
+    constexpr int GB = 64 * T::GW;                // groups per block
+    constexpr int KB = GB * T::G;                 // weights per block
+    constexpr int kTab = T::MT * T::EP * GB;      // int16 entries
+    __shared__ int16_t tab[kTab];
+    __shared__ __align__(16) int8_t xs[T::MT][KB];
+    __shared__ int8_t dig[T::E][T::G];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int Gtot = K / T::G;                    // groups per row
+    const int nblk = (Gtot + GB - 1) / GB;
+    const int row0 = blockIdx.x * (kEW * RS) + wave * RS;
+    const size_t row_bytes = T::GW == 8 ? (size_t)K / 4 : (size_t)K / 5;   // index plane (c4g2, c5g2) or bytes
+    const uint8_t* sign_plane = packed + (size_t)N * K / 4;                   // c5g2 only
+
+    for (int i = tid; i < T::E * T::G; i += kEThreads) dig[i / T::G][i % T::G] = (int8_t)entry_weight<F>(i / T::G, i % T::G);
+
+    int acc[RS][T::MT];
+#pragma unroll
+    for (int r = 0; r < RS; ++r)
+#pragma unroll
+        for (int t = 0; t < T::MT; ++t) acc[r][t] = 0;
+
+    for (int kb = 0; kb < nblk; ++kb) {
+        const int gin = min(GB, Gtot - kb * GB);             // groups in this block
+        const int words = (gin + T::GW - 1) / T::GW;         // packed words per row in this block
+        // 1. this wave's packed words of the block (loads in flight while the tables are built)
+        uint32_t wv[RS], sv[RS];
+#pragma unroll
+        for (int r = 0; r < RS; ++r) {
+            const int n = row0 + r;
+            wv[r] = 0u;
+            sv[r] = 0u;
+            if (n < N && lane < words) {
+                wv[r] = *reinterpret_cast<const uint32_t*>(packed + (size_t)n * row_bytes + (size_t)kb * 256 + 4 * lane);
+                if constexpr (F == kElutC5G2) sv[r] = sign_plane[(size_t)n * (K / 16) + (size_t)kb * 64 + lane];
+            }
+        }
+        // 2. the block's activation codes into LDS (after every wave is done with the previous block's tables)
+        __syncthreads();
+        const int kin = gin * T::G;
+        for (int i = tid; i < T::MT * (KB / 4); i += kEThreads) {
+            const int t = i / (KB / 4), w = i % (KB / 4);
+            uint32_t v = 0u;
+            if (t < M && 4 * w < kin)
+                v = *reinterpret_cast<const uint32_t*>(xq + (size_t)t * K + (size_t)kb * KB + 4 * w);
+            reinterpret_cast<uint32_t*>(xs[t])[w] = v;
+        }
+        __syncthreads();
+        // 3. the tables: entry e of group p of token t = sum_j d_j(e) a_j
+        for (int i = tid; i < T::MT * T::E * GB; i += kEThreads) {
+            const int q = i % GB;
+            const int te = i / GB;
+            const int e = te % T::E, t = te / T::E;
+            const int p = (q % 64) * T::GW + q / 64;
+            int v = 0;
+            if (p < gin) {
+#pragma unroll
+                for (int j = 0; j < T::G; ++j) v += (int)dig[e][j] * (int)xs[t][p * T::G + j];
+            }
+            tab[(t * T::EP + e) * GB + q] = (int16_t)v;
+        }
+        __syncthreads();
+        // 4. lookups: item i of lane l's word is group l GW + i, at table column i 64 + l
+        if (lane < words) {
+#pragma unroll
+            for (int r = 0; r < RS; ++r) {
+#pragma unroll
+                for (int i = 0; i < T::GW; ++i) {
+                    int idx, m;
+                    if constexpr (F == kElutC3G5) {
+                        const uint32_t b = (wv[r] >> (8 * i)) & 0xFFu;
+                        idx = (int)(b & 0x7Fu);
+                        m = -(int)(b >> 7);
+                    } else {
+                        idx = (int)((wv[r] >> (4 * i)) & 0xFu);
+                        m = F == kElutC5G2 ? -(int)((sv[r] >> i) & 1u) : 0;
+                    }
+                    const int col = i * 64 + lane;
+#pragma unroll
+                    for (int t = 0; t < T::MT; ++t) {
+                        const int v = tab[(t * T::EP + idx) * GB + col];
+                        acc[r][t] += (v + m) ^ m;            // Eq. 5: the sign bit widened to a mask
+                    }
+                }
+            }
+        }
+    }
+    // 5. every row's sum over the lanes, then the epilogue
+#pragma unroll
+    for (int r = 0; r < RS; ++r) {
+        const int n = row0 + r;
+#pragma unroll
+        for (int t = 0; t < T::MT; ++t) {
+            const int total = wave_sum_all(acc[r][t]);
+            if (lane == 0 && n < N && t < M) {
+                y[(size_t)t * N + n] = (float)total * (*w_scale / x_scale[t]);
+                if (acc_out) acc_out[(size_t)t * N + n] = total;
+            }
+        }
+    }
+}
+
+// Packing: one thread per packed word of a row (c4g2 and c5g2: 8 groups, plus their sign byte; c3g5: 4 groups).
+// Values outside the set are clamped into it.
+template <int F>
+__global__ __launch_bounds__(256) void pack_elut_words(const int8_t* __restrict__ Wq, int N, int K,
+                                                       uint8_t* __restrict__ packed) {
+    using T = ElutFmt<F>;
+    const size_t wpr = (size_t)K / (T::G * T::GW);       // words per row
+    const size_t d = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (d >= (size_t)N * wpr) return;
+    const size_t n = d / wpr;
+    const int w = (int)(d - n * wpr);
+    const int8_t* src = Wq + n * (size_t)K + (size_t)w * T::G * T::GW;
+    const int lo = -(T::C / 2), hi = T::C - 1 - T::C / 2;
+    uint32_t word = 0u, sign = 0u;
+    for (int i = 0; i < T::GW; ++i) {
+        int v = 0;
+        for (int j = 0; j < T::G; ++j) {
+            const int wj = min(max((int)src[i * T::G + j], lo), hi);
+            v = v * T::C + (T::kMirror ? wj : wj - lo);
+        }
+        const uint32_t idx = (uint32_t)(v < 0 ? -v : v);
+        const uint32_t sg = v < 0 ? 1u : 0u;
+        if constexpr (F == kElutC3G5) word |= (idx | (sg << 7)) << (8 * i);
+        else word |= idx << (4 * i);
+        sign |= sg << i;
+    }
+    const size_t row_bytes = T::GW == 8 ? (size_t)K / 4 : (size_t)K / 5;
+    *reinterpret_cast<uint32_t*>(packed + n * row_bytes + 4 * (size_t)w) = word;
+    if constexpr (F == kElutC5G2) packed[(size_t)N * K / 4 + n * (K / 16) + w] = (uint8_t)sign;
+}
+
+template <int F, int RS>
+hipError_t launch_elut_rs(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
+                          int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    using T = ElutFmt<F>;
+    const dim3 grid((unsigned)((N + kEW * RS - 1) / (kEW * RS))), block(kEThreads);
+    for (int m0 = 0; m0 < M; m0 += T::MT) {
+        const int mc = M - m0 < T::MT ? M - m0 : T::MT;
+        hipLaunchKernelGGL((elut_generic_kernel<F, RS>), grid, block, 0, stream,
+                           static_cast<const uint8_t*>(packed), w_scale, xq + (size_t)m0 * K, x_scale + m0, mc, N, K,
+                           y + (size_t)m0 * N, acc ? acc + (size_t)m0 * N : nullptr);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+template <int F>
+hipError_t launch_elut_fmt(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
+                           int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    // rows per wave: as many work groups as CUs where the rows allow, up to 8 rows per wave
+    const int cus = device_cus();
+    const int rs_need = (N + kEW * cus - 1) / (kEW * cus);
+    if (rs_need <= 1) return launch_elut_rs<F, 1>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    if (rs_need <= 2) return launch_elut_rs<F, 2>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    if (rs_need <= 4) return launch_elut_rs<F, 4>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    return launch_elut_rs<F, 8>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+}
+
+template <int F>
+hipError_t launch_pack_fmt(const int8_t* Wq, int N, int K, void* packed, hipStream_t stream) {
+    using T = ElutFmt<F>;
+    const size_t words = (size_t)N * K / (T::G * T::GW);
+    hipLaunchKernelGGL((pack_elut_words<F>), dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream, Wq, N, K,
+                       static_cast<uint8_t*>(packed));
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_elut_generic(int fmt, const void* packed, const float* w_scale, const int8_t* xq,
+                               const float* x_scale, int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    switch (fmt) {
+        case kElutC4G2: return launch_elut_fmt<kElutC4G2>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+        case kElutC5G2: return launch_elut_fmt<kElutC5G2>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+        default: return launch_elut_fmt<kElutC3G5>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    }
+}
+
+hipError_t launch_pack_elut(int fmt, const int8_t* Wq, int N, int K, void* packed, hipStream_t stream) {
+    switch (fmt) {
+        case kElutC4G2: return launch_pack_fmt<kElutC4G2>(Wq, N, K, packed, stream);
+        case kElutC5G2: return launch_pack_fmt<kElutC5G2>(Wq, N, K, packed, stream);
+        default: return launch_pack_fmt<kElutC3G5>(Wq, N, K, packed, stream);
+    }
+}
+
+}  // namespace bitnet

@@ -5,7 +5,8 @@ quantisation, no packing), so the HIP path and the CPU oracle can both be fed fr
 
 Recipe (the paper's models are trained ternary LLMs whose shapes it does not list; these stand in for them):
 
-* weights: fp32 N(0, 0.02), one generator per tensor;
+* weights: fp32 N(0, 0.02), one generator per tensor (integer weights of C values: uniform over the set, or for
+  C = 3 the frequencies of absmean-ternarised Gaussian weights);
 * activations: fp32 N(0, 1), then exactly round(0.001 * M * K) distinct positions, drawn without
   replacement from the same generator, are multiplied by 20 (sign kept);
 * seed of tensor i of workload c: 0xB17E7 + 1000 * c + i.
@@ -37,6 +38,19 @@ def weight_f32(N: int, K: int, seed: int, device="cpu") -> torch.Tensor:
     w = torch.empty((N, K), dtype=torch.float32, device=device)
     w.normal_(0.0, WEIGHT_STD, generator=g)
     return w
+
+
+def int_weights(N: int, K: int, C: int, seed: int, device="cpu") -> torch.Tensor:
+    """int8 [N, K] weights from the set of C consecutive integers -(C // 2) .. C - 1 - C // 2: for C = 3 with the
+    frequencies of absmean-ternarised Gaussian weights (0 with probability 0.31), otherwise uniform."""
+    g = _generator(seed, device)
+    lo = -(C // 2)
+    if C == 3:
+        u = torch.rand((N, K), generator=g, device=device)
+        w = torch.where(u < 0.345, -1, torch.where(u < 0.655, 0, 1))
+    else:
+        w = torch.randint(0, C, (N, K), generator=g, device=device) + lo
+    return w.to(torch.int8)
 
 
 def activation_f32(M: int, K: int, seed: int, device="cpu") -> torch.Tensor:

@@ -35,14 +35,18 @@ def test_packed_bytes_match_layout_definitions(N, K):
     assert B.bitnet_packed_bytes("i2s", N, K) == O.i2s_packed_bytes(N, K)
     assert B.bitnet_packed_bytes("tl2", N, K) == O.tl2_packed_bytes(N, K)
     assert B.bitnet_packed_bytes("tl1", N, K) == O.tl1_packed_bytes(N, K)
+    for fmt in O.ELUT_FORMATS:
+        ok = K % (320 if fmt == "c3g5" else 64) == 0
+        assert B.bitnet_packed_bytes(fmt, N, K) == (O.elut_packed_bytes(fmt, N, K) if ok else 0)
 
 
 def test_packed_bytes_rejects_bad_shapes():
-    for layout in ("i2s", "tl2", "tl1"):
+    for layout in ("i2s", "tl2", "tl1", "c4g2", "c5g2", "c3g5"):
         assert B.bitnet_packed_bytes(layout, 15, 64) == 0
         assert B.bitnet_packed_bytes(layout, 16, 65) == 0
         assert B.bitnet_packed_bytes(layout, 0, 64) == 0
     assert B.bitnet_packed_bytes(7, 16, 64) == 0
+    assert B.bitnet_packed_bytes("c3g5", 16, 640) == 16 * 640 // 5 and B.bitnet_packed_bytes("c3g5", 16, 384) == 0
 
 
 FAKE = 1 << 20          # aligned, never dereferenced: validation fails before any launch
@@ -69,7 +73,7 @@ def _mpgemm(**kw):
 
 @cpu_only
 def test_mpgemm_validation_statuses():
-    assert _mpgemm(layout=5) == 4
+    assert _mpgemm(layout=9) == 4
     assert _mpgemm(packed=None) == 1
     assert _mpgemm(y=None) == 1
     assert _mpgemm(N=40) == 2
@@ -122,6 +126,19 @@ def test_quantize_and_pack_validation_statuses():
     assert lib.bitnet_pack_weights(0, FAKE, 64, 64, FAKE, 100, FAKE, FAKE, ws, None) == 1
     assert lib.bitnet_pack_weights(0, FAKE, 64, 64, FAKE, 1 << 20, FAKE, FAKE, ws - 8, None) == 5
     assert lib.bitnet_pack_weights(0, FAKE, 64, 64, FAKE + 2, 1 << 20, FAKE, FAKE, ws, None) == 3
+
+
+@cpu_only
+def test_pack_int_weights_validation_statuses():
+    lib = B.lib()
+    assert lib.bitnet_pack_int_weights(0, FAKE, 64, 640, FAKE, 1 << 20, None) == 4          # ternary layouts: no
+    assert lib.bitnet_pack_int_weights(5, FAKE, 64, 448, FAKE, 1 << 20, None) == 2          # c3g5 needs K % 320
+    assert lib.bitnet_pack_int_weights(3, None, 64, 640, FAKE, 1 << 20, None) == 1
+    assert lib.bitnet_pack_int_weights(4, FAKE, 64, 640, FAKE, 100, None) == 1
+    assert lib.bitnet_pack_int_weights(3, FAKE + 4, 64, 640, FAKE, 1 << 20, None) == 3
+    ws = B.bitnet_pack_workspace_bytes(64, 640)
+    assert lib.bitnet_pack_weights(3, FAKE, 64, 640, FAKE, 1 << 20, FAKE, FAKE, ws, None) == 4   # integer layouts
+    assert _mpgemm(layout=5, K=448) == 2
 
 
 @cpu_only
