@@ -35,6 +35,7 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 MFMA, TOP/s
 ROT_BYTES = 512 << 20            # rotate through at least 2x the Infinity Cache
 DECODE_MAX_TOKENS = 16
+SMALL_BATCH_MAX = 112            # 17..112 tokens: the decode GEMV in token slices (I2_S, TL1)
 CPU_ROWS = 512                   # oracle timing sample per weight for stacks of layers
 METRIC = "decode GEMV weight GB/s (% HBM peak) + tokens/s; prefill int8 TOPS (% MFMA peak)"
 
@@ -261,17 +262,37 @@ def main():
         unit = "TOP/s"
         launches = len(groups) * n_layers
         avg_launch_ms = second_ms / launches
-        achieved = (flops / launches) / (avg_launch_ms * 1e-3) / 1e12
-        kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
-        if layout != "i2s":
-            kernel = f"{layout}_to_i2s transcoding per group + " + kernel
+        sliced = M <= SMALL_BATCH_MAX and layout in ("i2s", "tl1")
+        if sliced:
+            kernel = (f"i2s_decode_stream_kernel{' on TL1 words' if layout == 'tl1' else ''} in token slices "
+                      "(bitnet_mpgemm_fused, 17-112 tokens: one launch per activation group)")
+        elif int_layout(layout):
+            kernel = f"elut_generic_kernel ({layout} table lookups) per weight"
+        else:
+            kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
+            if layout != "i2s":
+                kernel = f"{layout}_to_i2s transcoding per group + " + kernel
+        # the roofline that binds: HBM for the weight stream (packed weights, the codes read, the fp32 outputs
+        # written) or int8 MFMA, whichever takes longer at its peak
+        gemm_bytes = sum(sum(packed[n].numel() + 4 * M * by_name[n][1] for n in g) + M * by_name[g[0]][0]
+                         for g in groups) * n_layers
+        hbm_bound = gemm_bytes / (HBM_PEAK_GBS * 1e9) > flops / (INT8_PEAK_TOPS * 1e12)
         traffic = measured_traffic(*TRAFFIC[key]) if (key := (args.workload, M, layout)) in TRAFFIC else None
-        roofline = {"bound": "mfma", "kernel": kernel,
-                    "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-                    "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": traffic,
-                    "traffic_unit": "bytes per launch (FETCH_SIZE x copy factor + WRITE_SIZE)" if traffic else None,
-                    "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_ops": int(flops / launches),
-                    "launches_per_step": launches}
+        if hbm_bound:
+            achieved = (gemm_bytes / launches) / (avg_launch_ms * 1e-3) / 1e9
+            roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                        "traffic_unit": "bytes per launch (FETCH_SIZE x copy factor + WRITE_SIZE)" if traffic else None,
+                        "avg_launch_us": round(avg_launch_ms * 1e3, 3),
+                        "avg_algorithmic_bytes": int(gemm_bytes / launches), "launches_per_step": launches}
+        else:
+            achieved = (flops / launches) / (avg_launch_ms * 1e-3) / 1e12
+            roofline = {"bound": "mfma", "kernel": kernel,
+                        "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
+                        "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": traffic,
+                        "traffic_unit": "bytes per launch (FETCH_SIZE x copy factor + WRITE_SIZE)" if traffic else None,
+                        "avg_launch_us": round(avg_launch_ms * 1e3, 3), "avg_algorithmic_ops": int(flops / launches),
+                        "launches_per_step": launches}
     tokens_per_s = M / (ms_per_step * 1e-3)
 
     parity = None

@@ -145,9 +145,11 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *          rewritten in the I2_S layout (N * K / 4 bytes) that the prefill GEMM reads; any contents on entry,
  *          nothing kept between calls.  Calls that run concurrently must not share it.
  *   Shapes: M >= 1, N % 16 == 0, K % 64 == 0, K <= 132096 (127 * K < 2^24 keeps acc exact in fp32);
- *   I2_S and TL1 also need N * K and M * K below 2^32.  I2_S: M <= 16 runs the decode GEMV, larger M the prefill
- *   GEMM.  TL1: M <= 16 runs the same decode GEMV, which expands the pair codes to int8 in registers; larger M
- *   rewrites the weights in the I2_S layout in the workspace (N * K / 4 bytes) and runs the prefill GEMM.
+ *   I2_S and TL1 also need N * K and M * K below 2^32.  I2_S: M <= 16 runs the decode GEMV; 17 <= M <= 112 with
+ *   x_rowsum given and K <= 16384 runs the same GEMV in slices of up to 16 tokens, one launch for all slices (the
+ *   small-batch regime between decode and prefill, which the paper leaves open, Sec. "Limitations"); larger M the
+ *   prefill GEMM.  TL1: the same decode GEMV (the pair codes expanded to int8 in registers) where I2_S runs it;
+ *   otherwise the weights are rewritten in the I2_S layout in the workspace (N * K / 4 bytes) for the prefill GEMM.
  *   Integer-weight layouts (C4G2, C5G2, C3G5): table lookups with the tables built in LDS for 4 tokens at a time
  *   (2 for C3G5), any M; x_rowsum is not used and no workspace is needed.
  *   TL2: one token runs the table lookups of Eq. 3 (tables built in LDS) where the row's tables fit (K <= 14336);

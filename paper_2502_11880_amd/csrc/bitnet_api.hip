@@ -230,7 +230,7 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
         return hip_status(bitnet::launch_elut_generic(elut_format(layout), packed, w_scale, xq, x_scale, (int)M, (int)N,
                                                       (int)K, y, acc, s),
                           "bitnet_mpgemm launch");
-    if (i2s_tiled(layout) && M <= kDecodeMaxTokens)
+    if (i2s_tiled(layout) && (M <= kDecodeMaxTokens || bitnet::i2s_sliced_ok(M, K, x_rowsum != nullptr)))
         return hip_status(bitnet::launch_i2s_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
                                                     (int)M, (int)K, s, word_format(layout)),
                           "bitnet_mpgemm launch");
@@ -392,7 +392,9 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
                                             (int)K, y[i], nullptr, s);
         return hip_status(e, "bitnet_mpgemm_fused launch");
     }
-    if (layout == BITNET_LAYOUT_I2S || (layout == BITNET_LAYOUT_TL1 && M <= kDecodeMaxTokens)) {
+    // the small-batch regime (17..128 tokens, K <= 16384): the decode GEMV in token slices, for I2_S and TL1
+    const bool sliced = i2s_tiled(layout) && bitnet::i2s_sliced_ok(M, K, true);
+    if (layout == BITNET_LAYOUT_I2S || (layout == BITNET_LAYOUT_TL1 && (M <= kDecodeMaxTokens || sliced))) {
         const int fmt = word_format(layout);
         bitnet::FusedLinears L{};
         L.count = n_linears;
@@ -412,7 +414,7 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
                               "bitnet_mpgemm_fused launch");
         hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
         if (e == hipSuccess)
-            e = M <= kDecodeMaxTokens
+            e = (M <= kDecodeMaxTokens || sliced)
                     ? bitnet::launch_i2s_decode(L, xq, x_scale, x_rowsum, (int)M, (int)K, s, fmt)
                     : bitnet::launch_i2s_prefill(L, xq, x_scale, x_rowsum, (int)M, (int)K, ws, ws_bytes, s);
         return hip_status(e, "bitnet_mpgemm_fused launch");

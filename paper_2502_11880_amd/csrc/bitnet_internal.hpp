@@ -219,7 +219,12 @@ size_t prefill_workspace_bytes(const FusedLinears& L, int64_t M, int64_t K);
 hipError_t launch_i2s_prefill(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                               int M, int K, void* ws, size_t ws_bytes, hipStream_t stream);
 constexpr int64_t kFusedMaxK = 61440;   // single-token fused quantise+GEMV keeps the K codes in LDS
-// fmt: kFmtI2s or kFmtTl1 (the weights' word format; both formats share the I2_S tiling)
+// fmt: kFmtI2s or kFmtTl1 (the weights' word format; both formats share the I2_S tiling).  Up to 16 tokens; more
+// (the small-batch regime) where i2s_sliced_ok holds: token slices of up to 16 in one launch.
+constexpr int kSmallBatchMaxTokens = 112;   // from 128 tokens the prefill GEMM is as fast
+inline bool i2s_sliced_ok(int64_t M, int64_t K, bool has_rowsum) {
+    return M > 16 && M <= kSmallBatchMaxTokens && has_rowsum && K <= 16384;
+}
 hipError_t launch_i2s_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
                              int M, int K, hipStream_t stream, int fmt = kFmtI2s);
 hipError_t launch_i2s_gemv1_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,

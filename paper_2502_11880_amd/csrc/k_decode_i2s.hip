@@ -157,14 +157,26 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_kernel(FusedLinears L, 
 // them.  The work group then walks row groups as the single-token kernel does, two batches of weights in flight.
 // HAS_ACC: some weight of the launch also stores its int32 sums (the parity hook); the other instance holds no
 // code for them (2% of the eight-token step).
+//
+// Token slices (more than 16 tokens, the small-batch regime): blockIdx.y is a slice of `slice` tokens; every slice
+// walks the same row groups in the same order, and with gridDim.x a multiple of 8 the work groups (x, y) of all
+// slices run on the XCD x % 8, so the slices of a row group meet its weight bytes in one L2 rather than each
+// fetching them from HBM.
 template <int WAVES, int U, int MG, bool HAS_RS, bool HAS_ACC, int FMT>
 __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLinears L, const int8_t* __restrict__ xq,
                                                                        const float* __restrict__ x_scale,
                                                                        const int32_t* __restrict__ x_rowsum, int M,
-                                                                       int K) {
+                                                                       int K, int slice) {
     extern __shared__ __align__(16) int8_t xs[];      // M rows of K + 16 codes
     __shared__ v4i part[2][WAVES][64];
     __shared__ int tsum[WAVES][16];
+
+    // this work group's token slice: tokens m0 .. m0 + M - 1
+    const int m0 = (int)blockIdx.y * slice;
+    M = min(M - m0, slice);
+    xq += (size_t)m0 * K;
+    x_scale += m0;
+    if (HAS_RS) x_rowsum += m0;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -302,9 +314,9 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
                 const int m = 4 * q + v;
                 if (m < M) {
                     const int val = tot[v] - rs_m[v];
-                    y[(size_t)m * N + n] = (float)val * (bw / xs_m[v]);
+                    y[(size_t)(m0 + m) * N + n] = (float)val * (bw / xs_m[v]);
                     if constexpr (HAS_ACC) {
-                        if (acc_out) acc_out[(size_t)m * N + n] = val;
+                        if (acc_out) acc_out[(size_t)(m0 + m) * N + n] = val;
                     }
                 }
             }
@@ -596,35 +608,43 @@ hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t
     return launch_stream<FMT, WAVES, U, 16>(L, x, K, xq, s, rs, stream);
 }
 
+// M tokens in slices of `slice` (M <= slice: one slice, the whole launch on one token set).
 template <int FMT, int W, int U, int MG>
 hipError_t launch_mstream(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
-                          int M, int K, hipStream_t stream) {
+                          int M, int K, hipStream_t stream, int slice = 16) {
     bool has_acc = false;
     for (int i = 0; i < L.count; ++i) has_acc = has_acc || L.acc[i] != nullptr;
     const void* kern = has_acc ? reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, true, FMT>)
                                : reinterpret_cast<const void*>(i2s_decode_stream_kernel<W, U, MG, true, false, FMT>);
-    const size_t lds = (size_t)M * (K + 16);
+    const int per = M < slice ? M : slice;                    // tokens of one slice
+    const int slices = (M + per - 1) / per;
+    const size_t lds = (size_t)per * (K + 16);
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * W, lds) != hipSuccess || occ <= 0) occ = 1;
-    const int64_t max_g = (int64_t)device_cus() * occ;
+    int64_t max_g = (int64_t)device_cus() * occ;
+    if (slices > 1) max_g = max_g / slices / kNumXcd * kNumXcd;  // every slice resident at once, XCD-aligned columns
+    if (max_g < kNumXcd) max_g = kNumXcd;
     const int64_t rounds = (L.total + max_g - 1) / max_g;
-    const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * W);
+    int64_t gx = (L.total + rounds - 1) / rounds;
+    if (slices > 1 && gx > kNumXcd) gx = gx / kNumXcd * kNumXcd;
+    const dim3 grid((unsigned)gx, (unsigned)slices), block(64 * W);
     if (has_acc)
         hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, true, FMT>), grid, block, lds, stream, L, xq,
-                           x_scale, x_rowsum, M, K);
+                           x_scale, x_rowsum, M, K, per);
     else
         hipLaunchKernelGGL((i2s_decode_stream_kernel<W, U, MG, true, false, FMT>), grid, block, lds, stream, L, xq,
-                           x_scale, x_rowsum, M, K);
+                           x_scale, x_rowsum, M, K, per);
     return hipGetLastError();
 }
 
 template <int FMT, int W, int U>
 hipError_t launch_mstream_m(const FusedLinears& L, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum,
-                            int M, int K, hipStream_t stream) {
-    if (M <= 4) return launch_mstream<FMT, W, U, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-    if (M <= 8) return launch_mstream<FMT, W, U, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-    if (M <= 12) return launch_mstream<FMT, W, U, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
-    return launch_mstream<FMT, W, U, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+                            int M, int K, hipStream_t stream, int slice) {
+    const int per = M < slice ? M : slice;                    // tokens per work group
+    if (per <= 4) return launch_mstream<FMT, W, U, 1>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+    if (per <= 8) return launch_mstream<FMT, W, U, 2>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+    if (per <= 12) return launch_mstream<FMT, W, U, 3>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+    return launch_mstream<FMT, W, U, 4>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
 }
 
 }  // namespace
@@ -662,23 +682,28 @@ hipError_t launch_decode_fmt(const FusedLinears& L, const int8_t* xq, const floa
                              int M, int K, hipStream_t stream) {
     const int nkb = (K + kI2sBlockK - 1) / kI2sBlockK;
     const int cus = device_cus();
-    const bool fits = (int64_t)M * (K + 16) <= kDecodeStageBytes;   // the tokens' codes fit in LDS
+    // tokens per work group: up to 16 (one MFMA's rows), as many as fit in LDS; more tokens run as token slices
+    int slice = 16;
+    while (slice > 4 && (int64_t)slice * (K + 16) > kDecodeStageBytes) slice -= 4;
+    const int per = M < slice ? M : slice;
+    const bool fits = (int64_t)per * (K + 16) <= kDecodeStageBytes;   // a slice's codes fit in LDS
+    if (M > 16 && !(x_rowsum && fits && nkb <= 64)) return hipErrorInvalidValue;
     if (x_rowsum && fits && nkb <= 16 && L.total > cus / 2) {
         // 4-wave work groups (K <= 4096) where the launch has more row groups than half the CUs: each group stages
         // the codes once as the 16-wave groups do, without waiting on the slowest of 16 waves at each barrier
         const int u4 = (nkb + 3) / 4;
-        if (u4 <= 1) return launch_mstream_m<FMT, 4, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u4 <= 2) return launch_mstream_m<FMT, 4, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u4 <= 3) return launch_mstream_m<FMT, 4, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
-        return launch_mstream_m<FMT, 4, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u4 <= 1) return launch_mstream_m<FMT, 4, 1>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+        if (u4 <= 2) return launch_mstream_m<FMT, 4, 2>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+        if (u4 <= 3) return launch_mstream_m<FMT, 4, 3>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+        return launch_mstream_m<FMT, 4, 4>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
     }
     if (x_rowsum && fits && nkb <= 64) {
         // 16-wave work groups, all of a row group's blocks in one batch; past what fits on the chip they stream
         const int u16 = (nkb + 15) / 16;
-        if (u16 <= 1) return launch_mstream_m<FMT, 16, 1>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u16 <= 2) return launch_mstream_m<FMT, 16, 2>(L, xq, x_scale, x_rowsum, M, K, stream);
-        if (u16 <= 3) return launch_mstream_m<FMT, 16, 3>(L, xq, x_scale, x_rowsum, M, K, stream);
-        return launch_mstream_m<FMT, 16, 4>(L, xq, x_scale, x_rowsum, M, K, stream);
+        if (u16 <= 1) return launch_mstream_m<FMT, 16, 1>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+        if (u16 <= 2) return launch_mstream_m<FMT, 16, 2>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+        if (u16 <= 3) return launch_mstream_m<FMT, 16, 3>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
+        return launch_mstream_m<FMT, 16, 4>(L, xq, x_scale, x_rowsum, M, K, stream, slice);
     }
     int waves, u;
     decode_shape(L.total, K, 4, 4, waves, u);
