@@ -25,6 +25,8 @@ What it computes, with the part of the paper each step follows:
 * ``elut_tables`` / ``elut_gemm`` -- Eq. 3 / Algorithm "ELUT mpGEMM" with mirror consolidation
   (Sec. 3.1.1) and the 1-bit sign operation of Eq. 5: an independent second route to the same integers;
   ``tl1_tables`` / ``elut_gemm_tl1`` the same for the TL1 format (Algorithm TL1: 9-entry pair tables).
+* ``elut_gemm_lossy`` / ``elut_gemm_tl1_lossy`` -- the lossy TL2_0 and TL1_0 kernels of Table 1 (Sec. 3.2.1): the
+  same lookups on tables quantised to int8, with one power-of-two scale per token and table block.
 * ``elut_*`` / ``pack_elut`` -- the ELUT method for integer weights of other cardinalities (Appendix "Insight",
   Table 3, Algorithm "ELUT mpGEMM"): group codes, tables of the C^g sums (mirrored for symmetric sets) and the
   packed formats c4g2, c5g2 and c3g5.
@@ -523,6 +525,68 @@ def elut_gemm_tl1(xq: np.ndarray, packed_tl1: np.ndarray, N: int, K: int) -> np.
         vals = np.take_along_axis(lut[m][None, :, :], code[:, :, None], axis=2)[..., 0]   # [N, K/2]
         acc[m] = vals.sum(axis=1)
     return acc.astype(np.int32)
+
+
+# ----------------------------------------------------------------------------------------------
+# Lossy TL2_0 / TL1_0 (Sec. 3.2.1, Table 1): the table sums quantised to int8 before the lookups
+# ----------------------------------------------------------------------------------------------
+LOSSY_TRIPLES_PER_BLOCK = TL2_BLOCK_K // 3      # one scale per token for the 128 triples of a 384-k block
+LOSSY_PAIRS_PER_UNIT = TAIL_UNIT_K // 2         # one scale per token for the 32 pairs of a 64-k unit
+
+
+def lossy_shift(max_abs) -> np.ndarray:
+    """The smallest s >= 0 with max_abs <= 127 * 2^s: the table block's int8 scale is 2^-s."""
+    m = np.asarray(max_abs, dtype=np.int64)
+    s = np.zeros_like(m)
+    while np.any(m > 127 * (1 << s)):
+        s = np.where(m > 127 * (1 << s), s + 1, s)
+    return s
+
+
+def quantize_table(lut: np.ndarray, blocks: np.ndarray):
+    """int8 tables of one kind: lut [M, G, E] int sums; blocks [G] the block of every group.  Per token and block
+    the entries are divided by 2^s (s from the block's largest |entry|) and rounded half to even.  Returns the
+    quantised entries [M, G, E] and the shift of every token and group [M, G]."""
+    lut = np.asarray(lut, dtype=np.int64)
+    M, G, _ = lut.shape
+    shift = np.zeros((M, G), dtype=np.int64)
+    for b in np.unique(blocks):
+        sel = blocks == b
+        mx = np.abs(lut[:, sel, :]).reshape(M, -1).max(axis=1)                 # [M]
+        shift[:, sel] = lossy_shift(mx)[:, None]
+    q = np.rint(lut / (2.0 ** shift)[..., None]).astype(np.int64)             # exact: |lut| < 2^10, powers of two
+    return q, shift
+
+
+def elut_gemm_lossy(xq: np.ndarray, packed_tl2: np.ndarray, N: int, K: int) -> np.ndarray:
+    """TL2_0: Eq. 3 lookups on int8-quantised tables.  Each triple (and each TL1 tail pair) contributes its
+    quantised entry with the Eq. 5 sign operation; a block's sum is scaled back by 2^s, exactly."""
+    idx, sign, tail = tl2_decode_fields(packed_tl2, N, K)
+    lut, lut1 = elut_tables(xq, K)
+    q, sh = quantize_table(lut, np.arange(lut.shape[1]) // LOSSY_TRIPLES_PER_BLOCK)
+    q1, sh1 = quantize_table(lut1, np.arange(lut1.shape[1]) // LOSSY_PAIRS_PER_UNIT)
+    M = lut.shape[0]
+    acc = np.zeros((M, N), dtype=np.int64)
+    for m in range(M):
+        if lut.shape[1]:
+            vals = np.take_along_axis(q[m][None, :, :], idx[:, :, None], axis=2)[..., 0]      # [N, G]
+            acc[m] += (sign_op(vals, sign) << sh[m][None, :]).sum(axis=1)
+        if lut1.shape[1]:
+            vals1 = np.take_along_axis(q1[m][None, :, :], tail[:, :, None], axis=2)[..., 0]
+            acc[m] += (vals1 << sh1[m][None, :]).sum(axis=1)
+    return acc
+
+
+def elut_gemm_tl1_lossy(xq: np.ndarray, packed_tl1: np.ndarray, N: int, K: int) -> np.ndarray:
+    """TL1_0: Algorithm TL1's lookups on int8-quantised pair tables (one scale per token and 64-k unit)."""
+    code = tl1_decode_codes(packed_tl1, N, K)
+    q, sh = quantize_table(tl1_tables(xq), np.arange(K // 2) // LOSSY_PAIRS_PER_UNIT)
+    M = q.shape[0]
+    acc = np.zeros((M, N), dtype=np.int64)
+    for m in range(M):
+        vals = np.take_along_axis(q[m][None, :, :], code[:, :, None], axis=2)[..., 0]
+        acc[m] = (vals << sh[m][None, :]).sum(axis=1)
+    return acc
 
 
 # ----------------------------------------------------------------------------------------------

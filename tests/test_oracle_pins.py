@@ -521,3 +521,50 @@ def test_elut_positions_hand_computed_and_every_field_once():
         if fmt == "c5g2":
             bits = sb.ravel() * 8 + sbit.ravel()
             assert np.unique(bits).size == bits.size and bits.max() == 8 * O.elut_packed_bytes(fmt, N, K) - 1
+
+
+# ---------------------------------------------------------------------------------------------
+# Lossy TL2_0 / TL1_0 (Sec. 3.2.1, Table 1): int8 tables with a power-of-two scale per token and block
+# ---------------------------------------------------------------------------------------------
+def test_lossy_shift_is_the_smallest_that_fits_int8():
+    assert [int(v) for v in O.lossy_shift([0, 127, 128, 254, 255, 381, 508, 509])] == [0, 0, 1, 1, 2, 2, 2, 3]
+
+
+def test_lossy_tl2_worked_example():
+    # one 384-k block, every activation code 127 and every weight +1: the largest entry (+++) is 381, so s = 2 and
+    # that entry becomes round(381 / 4) = round(95.25) = 95; each of the 128 triples gives 95 * 4 = 380 instead
+    # of 381, so the sum is 128 * 380 = 48640 (the exact sum is 127 * 384 = 48768)
+    N, K = 16, 384
+    t = np.ones((N, K), np.int8)
+    xq = np.full((1, K), 127, np.int8)
+    acc = O.elut_gemm_lossy(xq, O.pack_tl2(t), N, K)
+    assert np.all(acc == 48640) and int(O.mad_gemm(xq, t)[0, 0]) == 48768
+    # TL1_0 on the same weights: pair (+,+) = 254, s = 1, round(127) = 127: exact
+    assert np.all(O.elut_gemm_tl1_lossy(xq, O.pack_tl1(t), N, K) == 48768)
+    # codes (127, 0, 0) with weights (+, 0, 0): entry 127 at s = 2 (one triple of all 127 makes the block's largest
+    # entry 381) -> round(31.75) = 32, scaled back to 128 per triple
+    xq2 = np.tile(np.array([[127, 0, 0]], np.int8), (1, 128))
+    xq2[0, :3] = 127                                        # one triple of all 127 sets the block's shift to 2
+    t2 = np.zeros((N, K), np.int8)
+    t2[:, 3::3] = 1                                         # every triple but the first: (+, 0, 0)
+    assert np.all(O.elut_gemm_lossy(xq2, O.pack_tl2(t2), N, K) == 127 * 32 * 4)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 16, 448), (3, 32, 832), (2, 16, 1600)])
+def test_lossy_exact_when_tables_fit_int8_and_error_bounded(M, N, K):
+    rng = np.random.default_rng(M + N + K)
+    t = rng.integers(-1, 2, size=(N, K)).astype(np.int8)
+    small = rng.integers(-42, 43, size=(M, K)).astype(np.int8)            # every TL2 entry within 3 * 42 = 126
+    assert np.array_equal(O.elut_gemm_lossy(small, O.pack_tl2(t), N, K), O.mad_gemm(small, t))
+    assert np.array_equal(O.elut_gemm_tl1_lossy(small, O.pack_tl1(t), N, K), O.mad_gemm(small, t))
+    xq = rng.integers(-128, 128, size=(M, K)).astype(np.int8)
+    exact = O.mad_gemm(xq, t).astype(np.int64)
+    sym = xq.astype(np.int16).clip(-127, 127).astype(np.int8)
+    for route, packed in [(O.elut_gemm_lossy, O.pack_tl2(t)), (O.elut_gemm_tl1_lossy, O.pack_tl1(t))]:
+        lossy = route(xq, packed, N, K)
+        # rounding half to even is odd-symmetric, so negating the codes negates the result
+        assert np.array_equal(route(-sym, packed, N, K), -route(sym, packed, N, K))
+        # every group's entry is off by at most half its block's step 2^s, and s <= 2 for these tables
+        groups = K // 3 + K // 2
+        assert np.all(np.abs(lossy - exact) <= groups * 2)
+        assert not np.array_equal(lossy, exact)                              # these codes do lose precision
