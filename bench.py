@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", type=int, default=4)
     p.add_argument("--tokens", type=int, default=None)
-    p.add_argument("--layout", default="i2s", choices=["i2s", "tl2", "tl1", "c4g2", "c5g2", "c3g5"])
+    p.add_argument("--layout", default="i2s", choices=["i2s", "tl2", "tl1", "c4g2", "c5g2", "c3g5", "tl2_0", "tl1_0"])
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-parity", action="store_true")
@@ -60,6 +60,7 @@ def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
+LOSSY = {"tl2_0": "tl2_elut_decode_kernel", "tl1_0": "tl1_elut_decode_kernel"}   # layout -> kernel
 INT_BETA = 0.02                  # per-tensor scale given with the integer-weight layouts' weights
 INT_C = {"c4g2": 4, "c5g2": 5, "c3g5": 3}
 
@@ -243,6 +244,8 @@ def main():
         words = " on TL1 words" if layout == "tl1" else ""
         if int_layout(layout):
             kernel = f"elut_generic_kernel ({layout} table lookups) per weight, after quantize_rows_reg per group"
+        elif layout in LOSSY:
+            kernel = f"{LOSSY[layout]} (int8-quantised tables) per weight, after quantize_rows_reg per group"
         elif layout == "tl2" and M == 1:
             kernel = "tl2_mfma_decode_kernel (bitnet_mpgemm_fused, one token: quantiser fused)"
         elif layout == "tl2":
@@ -268,6 +271,8 @@ def main():
                       "(bitnet_mpgemm_fused, 17-112 tokens: one launch per activation group)")
         elif int_layout(layout):
             kernel = f"elut_generic_kernel ({layout} table lookups) per weight"
+        elif layout in LOSSY:
+            kernel = f"{LOSSY[layout]} (int8-quantised tables) in 8-token slices per weight"
         else:
             kernel = "i2s_prefill_kernel (bitnet_mpgemm_fused, M > 16: one launch per activation group)"
             if layout != "i2s":
@@ -391,7 +396,7 @@ def parity_check(args, layout, M, linears, groups, by_name, xs, ys, fargs, n_lay
         N = by_name[n][1]
         W = bench_weight(args, inputs, layout, index[n], N, K).numpy()
         t_ref, beta = (W, np.float32(INT_BETA)) if int_layout(layout) else O.ternarize(W)
-        acc_ref = O.mad_gemm(xq_ref, t_ref)
+        acc_ref = oracle_acc(O, layout, xq_ref, t_ref)
         refs[n] = (acc_ref, O.epilogue(acc_ref, beta, s_ref))
         del t_ref
     dev = xs[0].device
@@ -425,6 +430,17 @@ def parity_check(args, layout, M, linears, groups, by_name, xs, ys, fargs, n_lay
             "pass": bool(codes_ok and zeros_ok and worst <= 1e-5)}
 
 
+def oracle_acc(O, layout, xq, t):
+    """The oracle's accumulators for a layout: the exact integer products, or for the lossy layouts the lookups on
+    int8-quantised tables over the oracle's own packing."""
+    N, K = t.shape
+    if layout == "tl2_0":
+        return O.elut_gemm_lossy(xq, O.pack_tl2(t), N, K)
+    if layout == "tl1_0":
+        return O.elut_gemm_tl1_lossy(xq, O.pack_tl1(t), N, K)
+    return O.mad_gemm(xq, t)
+
+
 def cpu_model():
     """The host CPU's model name (Linux /proc/cpuinfo), or None."""
     try:
@@ -456,12 +472,14 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
     n_layers = inputs.WORKLOADS[args.workload].get("layers", 1)
     # very large layers: the first CPU_ROWS output rows of each weight stand in for all of them
     row_cap = CPU_ROWS if n_layers > 1 else None
-    ts, betas = {}, {}
+    ts, betas, packs = {}, {}, {}
     sample_bytes = 0
     for i, (name, K, N) in enumerate(linears):
         Ns = N if row_cap is None else min(N, row_cap)
         W = bench_weight(args, inputs, args.layout, i, Ns, K).numpy()
         ts[name], betas[name] = (W, INT_BETA) if int_layout(args.layout) else O.ternarize(W)
+        if args.layout in LOSSY:
+            packs[name] = (O.pack_tl2 if args.layout == "tl2_0" else O.pack_tl1)(ts[name])
         sample_bytes += Ns * K // 4
     # prefill: a bounded sample of token rows stands in for the full M
     Mc = M if decode else min(M, 4)
@@ -477,7 +495,13 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
                 for gi, g in enumerate(groups):
                     xq, s = O.quantize_act(xs[gi])
                     for n in g:
-                        O.epilogue(O.mad_gemm(xq, ts[n]), betas[n], s)
+                        if args.layout == "tl2_0":
+                            acc = O.elut_gemm_lossy(xq, packs[n], *ts[n].shape)
+                        elif args.layout == "tl1_0":
+                            acc = O.elut_gemm_tl1_lossy(xq, packs[n], *ts[n].shape)
+                        else:
+                            acc = O.mad_gemm(xq, ts[n])
+                        O.epilogue(acc, betas[n], s)
                 steps += 1
                 el = time.perf_counter() - t0
                 if el >= args.cpu_seconds / 2:
@@ -503,7 +527,9 @@ def cpu_baseline(args, M, linears, groups, by_name, step_weight_bytes, flops, de
                              "tokens_per_s": round(Mc / per_step, 3)}
     allc = legs[host_threads()]
     one = legs[1]
-    how = "; numpy quantiser and epilogue, float64 BLAS matrix product (exact for these integers)"
+    how = ("; numpy quantiser and epilogue, float64 BLAS matrix product (exact for these integers)"
+           if args.layout not in LOSSY else "; numpy quantiser, table build, int8 table quantisation, lookups and "
+           "epilogue (the packing is done beforehand)")
     return {**allc, "kind": "oracle", "sample": allc["sample"] + how, "cpu_model": cpu_model(),
             "host_threads": host_threads(),
             "single_thread": {k: one[k] for k in ("value", "unit", "cores", "sample", "tokens_per_s")}}

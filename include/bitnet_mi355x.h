@@ -74,6 +74,13 @@ typedef enum {
  *   Size N*K/4 + N*K/16.
  * BITNET_LAYOUT_C3G5: C = 3 {-1, 0, 1}, g = 5, one byte per group at n K/5 + j: index |sum_i 3^(4-i) w_i| (0..121)
  *   in bits 0-6, sign [sum < 0] in bit 7; 1.6 bits per weight.  Needs K % 320 == 0.  Size N*K/5.
+ *
+ * Lossy kernels (Table 1 "TL2_0", "TL1_0"; Sec. 3.2.1): BITNET_LAYOUT_TL2_0 and BITNET_LAYOUT_TL1_0 pack exactly as
+ *   TL2 and TL1, but bitnet_mpgemm looks the groups up in tables quantised to int8: per token and table block (the
+ *   128 triples of a 384-k TL2 block, or the 32 pairs of a 64-k TL1 unit) every entry is divided by 2^s, s the
+ *   smallest shift that brings the block's largest |entry| within 127, and rounded half to even; the block's sum
+ *   is multiplied back by 2^s.  The accumulators are exact integers of that rule, close to but not equal to
+ *   sum_k xq t (the paper's lossy kernels; the quantisation itself is this library's reading).
  */
 typedef enum {
     BITNET_LAYOUT_I2S = 0,
@@ -81,7 +88,9 @@ typedef enum {
     BITNET_LAYOUT_TL1 = 2,
     BITNET_LAYOUT_C4G2 = 3,
     BITNET_LAYOUT_C5G2 = 4,
-    BITNET_LAYOUT_C3G5 = 5
+    BITNET_LAYOUT_C3G5 = 5,
+    BITNET_LAYOUT_TL2_0 = 6,
+    BITNET_LAYOUT_TL1_0 = 7
 } bitnet_layout;
 
 /* Bytes of the packed buffer for an N x K weight in `layout`; 0 if the shape or layout is unsupported. */
@@ -151,7 +160,8 @@ size_t bitnet_mpgemm_workspace_bytes(int layout, int64_t M, int64_t N, int64_t K
  *   prefill GEMM.  TL1: the same decode GEMV (the pair codes expanded to int8 in registers) where I2_S runs it;
  *   otherwise the weights are rewritten in the I2_S layout in the workspace (N * K / 4 bytes) for the prefill GEMM.
  *   Integer-weight layouts (C4G2, C5G2, C3G5): table lookups with the tables built in LDS for 4 tokens at a time
- *   (2 for C3G5), any M; x_rowsum is not used and no workspace is needed.
+ *   (2 for C3G5), any M; x_rowsum is not used and no workspace is needed.  TL2_0 and TL1_0: the lossy table
+ *   lookups described with the layouts, 8 tokens per launch, any M, no workspace; acc receives their integers.
  *   TL2: one token runs the table lookups of Eq. 3 (tables built in LDS) where the row's tables fit (K <= 14336);
  *   otherwise, up to 16 tokens with 384 <= K < 18816, the packed triples are expanded to int8 weights and
  *   multiplied on int8 MFMA; more than 16 tokens (with N * K and M * K below 2^32) rewrite the weights in the

@@ -20,8 +20,11 @@ BITNET_LAYOUT_TL1 = 2
 BITNET_LAYOUT_C4G2 = 3
 BITNET_LAYOUT_C5G2 = 4
 BITNET_LAYOUT_C3G5 = 5
+BITNET_LAYOUT_TL2_0 = 6
+BITNET_LAYOUT_TL1_0 = 7
 LAYOUTS = {"i2s": BITNET_LAYOUT_I2S, "tl2": BITNET_LAYOUT_TL2, "tl1": BITNET_LAYOUT_TL1, "c4g2": BITNET_LAYOUT_C4G2,
-           "c5g2": BITNET_LAYOUT_C5G2, "c3g5": BITNET_LAYOUT_C3G5}
+           "c5g2": BITNET_LAYOUT_C5G2, "c3g5": BITNET_LAYOUT_C3G5, "tl2_0": BITNET_LAYOUT_TL2_0,
+           "tl1_0": BITNET_LAYOUT_TL1_0}
 INT_LAYOUTS = ("c4g2", "c5g2", "c3g5")
 
 BITNET_OK = 0

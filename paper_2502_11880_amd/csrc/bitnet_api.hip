@@ -46,7 +46,13 @@ bool layout_shape_ok(int layout, int64_t N, int64_t K) {
 }
 
 bool layout_ok(int layout) {
-    return layout >= BITNET_LAYOUT_I2S && layout <= BITNET_LAYOUT_C3G5;
+    return layout >= BITNET_LAYOUT_I2S && layout <= BITNET_LAYOUT_TL1_0;
+}
+
+// The lossy kernels (TL2_0, TL1_0) read the packed formats of TL2 and TL1.
+bool lossy_layout(int layout) { return layout == BITNET_LAYOUT_TL2_0 || layout == BITNET_LAYOUT_TL1_0; }
+int packed_as(int layout) {
+    return layout == BITNET_LAYOUT_TL2_0 ? BITNET_LAYOUT_TL2 : layout == BITNET_LAYOUT_TL1_0 ? BITNET_LAYOUT_TL1 : layout;
 }
 
 // The integer-weight ELUT layouts (packed from integer weights by bitnet_pack_int_weights)
@@ -63,6 +69,7 @@ bool i2s_tiled(int layout) { return layout == BITNET_LAYOUT_I2S || layout == BIT
 int word_format(int layout) { return layout == BITNET_LAYOUT_TL1 ? bitnet::kFmtTl1 : bitnet::kFmtI2s; }
 
 size_t packed_bytes_of(int layout, int64_t N, int64_t K) {
+    layout = packed_as(layout);
     if (i2s_tiled(layout) || layout == BITNET_LAYOUT_C4G2) return (size_t)N * (size_t)K / 4;
     if (layout == BITNET_LAYOUT_C5G2) return (size_t)N * (size_t)K / 4 + (size_t)N * (size_t)K / 16;
     if (layout == BITNET_LAYOUT_C3G5) return (size_t)N * (size_t)K / 5;
@@ -123,7 +130,7 @@ bitnet_status bitnet_pack_weights(int layout, const float* W, int64_t N, int64_t
                     packed_bytes_of(layout, N, K));
     if (!ws || ws_bytes < bitnet::pack_workspace_bytes())
         return fail(BITNET_E_WORKSPACE, "pack workspace needs %zu bytes", bitnet::pack_workspace_bytes());
-    return hip_status(bitnet::launch_pack(layout, W, N, K, packed, w_scale, ws, (hipStream_t)stream),
+    return hip_status(bitnet::launch_pack(packed_as(layout), W, N, K, packed, w_scale, ws, (hipStream_t)stream),
                       "bitnet_pack_weights launch");
 }
 
@@ -226,6 +233,20 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
                          int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
                          float* y, int32_t* acc, void* ws, size_t ws_bytes, hipStream_t s) {
     (void)packed_bytes;
+    if (lossy_layout(layout)) {
+        // TL2_0 / TL1_0: table lookups on int8-quantised tables, slices of 8 tokens
+        for (int64_t m0 = 0; m0 < M; m0 += bitnet::kElutMaxTokens) {
+            const int mc = (int)((M - m0) < bitnet::kElutMaxTokens ? (M - m0) : bitnet::kElutMaxTokens);
+            const hipError_t e =
+                layout == BITNET_LAYOUT_TL2_0
+                    ? bitnet::launch_tl2_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
+                                                     y + m0 * N, acc ? acc + m0 * N : nullptr, s, true)
+                    : bitnet::launch_tl1_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
+                                                     y + m0 * N, acc ? acc + m0 * N : nullptr, s, true);
+            if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
+        }
+        return ok();
+    }
     if (elut_layout(layout))   // table lookups of the integer-weight formats, any M (slices of 2 or 4 tokens)
         return hip_status(bitnet::launch_elut_generic(elut_format(layout), packed, w_scale, xq, x_scale, (int)M, (int)N,
                                                       (int)K, y, acc, s),
@@ -384,13 +405,16 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
 
     hipStream_t s = (hipStream_t)stream;
-    if (elut_layout(layout)) {
+    if (elut_layout(layout) || lossy_layout(layout)) {
         // the quantiser once, then the table lookups of each weight
         hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
-        for (int i = 0; i < n_linears && e == hipSuccess; ++i)
-            e = bitnet::launch_elut_generic(elut_format(layout), packed[i], w_scale[i], xq, x_scale, (int)M, (int)N[i],
-                                            (int)K, y[i], nullptr, s);
-        return hip_status(e, "bitnet_mpgemm_fused launch");
+        if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm_fused launch");
+        for (int i = 0; i < n_linears; ++i) {
+            const bitnet_status st = mpgemm_run(layout, packed[i], packed_bytes[i], w_scale[i], N[i], K, xq, x_scale,
+                                                x_rowsum, M, y[i], nullptr, nullptr, 0, s);
+            if (st != BITNET_OK) return st;
+        }
+        return ok();
     }
     // the small-batch regime (17..128 tokens, K <= 16384): the decode GEMV in token slices, for I2_S and TL1
     const bool sliced = i2s_tiled(layout) && bitnet::i2s_sliced_ok(M, K, true);

@@ -30,6 +30,7 @@ namespace {
 
 constexpr int kSlot = 32;                                   // bytes per triple (or pair) table
 constexpr int kTokenStride = (kTl2BlockK / 3 + 4) * kSlot;  // 128 triples + 4 skew slots per token
+constexpr int kTl1TokenStride = 32 * kSlot;                 // the 32 pair tables of a 64-k unit per token
 
 __device__ __forceinline__ int skewed_slot(int g) { return g + (g >> 5); }
 
@@ -70,7 +71,33 @@ __device__ __forceinline__ void store_table(uint8_t* slot, const uint32_t w[8]) 
 
 __device__ __forceinline__ int lds_i16(const uint8_t* p) { return (int)*reinterpret_cast<const int16_t*>(p); }
 
-template <int WAVES, int MT>
+// Lossy tables (TL2_0, TL1_0; Sec. 3.2.1): the smallest s >= 0 with max_abs <= 127 * 2^s, and an entry divided by
+// 2^s and rounded half to even (the product by 2^-s is exact in fp32, rintf rounds ties to even).
+__device__ __forceinline__ int lossy_shift_of(int max_abs) {
+    int s = 0;
+    while (max_abs > (127 << s)) ++s;
+    return s;
+}
+__device__ __forceinline__ int lossy_q(int e, int s) {
+    return s == 0 ? e : (int)rintf((float)e * __int_as_float((127 - s) << 23));
+}
+// The words of a table with every int16 entry quantised.
+__device__ __forceinline__ void quantize_words(uint32_t w[8], int s) {
+    if (s == 0) return;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int lo = (int)(int16_t)(w[i] & 0xFFFFu), hi = (int)(int16_t)(w[i] >> 16);
+        w[i] = pack16(lossy_q(lo, s), lossy_q(hi, s));
+    }
+}
+// Largest |entry| over the wave's tables of one token (each lane passes the largest of its own).
+__device__ __forceinline__ int wave_max_int(int v) {
+    return (int)wave_max_all((float)v);
+}
+
+// LOSSY (TL2_0, Sec. 3.2.1): each token's tables of a block (128 triples, or the 32 pairs of a TL1 unit) are
+// quantised to int8 with the block's power-of-two scale before the lookups, and the block's sum is scaled back.
+template <int WAVES, int MT, bool LOSSY>
 __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
     const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
     const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out) {
@@ -95,15 +122,29 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
         const v4u iw = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * lane));
         const uint32_t sw = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * lane));
         // tables of this block's 128 triples: lane builds triples lane and lane + 64
+        int shift[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) shift[m] = 0;
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
             if (m >= M) break;
             const int8_t* a = xq + (size_t)m * K + (size_t)blk * kTl2BlockK;
+            if constexpr (LOSSY) {
+                // the block's largest |entry| is the largest |a0| + |a1| + |a2| of its triples
+                int mx = 0;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int g = lane + 64 * h;
+                    mx = max(mx, abs((int)a[3 * g]) + abs((int)a[3 * g + 1]) + abs((int)a[3 * g + 2]));
+                }
+                shift[m] = lossy_shift_of(wave_max_int(mx));
+            }
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int g = lane + 64 * h;
                 uint32_t w[8];
                 triple_table(a[3 * g], a[3 * g + 1], a[3 * g + 2], w);
+                if constexpr (LOSSY) quantize_words(w, shift[m]);
                 store_table(lut + m * kTokenStride + skewed_slot(g) * kSlot, w);
             }
         }
@@ -113,6 +154,9 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
         // Lookups without branches: tokens past M (MT > M) read token 0's tables and are never stored, so all
         // 32 x MT reads of a lane can be in flight together (a guarded read per triple waits for each one).
         const uint8_t* base = lut + skewed_slot(32 * q) * kSlot;
+        int bsum[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) bsum[m] = 0;
 #pragma unroll
         for (int i = 0; i < 32; ++i) {
             const uint32_t word = i < 8 ? iw.x : i < 16 ? iw.y : i < 24 ? iw.z : iw.w;
@@ -120,11 +164,11 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
             const int msk = -(int)((sw >> i) & 1u);
             const uint8_t* e = base + i * kSlot + 2 * idx;
 #pragma unroll
-            for (int m = 0; m < MT; ++m) acc[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride) ^ msk;
+            for (int m = 0; m < MT; ++m) bsum[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride) ^ msk;
         }
         const int nneg = __popc(sw);
 #pragma unroll
-        for (int m = 0; m < MT; ++m) acc[m] += nneg;
+        for (int m = 0; m < MT; ++m) acc[m] += (bsum[m] + nneg) << shift[m];
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
@@ -136,25 +180,36 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
             const uint32_t word = *reinterpret_cast<const uint32_t*>(
                 tail_plane + ((size_t)rg * 64 * units + (size_t)lane * units + u) * 4);
             // pair tables of this unit's 32 pairs (k = three + 64u + 2p), lanes 0..31
+            int shift[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) shift[m] = 0;
 #pragma unroll
             for (int m = 0; m < MT; ++m) {
-                if (m < M && lane < 32) {
-                    const int8_t* b = xq + (size_t)m * K + three + kSubK * u + 2 * lane;
+                if (m >= M) break;
+                const int8_t* b = xq + (size_t)m * K + three + kSubK * u + 2 * (lane & 31);
+                if constexpr (LOSSY) shift[m] = lossy_shift_of(wave_max_int(lane < 32 ? abs((int)b[0]) + abs((int)b[1]) : 0));
+                if (lane < 32) {
                     uint32_t w[8];
                     pair_table(b[0], b[1], w);
+                    if constexpr (LOSSY) quantize_words(w, shift[m]);
                     store_table(lut + m * kTokenStride + lane * kSlot, w);
                 }
             }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            int usum[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) usum[m] = 0;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int code = (int)((word >> (4 * i)) & 15u);
                 const uint8_t* e = lut + (8 * q + i) * kSlot + 2 * code;
 #pragma unroll
-                for (int m = 0; m < MT; ++m) acc[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride);
+                for (int m = 0; m < MT; ++m) usum[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride);
             }
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[m] += usum[m] << shift[m];
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
@@ -185,6 +240,95 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
         for (int w = 0; w < WAVES; ++w) s += red[(w * 16 + m) * 16 + lane];
         const float sc = beta / x_scale[m];
         y[(size_t)m * N + n] = (float)s * sc;
+        if (acc_out) acc_out[(size_t)m * N + n] = s;
+    }
+}
+
+// The TL1 layout by table lookup (Algorithm TL1; Table 5), one work group per 16-row group: wave w takes the 64-k
+// units w, w + WAVES, ...; lanes 0..31 build the 9-entry tables of the unit's 32 pairs for up to 8 tokens, and
+// lane (r, q) looks up the 8 pairs of its word (row r, k = 16 q .. 16 q + 15 of the unit).  LOSSY (TL1_0,
+// Sec. 3.2.1): each token's tables of a unit are quantised to int8 with the unit's power-of-two scale and the
+// unit's sum is scaled back.
+template <int WAVES, int MT, bool LOSSY>
+__global__ __launch_bounds__(64 * WAVES) void tl1_elut_decode_kernel(
+    const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
+    const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int q = lane >> 4, r = lane & 15;
+    const int rg = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int nsub = K / kSubK;
+    const uint8_t* rgbase = packed + (size_t)rg * 4 * K;
+    uint8_t* lut = lds + (size_t)wave * M * kTl1TokenStride;
+
+    int acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = 0;
+
+    for (int u = wave; u < nsub; u += WAVES) {
+        // the lane's word of unit u: sub-tile j of block s, in the I2_S tiling
+        const int sb = u >> 2, j = u & 3;
+        const int T = min(4, nsub - 4 * sb);
+        const uint32_t word = *reinterpret_cast<const uint32_t*>(rgbase + (size_t)sb * 1024 + 4 * T * lane + 4 * j);
+        int shift[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) shift[m] = 0;
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            if (m >= M) break;
+            const int8_t* b = xq + (size_t)m * K + kSubK * u + 2 * (lane & 31);
+            if constexpr (LOSSY) shift[m] = lossy_shift_of(wave_max_int(lane < 32 ? abs((int)b[0]) + abs((int)b[1]) : 0));
+            if (lane < 32) {
+                uint32_t w[8];
+                pair_table(b[0], b[1], w);
+                if constexpr (LOSSY) quantize_words(w, shift[m]);
+                store_table(lut + m * kTl1TokenStride + lane * kSlot, w);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        int usum[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) usum[m] = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            // pair i of the word: byte i % 4, low nibble for i < 4; it is pair 8 q + i of the unit
+            const int code = (int)((word >> (8 * (i & 3) + 4 * (i >> 2))) & 15u);
+            const uint8_t* e = lut + (8 * q + i) * kSlot + 2 * code;
+#pragma unroll
+            for (int m = 0; m < MT; ++m) usum[m] += lds_i16(e + (m < M ? m : 0) * kTl1TokenStride);
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m) acc[m] += usum[m] << shift[m];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    }
+
+    // Reduce: over the four q quarters (lanes r, r+16, r+32, r+48), then over waves.
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        int v = acc[m];
+        v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 32, 64);
+        acc[m] = v;
+    }
+    __syncthreads();
+    int* red = reinterpret_cast<int*>(lds);
+    if (lane < 16) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+            if (m < M) red[(wave * 16 + m) * 16 + lane] = acc[m];
+    }
+    __syncthreads();
+    if (wave != 0 || lane >= 16) return;
+    const float beta = *w_scale;
+    const int n = rg * kRowsPerGroup + r;
+    for (int m = 0; m < M; ++m) {
+        int s = 0;
+        for (int w = 0; w < WAVES; ++w) s += red[(w * 16 + m) * 16 + lane];
+        y[(size_t)m * N + n] = (float)s * (beta / x_scale[m]);
         if (acc_out) acc_out[(size_t)m * N + n] = s;
     }
 }
@@ -960,43 +1104,101 @@ size_t tl2_elut_lds_bytes(int M) {
     return tables > red ? tables : red;
 }
 
-template <int MT>
+template <int MT, bool LOSSY>
 hipError_t launch_elut_mt(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
                           int N, int K, float* y, int32_t* acc, hipStream_t stream) {
     const unsigned grid = (unsigned)(N / kRowsPerGroup);
     const size_t lds = tl2_elut_lds_bytes(M);
     switch (tl2_elut_waves(M)) {
         case 16:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<16, MT>), dim3(grid), dim3(1024), lds, stream, pk, w_scale, xq,
-                               x_scale, M, N, K, y, acc);
+            hipLaunchKernelGGL((tl2_elut_decode_kernel<16, MT, LOSSY>), dim3(grid), dim3(1024), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
             break;
         case 8:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<8, MT>), dim3(grid), dim3(512), lds, stream, pk, w_scale, xq,
-                               x_scale, M, N, K, y, acc);
+            hipLaunchKernelGGL((tl2_elut_decode_kernel<8, MT, LOSSY>), dim3(grid), dim3(512), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
             break;
         case 4:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<4, MT>), dim3(grid), dim3(256), lds, stream, pk, w_scale, xq,
-                               x_scale, M, N, K, y, acc);
+            hipLaunchKernelGGL((tl2_elut_decode_kernel<4, MT, LOSSY>), dim3(grid), dim3(256), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
             break;
         case 2:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<2, MT>), dim3(grid), dim3(128), lds, stream, pk, w_scale, xq,
-                               x_scale, M, N, K, y, acc);
+            hipLaunchKernelGGL((tl2_elut_decode_kernel<2, MT, LOSSY>), dim3(grid), dim3(128), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
             break;
         default:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<1, MT>), dim3(grid), dim3(64), lds, stream, pk, w_scale, xq,
-                               x_scale, M, N, K, y, acc);
+            hipLaunchKernelGGL((tl2_elut_decode_kernel<1, MT, LOSSY>), dim3(grid), dim3(64), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
             break;
     }
     return hipGetLastError();
 }
 
+template <bool LOSSY>
+hipError_t launch_tl2_elut_lossy(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
+                                 int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    if (M <= 1) return launch_elut_mt<1, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    if (M <= 2) return launch_elut_mt<2, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    if (M <= 4) return launch_elut_mt<4, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    return launch_elut_mt<8, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+}
+
 hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                                  int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+                                  int M, int N, int K, float* y, int32_t* acc, hipStream_t stream, bool lossy) {
     const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    if (M <= 1) return launch_elut_mt<1>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (M <= 2) return launch_elut_mt<2>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (M <= 4) return launch_elut_mt<4>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    return launch_elut_mt<8>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    return lossy ? launch_tl2_elut_lossy<true>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream)
+                 : launch_tl2_elut_lossy<false>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+}
+
+// TL1 layout by table lookup (Algorithm TL1): the 32 pair tables of a 64-k unit per wave, lossy or not.
+int tl1_elut_waves(int M) {
+    int w = 16;
+    while (w > 1 && (size_t)w * M * kTl1TokenStride > 65536) w >>= 1;
+    return w;
+}
+
+size_t tl1_elut_lds_bytes(int M) {
+    const size_t tables = (size_t)tl1_elut_waves(M) * M * kTl1TokenStride;
+    const size_t red = (size_t)tl1_elut_waves(M) * 16 * 16 * sizeof(int);
+    return tables > red ? tables : red;
+}
+
+template <int MT, bool LOSSY>
+hipError_t launch_tl1_mt(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
+                         int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    const unsigned grid = (unsigned)(N / kRowsPerGroup);
+    const size_t lds = tl1_elut_lds_bytes(M);
+    switch (tl1_elut_waves(M)) {
+        case 16:
+            hipLaunchKernelGGL((tl1_elut_decode_kernel<16, MT, LOSSY>), dim3(grid), dim3(1024), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
+            break;
+        case 8:
+            hipLaunchKernelGGL((tl1_elut_decode_kernel<8, MT, LOSSY>), dim3(grid), dim3(512), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
+            break;
+        default:
+            hipLaunchKernelGGL((tl1_elut_decode_kernel<4, MT, LOSSY>), dim3(grid), dim3(256), lds, stream, pk,
+                               w_scale, xq, x_scale, M, N, K, y, acc);
+            break;
+    }
+    return hipGetLastError();
+}
+
+template <bool LOSSY>
+hipError_t launch_tl1_elut_lossy(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
+                                 int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    if (M <= 1) return launch_tl1_mt<1, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    if (M <= 2) return launch_tl1_mt<2, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    if (M <= 4) return launch_tl1_mt<4, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    return launch_tl1_mt<8, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+}
+
+hipError_t launch_tl1_elut_decode(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
+                                  int M, int N, int K, float* y, int32_t* acc, hipStream_t stream, bool lossy) {
+    const uint8_t* pk = static_cast<const uint8_t*>(packed);
+    return lossy ? launch_tl1_elut_lossy<true>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream)
+                 : launch_tl1_elut_lossy<false>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
 }
 
 size_t tl2_stream_lds_bytes(int K) {

@@ -35,6 +35,8 @@ def test_packed_bytes_match_layout_definitions(N, K):
     assert B.bitnet_packed_bytes("i2s", N, K) == O.i2s_packed_bytes(N, K)
     assert B.bitnet_packed_bytes("tl2", N, K) == O.tl2_packed_bytes(N, K)
     assert B.bitnet_packed_bytes("tl1", N, K) == O.tl1_packed_bytes(N, K)
+    assert B.bitnet_packed_bytes("tl2_0", N, K) == O.tl2_packed_bytes(N, K)      # the lossy kernels' formats
+    assert B.bitnet_packed_bytes("tl1_0", N, K) == O.tl1_packed_bytes(N, K)
     for fmt in O.ELUT_FORMATS:
         ok = K % (320 if fmt == "c3g5" else 64) == 0
         assert B.bitnet_packed_bytes(fmt, N, K) == (O.elut_packed_bytes(fmt, N, K) if ok else 0)
@@ -45,7 +47,7 @@ def test_packed_bytes_rejects_bad_shapes():
         assert B.bitnet_packed_bytes(layout, 15, 64) == 0
         assert B.bitnet_packed_bytes(layout, 16, 65) == 0
         assert B.bitnet_packed_bytes(layout, 0, 64) == 0
-    assert B.bitnet_packed_bytes(7, 16, 64) == 0
+    assert B.bitnet_packed_bytes(8, 16, 64) == 0
     assert B.bitnet_packed_bytes("c3g5", 16, 640) == 16 * 640 // 5 and B.bitnet_packed_bytes("c3g5", 16, 384) == 0
 
 
@@ -73,7 +75,7 @@ def _mpgemm(**kw):
 
 @cpu_only
 def test_mpgemm_validation_statuses():
-    assert _mpgemm(layout=9) == 4
+    assert _mpgemm(layout=9) == 4 and _mpgemm(layout=8) == 4
     assert _mpgemm(packed=None) == 1
     assert _mpgemm(y=None) == 1
     assert _mpgemm(N=40) == 2

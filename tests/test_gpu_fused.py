@@ -144,3 +144,25 @@ def test_fused_one_token_workload_groups(K, Ns):
 def test_fused_one_token_100b_groups(K, Ns):
     _announce("fused one token 100B-class", K, Ns)
     _fused_case(("i2s", "tl2", "tl1"), 1, K, Ns, seed=inputs.seed_for(4, 10 * len(Ns) + K % 7))
+
+
+def _fused_case_lossy(layout, M=3, K=1600, Ns=(64, 208)):
+    """bitnet_mpgemm_fused on a lossy layout: the quantiser, then each weight's lookups; equal to the separate calls
+    and to the oracle's lossy route."""
+    Ws = [inputs.weight_f32(N, K, seed=inputs.seed_for(15, 500 + i)) for i, N in enumerate(Ns)]
+    x = inputs.activation_f32(M, K, seed=inputs.seed_for(15, 599))
+    packs = [H.pack(W, layout) for W in Ws]
+    xq = torch.empty((M, K), dtype=torch.int8, device=H.DEV)
+    s = torch.empty(M, dtype=torch.float32, device=H.DEV)
+    rs = torch.empty(M, dtype=torch.int32, device=H.DEV)
+    ys = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
+    B.bitnet_mpgemm_fused(layout, [p for p, _ in packs], [b for _, b in packs], x.to(H.DEV), xq, s, rs, ys)
+    xq_ref, s_ref = O.quantize_act(x.numpy())
+    route = O.elut_gemm_lossy if layout == "tl2_0" else O.elut_gemm_tl1_lossy
+    pack = O.pack_tl2 if layout == "tl2_0" else O.pack_tl1
+    for W, (p, b), y, N in zip(Ws, packs, ys, Ns):
+        t_ref, beta = O.ternarize(W.numpy())
+        acc_ref = route(xq_ref, pack(t_ref), N, K)
+        H.check_y(H.to_np(y), O.epilogue(acc_ref, beta, s_ref), acc_ref)
+        y_sep, _ = H.mpgemm(layout, p, b, N, K, xq, s)
+        assert np.array_equal(H.to_np(y), H.to_np(y_sep))
