@@ -461,7 +461,7 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (rgs > ((int64_t)1 << 30)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
     bitnet::seal_fused(L);
     const bool tl2 = layout == BITNET_LAYOUT_TL2;
-    if (tl2 && M == 1 && quantise && bitnet::tl2_mfma_max_tokens((int)K) > 0)
+    if (tl2 && M == 1 && quantise && bitnet::tl2_mfma_quant_fits((int)K))
         return hip_status(bitnet::launch_tl2_mfma_quant(L, x, (int)K, xq, x_scale, x_rowsum, s),
                           "bitnet_mpgemm_fused launch");
     if (tl2 && M == 1 && bitnet::tl2_stream_fits((int)K)) {

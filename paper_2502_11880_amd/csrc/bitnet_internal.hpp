@@ -249,10 +249,12 @@ hipError_t launch_elut_tables(const int8_t* xq, int M, int K, int16_t* lut, int1
 // read.  Only where the whole row's tables fit in LDS (tl2_stream_fits); the caller falls back otherwise.
 bool tl2_stream_fits(int K);
 // Up to kTl2MfmaMaxTokens tokens per launch (already quantised), TL2 weights expanded to int8 for MFMA; every
-// weight of a group in one launch.  tl2_mfma_max_tokens(K) is the slice one launch takes at this K (0: the path
-// does not cover K: fewer than one or more than 48 384-k blocks); the launcher slices M itself.
+// weight of a group in one launch.  tl2_mfma_max_tokens(K) is the slice one launch takes at this K (0: K has no
+// 384-k block, or one token's codes do not fit in LDS); the launcher slices M itself.  Past 48 blocks a row group
+// takes several batches.
 constexpr int kTl2MfmaMaxTokens = 16;
 int tl2_mfma_max_tokens(int K);
+bool tl2_mfma_quant_fits(int K);      // launch_tl2_mfma_quant covers this K
 hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const float* x_scale, int M, int K,
                                   hipStream_t stream);
 hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,

@@ -359,7 +359,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_stream_kernel(FusedLinears L, 
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int q = lane >> 4, r = lane & 15;
+    const int q = lane >> 4;
     const int G = gridDim.x, bid = blockIdx.x;
     const int three = (K / kTl2BlockK) * kTl2BlockK;
     const int nblk = three / kTl2BlockK;
@@ -636,7 +636,11 @@ __device__ __forceinline__ void expand_triples(const v4u& iw, uint32_t sw, const
 // XV = 0: the codes and scales are read (xq, x_scale).  XV > 0: one token (M = 1), its fp32 row x quantised here
 // (Sec. 2.1; XV float4 per thread), as in the single-token I2_S kernel: the row is loaded before the first weights,
 // reduced to its absmax through LDS and converted into the LDS codes; work group 0 writes xq, x_scale, x_rowsum.
-template <int WAVES, int U, int CH, int XV>
+//
+// MB (K past 48 blocks): a row group takes nb = ceil(nblk / (WAVES U)) batches of WAVES U blocks, walked as the steps
+// of the stream (the accumulators carry over a row group's batches; its last batch holds the TL1 tail and the
+// reduction), and the codes of every token are copied whole into LDS.
+template <int WAVES, int U, int CH, int XV, bool MB>
 __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinears L, const float* __restrict__ x,
                                                                      int8_t* xq, float* x_scale,
                                                                      int32_t* x_rowsum, int M, int K) {
@@ -653,7 +657,15 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
     const int nblk = three / kTl2BlockK;                       // >= 1 (the launcher checks)
     const int units = (K - three) / kSubK;
     const int tail_wave = nblk % WAVES;                        // a wave with the fewest blocks
-    const int S = (L.total - bid + G - 1) / G;                 // row groups of this work group (grid <= total)
+    constexpr int kPerBatch = WAVES * U;
+    const int nb = MB ? (nblk + kPerBatch - 1) / kPerBatch : 1;  // batches per row group
+    const int S = ((L.total - bid + G - 1) / G) * nb;          // steps of this work group (grid <= total)
+    // step st = batch b of row group g
+    auto step_gb = [&](int st, int& g, int& b) {
+        const int gi = MB ? st / nb : st;
+        b = MB ? st - gi * nb : 0;
+        g = bid + gi * G;
+    };
     const int stride = K + 16;
     const uint2* itab = reinterpret_cast<const uint2*>(lds);
     const uint32_t* ptab = reinterpret_cast<const uint32_t*>(lds + kIdxTableBytes);
@@ -663,15 +675,16 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
     // waves other than the tail wave, and of units past `units`, repeat one real word)
     const bool tail_mine = wave == tail_wave && units > 0;
     auto issue = [&](v4u (&iw)[U], uint32_t (&sw)[U], uint32_t (&tw)[kMaxUnits], float& bw, int st) {
-        int li, rg;
-        locate(L, bid + st * G, li, rg);
+        int g, b, li, rg;
+        step_gb(st, g, b);
+        locate(L, g, li, rg);
         const size_t Nl = (size_t)pick(L.N, li);
         const uint8_t* idx_plane = pick(L.packed, li);
         const uint8_t* sign_plane = idx_plane + Nl * (three / 6);
         const uint8_t* tail_plane = sign_plane + Nl * (three / 24);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const size_t tile = (size_t)rg * nblk + min(wave + WAVES * u, nblk - 1);
+            const size_t tile = (size_t)rg * nblk + min(b * kPerBatch + wave + WAVES * u, nblk - 1);
             iw[u] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * lane));
             sw[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * lane));
         }
@@ -784,12 +797,15 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
     const v4i zero = {0, 0, 0, 0};
     const int8_t* arow = xs + (r < M ? r : 0) * stride;
     int par = 0;
+    v4i acc = zero;
     auto compute = [&](const v4u (&iw)[U], const uint32_t (&sw)[U], const uint32_t (&tw)[kMaxUnits], float bw,
                        int st) {
-        v4i acc = zero;
+        int g, b;
+        step_gb(st, g, b);
+        if (b == 0) acc = zero;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int blk = wave + WAVES * u;
+            const int blk = b * kPerBatch + wave + WAVES * u;
             if (blk < nblk) {
                 uint32_t wd[24];
                 expand_triples(iw[u], sw[u], itab, wd);
@@ -801,6 +817,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
                 }
             }
         }
+        if (b < nb - 1) return;      // the row group's last batch: the tail and the reduction
         if (tail_mine) {
 #pragma unroll
             for (int t = 0; t < kMaxUnits; ++t) {
@@ -819,7 +836,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
 #pragma unroll 4
             for (int w2 = 1; w2 < WAVES; ++w2) tot += part[par][w2][lane];
             int li, rg;
-            locate(L, bid + st * G, li, rg);
+            locate(L, g, li, rg);
             const int N = pick(L.N, li);
             const int n = rg * kRowsPerGroup + r;
             float* y = pick(L.y, li);
@@ -846,17 +863,27 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
         float ba = 0.0f, bb = 0.0f;
         // codes loaded ahead of the weights where their registers fit beside them (one token-group of chunks per
         // wave), after them otherwise
-        constexpr bool kEarly = XV == 0 && U * CH <= 3;
+        constexpr bool kEarly = XV == 0 && !MB && U * CH <= 3;
         load_tables();
         if constexpr (XV > 0) load_row();
         else if constexpr (kEarly) load_codes();
         issue(iwa, swa, twa, ba, 0);
         if constexpr (kMulti) issue(iwb, swb, twb, bb, 1);
         __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the tables and the conversion
-        if constexpr (XV == 0 && !kEarly) load_codes();
+        if constexpr (XV == 0 && !MB && !kEarly) load_codes();
         store_tables();
-        if constexpr (XV > 0) quantise_row();
-        else store_codes();
+        if constexpr (XV > 0) {
+            quantise_row();
+        } else if constexpr (MB) {
+            // every token's codes, whole (16-byte chunks; K % 64 == 0)
+            const int kc = K / 16;
+            for (int ch = tid; ch < M * kc; ch += 64 * WAVES) {
+                const int m = ch / kc, k = 16 * (ch - m * kc);
+                *reinterpret_cast<v4i*>(xs + m * stride + k) = *reinterpret_cast<const v4i*>(xq + (size_t)m * K + k);
+            }
+        } else {
+            store_codes();
+        }
         __syncthreads();                                   // the tables (and codes) are shared by every wave
         if (XV > 0 && bid == 0 && tid == 0) {
             int tot = 0;
@@ -1254,26 +1281,34 @@ size_t tl2_mfma_lds_bytes(int M, int K) { return (size_t)kTl2MfmaTables + (size_
 
 int tl2_mfma_max_tokens(int K) {
     const int nblk = K / kTl2BlockK;
-    if (nblk < 1 || nblk > kTl2MfmaMaxBlocks) return 0;
+    if (nblk < 1) return 0;
     const int waves = nblk <= 4 ? 4 : nblk <= 16 ? 8 : 16;
     const size_t budget = 160 * 1024 - (size_t)2 * waves * 64 * 16 - 256;   // less the reduction buffers
-    // past 32 blocks (three per wave) the staging registers allow 8 tokens per slice
+    // past 32 blocks (three per wave) the staging registers allow 8 tokens per slice; past 48 blocks (row groups
+    // in several batches) only LDS limits the slice
     for (int m = nblk > 32 ? 8 : kTl2MfmaMaxTokens; m >= 1; --m)
         if (tl2_mfma_lds_bytes(m, K) <= budget) return m;
     return 0;
 }
 
-template <int WAVES, int U, int CH, int XV>
+bool tl2_mfma_quant_fits(int K) {
+    // one token quantised inside: the fp32 row in registers, at most 8 float4 per thread of 16 waves (16 float4
+    // beside two batches of weight words need a stack frame, and that kernel ran 2.5x slower than the quantiser
+    // followed by the kernel that reads the codes)
+    return tl2_mfma_max_tokens(K) >= 1 && K / 4 <= 8 * 64 * 16;
+}
+
+template <int WAVES, int U, int CH, int XV, bool MB = false>
 hipError_t launch_mfma_kernel(const FusedLinears& L, const float* x, int8_t* xq, float* x_scale, int32_t* x_rowsum,
                               int M, int K, hipStream_t stream) {
     const size_t lds = tl2_mfma_lds_bytes(M, K);
-    const void* kern = reinterpret_cast<const void*>(tl2_mfma_decode_kernel<WAVES, U, CH, XV>);
+    const void* kern = reinterpret_cast<const void*>(tl2_mfma_decode_kernel<WAVES, U, CH, XV, MB>);
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * WAVES, lds) != hipSuccess || occ <= 0) occ = 1;
     const int64_t max_g = (int64_t)device_cus() * occ;
     const int64_t rounds = (L.total + max_g - 1) / max_g;
     const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * WAVES);
-    hipLaunchKernelGGL((tl2_mfma_decode_kernel<WAVES, U, CH, XV>), grid, block, lds, stream, L, x, xq, x_scale,
+    hipLaunchKernelGGL((tl2_mfma_decode_kernel<WAVES, U, CH, XV, MB>), grid, block, lds, stream, L, x, xq, x_scale,
                        x_rowsum, M, K);
     return hipGetLastError();
 }
@@ -1299,11 +1334,18 @@ hipError_t launch_mfma_quant(const FusedLinears& L, const float* x, int8_t* xq, 
     return launch_mfma_kernel<WAVES, U, 1, 8>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
 }
 
-// One token, quantised inside (tl2_mfma_max_tokens(K) >= 1).
+// One token quantised inside, row groups in several batches (K past 48 blocks, K / 4 <= 8192).
+hipError_t launch_mfma_quant_mb(const FusedLinears& L, const float* x, int8_t* xq, float* x_scale,
+                                int32_t* x_rowsum, int K, hipStream_t stream) {
+    return launch_mfma_kernel<16, 3, 1, 8, true>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
+}
+
+// One token, quantised inside (tl2_mfma_quant_fits(K)).
 hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                                  int32_t* x_rowsum, hipStream_t stream) {
     const int nblk = K / kTl2BlockK;
-    if (tl2_mfma_max_tokens(K) < 1) return hipErrorInvalidValue;
+    if (!tl2_mfma_quant_fits(K)) return hipErrorInvalidValue;
+    if (nblk > kTl2MfmaMaxBlocks) return launch_mfma_quant_mb(L, x, xq, x_scale, x_rowsum, K, stream);
     if (nblk <= 4) return launch_mfma_quant<4, 1>(L, x, xq, x_scale, x_rowsum, K, stream);
     if (nblk <= 8) return launch_mfma_quant<4, 2>(L, x, xq, x_scale, x_rowsum, K, stream);
     if (nblk <= 12) return launch_mfma_quant<4, 3>(L, x, xq, x_scale, x_rowsum, K, stream);
@@ -1328,7 +1370,10 @@ hipError_t launch_tl2_mfma_decode(const FusedLinears& L, const int8_t* xq, const
         const int8_t* xs = xq + (size_t)m0 * K;
         const float* ss = x_scale + m0;
         hipError_t e;
-        if (nblk <= 4) e = launch_mfma_cfg<4, 1>(Ls, xs, ss, m, K, stream);
+        if (nblk > kTl2MfmaMaxBlocks)
+            e = launch_mfma_kernel<16, 3, 3, 0, true>(Ls, nullptr, const_cast<int8_t*>(xs), const_cast<float*>(ss),
+                                                      nullptr, m, K, stream);
+        else if (nblk <= 4) e = launch_mfma_cfg<4, 1>(Ls, xs, ss, m, K, stream);
         else if (nblk <= 8) e = launch_mfma_cfg<8, 1>(Ls, xs, ss, m, K, stream);
         else if (nblk <= 16) e = launch_mfma_cfg<8, 2>(Ls, xs, ss, m, K, stream);
         else if (nblk <= 32) e = launch_mfma_cfg<16, 2>(Ls, xs, ss, m, K, stream);

@@ -122,10 +122,13 @@ def test_tl2_stream_one_token(N, K):
 
 # One token as one launch for several weights that share the activation, quantised inside the launch (the MFMA
 # kernel with the row converted in each work group): every wave configuration, 1 to 8 float4 of the row per
-# thread (K = 16512: five, rounded up to eight), with and without a TL1 tail.
+# thread (K = 16512: five, rounded up to eight), with and without a TL1 tail; past 48 blocks, row groups in two or
+# three batches with 8 float4 per thread (K = 19264 with a 1-unit tail; K = 32768, the longest such row), and past
+# 8 float4 per thread the quantiser followed by the multi-batch kernel (K = 33024; K = 65472 with a 3-unit tail).
 @pytest.mark.parametrize("K,Ns", [(3200, [3200, 3200, 3200]), (4096, [4096, 1024, 1024]), (8640, [3200, 16]),
                                   (14336, [4096]), (1536, [64, 48]), (16512, [32]), (448, [2400]),
-                                  (2304, [48]), (4480, [64, 32])])
+                                  (2304, [48]), (4480, [64, 32]), (19264, [48]), (32768, [64, 16]),
+                                  (33024, [64, 16]), (65472, [32])])
 def test_tl2_one_token_fused(K, Ns):
     _announce("tl2 one token fused", K, Ns)
     from tests.test_gpu_fused import _fused_case
@@ -135,11 +138,15 @@ def test_tl2_one_token_fused(K, Ns):
 # Several tokens through the MFMA kernel (triples expanded to int8 through the LDS tables): every wave / blocks-per-
 # wave configuration (4x1, 8x1, 8x2, 16x2, 16x3), TL1 tails of 1 to 5 units, 1 to 16 tokens per launch (both
 # staging widths), token slices (16 tokens at K = 14336 take two launches of 8; 40 tokens take 16 + 16 + 8), one
-# token where the single-token streaming kernel's tables do not fit (K = 16384), and past the kernel's 48 blocks
-# the table-lookup kernel (K = 19200).
+# token where the single-token streaming kernel's tables do not fit (K = 16384); past 48 blocks, row groups in
+# several batches with token slices sized to LDS (K = 19200 and 19264: 50 blocks, the second with a 1-unit tail;
+# K = 33024: three tokens per slice; K = 20480: five per slice and a 2-unit tail; K = 65600: one per slice; K = 121536:
+# the longest row whose codes fit), and past that the table-lookup kernel (K = 132096, the largest K).
 @pytest.mark.parametrize("M,N,K", [(2, 48, 832), (3, 64, 1600), (8, 96, 1536), (4, 208, 3200), (16, 64, 4096),
                                    (9, 32, 8640), (12, 48, 6080), (5, 16, 14336), (16, 32, 14336), (40, 48, 4096),
-                                   (1, 64, 16384), (2, 16, 19200), (7, 16, 384)])
+                                   (1, 64, 16384), (2, 16, 19200), (7, 16, 384), (1, 64, 19264), (3, 48, 33024),
+                                   (8, 32, 33024), (16, 16, 20480), (2, 16, 65600), (1, 16, 121536),
+                                   (1, 16, 132096)])
 def test_tl2_mfma_decode(M, N, K):
     _announce("tl2 mfma decode", M, N, K)
     _tl2_vs_oracle(M, N, K, seed=inputs.seed_for(8, 900 + M * 17 + N + K))
