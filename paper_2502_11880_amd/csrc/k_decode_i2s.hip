@@ -330,6 +330,9 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
         constexpr int kDepth = decltype(depth)::value;
         v4u wa[U], wb[U];
         float ba = 0.0f, bb = 0.0f;
+        // every wave's code loads enter the memory pipeline before any weight load (else the last waves' codes
+        // queue behind the first waves' weight batches)
+        __builtin_amdgcn_s_barrier();
         issue(wa, ba, 0);
         if constexpr (kDepth == 1) {
             stage();
@@ -429,6 +432,9 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
             const float4 v = x4[e < K4 ? e : K4 - 1];
             xv[i] = e < K4 ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         }
+        // every wave's row loads enter the memory pipeline before any weight load: without this barrier the last
+        // waves' row loads queue behind the first waves' weight batches, and the quantisation waits for them
+        __builtin_amdgcn_s_barrier();
         // two batches in flight before the quantisation (steps 0 and 1), or one when there is only one step
         v4u wa[U], wb[U];
         float ba = 0.0f, bb = 0.0f;

@@ -867,6 +867,9 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
         load_tables();
         if constexpr (XV > 0) load_row();
         else if constexpr (kEarly) load_codes();
+        // every wave's row (or code) loads enter the memory pipeline before any weight load, so that no wave's
+        // activation waits behind the other waves' weight batches
+        if constexpr (XV > 0 || kEarly) __builtin_amdgcn_s_barrier();
         issue(iwa, swa, twa, ba, 0);
         if constexpr (kMulti) issue(iwb, swb, twb, bb, 1);
         __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the tables and the conversion
