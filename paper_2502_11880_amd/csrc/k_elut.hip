@@ -17,7 +17,9 @@
 // activation codes staged in LDS) before the lanes look their groups up.  Table entry e of group p of token t
 // sits at ((t E' + e) * GB + q) with q = (p mod GW) * 64 + p / GW, so the 64 lanes of a wave reading item i of
 // their words touch 64 consecutive entries when their codes agree.  Each lane keeps one int32 sum per row and
-// token; a wave reduction and the epilogue y = acc * beta / s_t finish each row.
+// token; a wave reduction and the epilogue y = acc * beta / s_t finish each row.  The kernel instance builds the
+// tables of exactly the launch's tokens, and the next block's words and codes are loaded while the current block's
+// tables are built and read.
 #include "bitnet_internal.hpp"
 
 namespace bitnet {
@@ -44,27 +46,33 @@ struct ElutFmt<kElutC3G5> {
 constexpr int kEW = 16;                  // waves per work group
 constexpr int kEThreads = 64 * kEW;
 
-// Weight j of table entry e (the oracle's elut_entry_weights): base-C digits offset by the set's minimum, or the
-// balanced base-C digits of e with mirroring; weight 0 is the most significant digit.
+// Weight j of every table entry e, as a compile-time table: the base-C digits of e offset by the set's minimum, or
+// with mirroring the balanced base-C digits of e; weight 0 is the most significant digit.  A table entry is then a
+// sum of the group's codes with constant coefficients.
 template <int F>
-__device__ __forceinline__ int entry_weight(int e, int j) {
-    using T = ElutFmt<F>;
-    int v = e, d = 0;
-    for (int i = T::G - 1; i >= j; --i) {
-        if (T::kMirror) {
-            int r = v % T::C;
-            if (r > T::C / 2) r -= T::C;
-            d = r;
-            v = (v - r) / T::C;
-        } else {
-            d = v % T::C - T::C / 2;
-            v /= T::C;
+struct DigitTable {
+    int8_t d[ElutFmt<F>::E][ElutFmt<F>::G];
+    constexpr DigitTable() : d{} {
+        using T = ElutFmt<F>;
+        for (int e = 0; e < T::E; ++e) {
+            int v = e;
+            for (int j = T::G - 1; j >= 0; --j) {
+                int r = 0;
+                if (T::kMirror) {
+                    r = v % T::C;
+                    if (r > T::C / 2) r -= T::C;
+                    v = (v - r) / T::C;
+                } else {
+                    r = v % T::C - T::C / 2;
+                    v /= T::C;
+                }
+                d[e][j] = (int8_t)r;
+            }
         }
     }
-    return d;
-}
+};
 
-template <int F, int RS>
+template <int F, int RS, int MT>
 __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* __restrict__ packed,
                                                                  const float* __restrict__ w_scale,
                                                                  const int8_t* __restrict__ xq,
@@ -74,10 +82,12 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
     using T = ElutFmt<F>;
     constexpr int GB = 64 * T::GW;                // groups per block
     constexpr int KB = GB * T::G;                 // weights per block
-    constexpr int kTab = T::MT * T::EP * GB;      // int16 entries
+    constexpr int kTab = MT * T::EP * GB;         // int16 entries
+    constexpr int kXw = MT * (KB / 4);            // 32-bit words of activation codes per block
+    static_assert(kXw <= kEThreads, "one word of codes per thread and block");
     __shared__ int16_t tab[kTab];
-    __shared__ __align__(16) int8_t xs[T::MT][KB];
-    __shared__ int8_t dig[T::E][T::G];
+    __shared__ __align__(16) int8_t xs[MT][KB];
+    constexpr DigitTable<F> kDig{};
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -87,55 +97,77 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
     const size_t row_bytes = T::GW == 8 ? (size_t)K / 4 : (size_t)K / 5;   // index plane (c4g2, c5g2) or bytes
     const uint8_t* sign_plane = packed + (size_t)N * K / 4;                   // c5g2 only
 
-    for (int i = tid; i < T::E * T::G; i += kEThreads) dig[i / T::G][i % T::G] = (int8_t)entry_weight<F>(i / T::G, i % T::G);
+    // The loads of block kb: this wave's packed words (lane l: word l of each of its rows) and one word of the
+    // block's activation codes per thread (token tid / (KB/4)).  Addresses are clamped to real words and the
+    // values past the block, the rows or the tokens zeroed, so every load is unconditional.
+    auto load_block = [&](int kb, uint32_t (&wv)[RS], uint32_t (&sv)[RS], uint32_t& xv) {
+        const int gin = min(GB, Gtot - kb * GB);
+        const int words = (gin + T::GW - 1) / T::GW;
+        const int kin = gin * T::G;
+        const int l = min(lane, words - 1);
+#pragma unroll
+        for (int r = 0; r < RS; ++r) {
+            const int n = min(row0 + r, N - 1);
+            const bool ok = row0 + r < N && lane < words;
+            const uint32_t w = *reinterpret_cast<const uint32_t*>(packed + (size_t)n * row_bytes + (size_t)kb * 256 + 4 * l);
+            wv[r] = ok ? w : 0u;
+            if constexpr (F == kElutC5G2) {
+                const uint32_t sg = sign_plane[(size_t)n * (K / 16) + (size_t)kb * 64 + l];
+                sv[r] = ok ? sg : 0u;
+            } else {
+                sv[r] = 0u;
+            }
+        }
+        const int t = tid / (KB / 4), w = tid - t * (KB / 4);
+        const bool xok = tid < kXw && t < M && 4 * w < kin;
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(xq + (size_t)min(t, M - 1) * K + (size_t)kb * KB +
+                                                              min(4 * w, kin - 4));
+        xv = xok ? v : 0u;
+    };
 
-    int acc[RS][T::MT];
+    int acc[RS][MT];
 #pragma unroll
     for (int r = 0; r < RS; ++r)
 #pragma unroll
-        for (int t = 0; t < T::MT; ++t) acc[r][t] = 0;
+        for (int t = 0; t < MT; ++t) acc[r][t] = 0;
 
+    // Block kb + 1's loads are issued before block kb's tables are built, so they land during its arithmetic.
+    uint32_t wn[RS], sn[RS], xn;
+    load_block(0, wn, sn, xn);
     for (int kb = 0; kb < nblk; ++kb) {
-        const int gin = min(GB, Gtot - kb * GB);             // groups in this block
-        const int words = (gin + T::GW - 1) / T::GW;         // packed words per row in this block
-        // 1. this wave's packed words of the block (loads in flight while the tables are built)
         uint32_t wv[RS], sv[RS];
 #pragma unroll
         for (int r = 0; r < RS; ++r) {
-            const int n = row0 + r;
-            wv[r] = 0u;
-            sv[r] = 0u;
-            if (n < N && lane < words) {
-                wv[r] = *reinterpret_cast<const uint32_t*>(packed + (size_t)n * row_bytes + (size_t)kb * 256 + 4 * lane);
-                if constexpr (F == kElutC5G2) sv[r] = sign_plane[(size_t)n * (K / 16) + (size_t)kb * 64 + lane];
-            }
+            wv[r] = wn[r];
+            sv[r] = sn[r];
         }
-        // 2. the block's activation codes into LDS (after every wave is done with the previous block's tables)
+        const uint32_t xv = xn;
+        const int gin = min(GB, Gtot - kb * GB);             // groups in this block
+        const int words = (gin + T::GW - 1) / T::GW;         // packed words per row in this block
+        // 1. the block's activation codes into LDS (after every wave is done with the previous block's tables)
         __syncthreads();
-        const int kin = gin * T::G;
-        for (int i = tid; i < T::MT * (KB / 4); i += kEThreads) {
-            const int t = i / (KB / 4), w = i % (KB / 4);
-            uint32_t v = 0u;
-            if (t < M && 4 * w < kin)
-                v = *reinterpret_cast<const uint32_t*>(xq + (size_t)t * K + (size_t)kb * KB + 4 * w);
-            reinterpret_cast<uint32_t*>(xs[t])[w] = v;
-        }
+        if (tid < kXw) reinterpret_cast<uint32_t*>(&xs[0][0])[tid] = xv;
+        load_block(min(kb + 1, nblk - 1), wn, sn, xn);
         __syncthreads();
-        // 3. the tables: entry e of group p of token t = sum_j d_j(e) a_j
-        for (int i = tid; i < T::MT * T::E * GB; i += kEThreads) {
-            const int q = i % GB;
-            const int te = i / GB;
-            const int e = te % T::E, t = te / T::E;
+        // 2. the tables: one thread per token and group reads the group's codes once and writes all its entries,
+        //    entry e = sum_j d_j(e) a_j with the digits as constants (groups past the block give zeros)
+        for (int i = tid; i < MT * GB; i += kEThreads) {
+            const int q = i % GB, t = i / GB;
             const int p = (q % 64) * T::GW + q / 64;
-            int v = 0;
-            if (p < gin) {
+            int a[T::G];
 #pragma unroll
-                for (int j = 0; j < T::G; ++j) v += (int)dig[e][j] * (int)xs[t][p * T::G + j];
+            for (int j = 0; j < T::G; ++j) a[j] = p < gin ? (int)xs[t][p * T::G + j] : 0;
+            int16_t* col = tab + (size_t)t * T::EP * GB + q;
+#pragma unroll
+            for (int e = 0; e < T::E; ++e) {
+                int v = 0;
+#pragma unroll
+                for (int j = 0; j < T::G; ++j) v += (int)kDig.d[e][j] * a[j];
+                col[e * GB] = (int16_t)v;
             }
-            tab[(t * T::EP + e) * GB + q] = (int16_t)v;
         }
         __syncthreads();
-        // 4. lookups: item i of lane l's word is group l GW + i, at table column i 64 + l
+        // 3. lookups: item i of lane l's word is group l GW + i, at table column i 64 + l
         if (lane < words) {
 #pragma unroll
             for (int r = 0; r < RS; ++r) {
@@ -152,7 +184,7 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
                     }
                     const int col = i * 64 + lane;
 #pragma unroll
-                    for (int t = 0; t < T::MT; ++t) {
+                    for (int t = 0; t < MT; ++t) {
                         const int v = tab[(t * T::EP + idx) * GB + col];
                         acc[r][t] += (v + m) ^ m;            // Eq. 5: the sign bit widened to a mask
                     }
@@ -160,12 +192,12 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
             }
         }
     }
-    // 5. every row's sum over the lanes, then the epilogue
+    // 4. every row's sum over the lanes, then the epilogue
 #pragma unroll
     for (int r = 0; r < RS; ++r) {
         const int n = row0 + r;
 #pragma unroll
-        for (int t = 0; t < T::MT; ++t) {
+        for (int t = 0; t < MT; ++t) {
             const int total = wave_sum_all(acc[r][t]);
             if (lane == 0 && n < N && t < M) {
                 y[(size_t)t * N + n] = (float)total * (*w_scale / x_scale[t]);
@@ -206,17 +238,30 @@ __global__ __launch_bounds__(256) void pack_elut_words(const int8_t* __restrict_
     if constexpr (F == kElutC5G2) packed[(size_t)N * K / 4 + n * (K / 16) + w] = (uint8_t)sign;
 }
 
+template <int F, int RS, int MT>
+hipError_t launch_elut_mt(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
+                          int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+    const dim3 grid((unsigned)((N + kEW * RS - 1) / (kEW * RS))), block(kEThreads);
+    hipLaunchKernelGGL((elut_generic_kernel<F, RS, MT>), grid, block, 0, stream, static_cast<const uint8_t*>(packed),
+                       w_scale, xq, x_scale, M, N, K, y, acc);
+    return hipGetLastError();
+}
+
+// Tokens in slices of up to T::MT per launch; the kernel instance builds tables for exactly the slice's tokens
+// (1, 2 or 4).
 template <int F, int RS>
 hipError_t launch_elut_rs(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
                           int N, int K, float* y, int32_t* acc, hipStream_t stream) {
     using T = ElutFmt<F>;
-    const dim3 grid((unsigned)((N + kEW * RS - 1) / (kEW * RS))), block(kEThreads);
     for (int m0 = 0; m0 < M; m0 += T::MT) {
         const int mc = M - m0 < T::MT ? M - m0 : T::MT;
-        hipLaunchKernelGGL((elut_generic_kernel<F, RS>), grid, block, 0, stream,
-                           static_cast<const uint8_t*>(packed), w_scale, xq + (size_t)m0 * K, x_scale + m0, mc, N, K,
-                           y + (size_t)m0 * N, acc ? acc + (size_t)m0 * N : nullptr);
-        const hipError_t e = hipGetLastError();
+        const int8_t* xs = xq + (size_t)m0 * K;
+        float* ys = y + (size_t)m0 * N;
+        int32_t* as = acc ? acc + (size_t)m0 * N : nullptr;
+        hipError_t e;
+        if (mc == 1) e = launch_elut_mt<F, RS, 1>(packed, w_scale, xs, x_scale + m0, mc, N, K, ys, as, stream);
+        else if (mc == 2 || T::MT < 4) e = launch_elut_mt<F, RS, 2>(packed, w_scale, xs, x_scale + m0, mc, N, K, ys, as, stream);
+        else e = launch_elut_mt<F, RS, (T::MT >= 4 ? 4 : 2)>(packed, w_scale, xs, x_scale + m0, mc, N, K, ys, as, stream);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
