@@ -31,6 +31,9 @@ namespace {
 constexpr int kSlot = 32;                                   // bytes per triple (or pair) table
 constexpr int kTokenStride = (kTl2BlockK / 3 + 4) * kSlot;  // 128 triples + 4 skew slots per token
 constexpr int kTl1TokenStride = 32 * kSlot;                 // the 32 pair tables of a 64-k unit per token
+constexpr int kElutLdsBudget = 144 * 1024;                  // tables of a table-lookup work group
+// Tokens whose TL2 tables a wave holds at once (16 waves x 2 x 4.1 KiB fit the budget).
+constexpr int tl2_elut_chunk(int mt) { return mt < 2 ? mt : 2; }
 
 __device__ __forceinline__ int skewed_slot(int g) { return g + (g >> 5); }
 
@@ -102,6 +105,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
     const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
     const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     extern __shared__ __align__(16) uint8_t lds[];
+    constexpr int TC = tl2_elut_chunk(MT);      // tokens whose tables share LDS at a time
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = lane >> 4, r = lane & 15;
     const int rg = xcd_logical_id(blockIdx.x, gridDim.x);
@@ -111,7 +115,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
     const uint8_t* idx_plane = packed;
     const uint8_t* sign_plane = packed + (size_t)N * (three / 6);
     const uint8_t* tail_plane = sign_plane + (size_t)N * (three / 24);
-    uint8_t* lut = lds + (size_t)wave * M * kTokenStride;
+    uint8_t* lut = lds + (size_t)wave * TC * kTokenStride;
 
     int acc[MT];                                 // MT >= M tokens; loops run to MT with uniform guards
 #pragma unroll
@@ -121,57 +125,60 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
         const size_t tile = (size_t)rg * nblk + blk;
         const v4u iw = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(idx_plane + tile * 1024 + 16 * lane));
         const uint32_t sw = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(sign_plane + tile * 256 + 4 * lane));
-        // tables of this block's 128 triples: lane builds triples lane and lane + 64
-        int shift[MT];
+        const int nneg = __popc(sw);
+        // tokens in chunks of TC: the chunk's tables of this block's 128 triples (lane builds triples lane and
+        // lane + 64), then its lookups
 #pragma unroll
-        for (int m = 0; m < MT; ++m) shift[m] = 0;
+        for (int c = 0; c < MT; c += TC) {
+            if (c >= M) break;
+            int shift[TC];
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-            if (m >= M) break;
-            const int8_t* a = xq + (size_t)m * K + (size_t)blk * kTl2BlockK;
-            if constexpr (LOSSY) {
-                // the block's largest |entry| is the largest |a0| + |a1| + |a2| of its triples
-                int mx = 0;
+            for (int j = 0; j < TC; ++j) shift[j] = 0;
+#pragma unroll
+            for (int j = 0; j < TC; ++j) {
+                const int m = c + j;
+                if (m >= M) break;
+                const int8_t* a = xq + (size_t)m * K + (size_t)blk * kTl2BlockK;
+                if constexpr (LOSSY) {
+                    // the block's largest |entry| is the largest |a0| + |a1| + |a2| of its triples
+                    int mx = 0;
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int g = lane + 64 * h;
+                        mx = max(mx, abs((int)a[3 * g]) + abs((int)a[3 * g + 1]) + abs((int)a[3 * g + 2]));
+                    }
+                    shift[j] = lossy_shift_of(wave_max_int(mx));
+                }
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     const int g = lane + 64 * h;
-                    mx = max(mx, abs((int)a[3 * g]) + abs((int)a[3 * g + 1]) + abs((int)a[3 * g + 2]));
+                    uint32_t w[8];
+                    triple_table(a[3 * g], a[3 * g + 1], a[3 * g + 2], w);
+                    if constexpr (LOSSY) quantize_words(w, shift[j]);
+                    store_table(lut + j * kTokenStride + skewed_slot(g) * kSlot, w);
                 }
-                shift[m] = lossy_shift_of(wave_max_int(mx));
+            }
+            wave_lds_handoff();
+            // Lookups without branches: tokens past M read the chunk's first tables and are never stored, so all
+            // 32 x TC reads of a lane can be in flight together (a guarded read per triple waits for each one).
+            const uint8_t* base = lut + skewed_slot(32 * q) * kSlot;
+            int bsum[TC];
+#pragma unroll
+            for (int j = 0; j < TC; ++j) bsum[j] = 0;
+#pragma unroll
+            for (int i = 0; i < 32; ++i) {
+                const uint32_t word = i < 8 ? iw.x : i < 16 ? iw.y : i < 24 ? iw.z : iw.w;
+                const int idx = (int)((word >> (4 * (i & 7))) & 15u);
+                const int msk = -(int)((sw >> i) & 1u);
+                const uint8_t* e = base + i * kSlot + 2 * idx;
+#pragma unroll
+                for (int j = 0; j < TC; ++j) bsum[j] += lds_i16(e + (c + j < M ? j : 0) * kTokenStride) ^ msk;
             }
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int g = lane + 64 * h;
-                uint32_t w[8];
-                triple_table(a[3 * g], a[3 * g + 1], a[3 * g + 2], w);
-                if constexpr (LOSSY) quantize_words(w, shift[m]);
-                store_table(lut + m * kTokenStride + skewed_slot(g) * kSlot, w);
-            }
+            for (int j = 0; j < TC; ++j)
+                if (c + j < MT) acc[c + j] += (bsum[j] + nneg) << shift[j];
+            wave_lds_handoff();
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-        // Lookups without branches: tokens past M (MT > M) read token 0's tables and are never stored, so all
-        // 32 x MT reads of a lane can be in flight together (a guarded read per triple waits for each one).
-        const uint8_t* base = lut + skewed_slot(32 * q) * kSlot;
-        int bsum[MT];
-#pragma unroll
-        for (int m = 0; m < MT; ++m) bsum[m] = 0;
-#pragma unroll
-        for (int i = 0; i < 32; ++i) {
-            const uint32_t word = i < 8 ? iw.x : i < 16 ? iw.y : i < 24 ? iw.z : iw.w;
-            const int idx = (int)((word >> (4 * (i & 7))) & 15u);
-            const int msk = -(int)((sw >> i) & 1u);
-            const uint8_t* e = base + i * kSlot + 2 * idx;
-#pragma unroll
-            for (int m = 0; m < MT; ++m) bsum[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride) ^ msk;
-        }
-        const int nneg = __popc(sw);
-#pragma unroll
-        for (int m = 0; m < MT; ++m) acc[m] += (bsum[m] + nneg) << shift[m];
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     }
 
     // TL1 tail (K mod 384 weights): handled by the wave after the last TL2 block.
@@ -179,40 +186,43 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
         for (int u = 0; u < units; ++u) {
             const uint32_t word = *reinterpret_cast<const uint32_t*>(
                 tail_plane + ((size_t)rg * 64 * units + (size_t)lane * units + u) * 4);
-            // pair tables of this unit's 32 pairs (k = three + 64u + 2p), lanes 0..31
-            int shift[MT];
 #pragma unroll
-            for (int m = 0; m < MT; ++m) shift[m] = 0;
+            for (int c = 0; c < MT; c += TC) {
+                if (c >= M) break;
+                // pair tables of this unit's 32 pairs (k = three + 64u + 2p), lanes 0..31
+                int shift[TC];
 #pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                if (m >= M) break;
-                const int8_t* b = xq + (size_t)m * K + three + kSubK * u + 2 * (lane & 31);
-                if constexpr (LOSSY) shift[m] = lossy_shift_of(wave_max_int(lane < 32 ? abs((int)b[0]) + abs((int)b[1]) : 0));
-                if (lane < 32) {
-                    uint32_t w[8];
-                    pair_table(b[0], b[1], w);
-                    if constexpr (LOSSY) quantize_words(w, shift[m]);
-                    store_table(lut + m * kTokenStride + lane * kSlot, w);
+                for (int j = 0; j < TC; ++j) shift[j] = 0;
+#pragma unroll
+                for (int j = 0; j < TC; ++j) {
+                    const int m = c + j;
+                    if (m >= M) break;
+                    const int8_t* b = xq + (size_t)m * K + three + kSubK * u + 2 * (lane & 31);
+                    if constexpr (LOSSY)
+                        shift[j] = lossy_shift_of(wave_max_int(lane < 32 ? abs((int)b[0]) + abs((int)b[1]) : 0));
+                    if (lane < 32) {
+                        uint32_t w[8];
+                        pair_table(b[0], b[1], w);
+                        if constexpr (LOSSY) quantize_words(w, shift[j]);
+                        store_table(lut + j * kTokenStride + lane * kSlot, w);
+                    }
                 }
+                wave_lds_handoff();
+                int usum[TC];
+#pragma unroll
+                for (int j = 0; j < TC; ++j) usum[j] = 0;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int code = (int)((word >> (4 * i)) & 15u);
+                    const uint8_t* e = lut + (8 * q + i) * kSlot + 2 * code;
+#pragma unroll
+                    for (int j = 0; j < TC; ++j) usum[j] += lds_i16(e + (c + j < M ? j : 0) * kTokenStride);
+                }
+#pragma unroll
+                for (int j = 0; j < TC; ++j)
+                    if (c + j < MT) acc[c + j] += usum[j] << shift[j];
+                wave_lds_handoff();
             }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-            int usum[MT];
-#pragma unroll
-            for (int m = 0; m < MT; ++m) usum[m] = 0;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int code = (int)((word >> (4 * i)) & 15u);
-                const uint8_t* e = lut + (8 * q + i) * kSlot + 2 * code;
-#pragma unroll
-                for (int m = 0; m < MT; ++m) usum[m] += lds_i16(e + (m < M ? m : 0) * kTokenStride);
-            }
-#pragma unroll
-            for (int m = 0; m < MT; ++m) acc[m] += usum[m] << shift[m];
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
         }
     }
 
@@ -1122,14 +1132,15 @@ __global__ __launch_bounds__(256) void elut_tables_kernel(const int8_t* __restri
 }  // namespace
 
 int tl2_elut_waves(int M) {
-    // Each wave holds M * kTokenStride bytes of tables; stay within 64 KiB per work group.
+    // Each wave holds the tables of a chunk of tokens (kTokenStride bytes each); stay within the LDS budget.
+    const int tc = tl2_elut_chunk(M);
     int w = 16;
-    while (w > 1 && (size_t)w * M * kTokenStride > 65536) w >>= 1;
+    while (w > 1 && (size_t)w * tc * kTokenStride > (size_t)kElutLdsBudget) w >>= 1;
     return w;
 }
 
 size_t tl2_elut_lds_bytes(int M) {
-    const size_t tables = (size_t)tl2_elut_waves(M) * M * kTokenStride;
+    const size_t tables = (size_t)tl2_elut_waves(M) * tl2_elut_chunk(M) * kTokenStride;
     const size_t red = (size_t)tl2_elut_waves(M) * 16 * 16 * sizeof(int);
     return tables > red ? tables : red;
 }
@@ -1183,7 +1194,7 @@ hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, cons
 // TL1 layout by table lookup (Algorithm TL1): the 32 pair tables of a 64-k unit per wave, lossy or not.
 int tl1_elut_waves(int M) {
     int w = 16;
-    while (w > 1 && (size_t)w * M * kTl1TokenStride > 65536) w >>= 1;
+    while (w > 1 && (size_t)w * M * kTl1TokenStride > (size_t)kElutLdsBudget) w >>= 1;
     return w;
 }
 
