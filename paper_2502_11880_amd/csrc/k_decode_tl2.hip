@@ -30,7 +30,6 @@ namespace {
 
 constexpr int kSlot = 32;                                   // bytes per triple (or pair) table
 constexpr int kTokenStride = (kTl2BlockK / 3 + 4) * kSlot;  // 128 triples + 4 skew slots per token
-constexpr int kTl1TokenStride = 32 * kSlot;                 // the 32 pair tables of a 64-k unit per token
 constexpr int kElutLdsBudget = 144 * 1024;                  // tables of a table-lookup work group
 // Tokens whose TL2 tables a wave holds at once (16 waves x 2 x 4.1 KiB fit the budget).
 constexpr int tl2_elut_chunk(int mt) { return mt < 2 ? mt : 2; }
@@ -254,66 +253,115 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
     }
 }
 
-// The TL1 layout by table lookup (Algorithm TL1; Table 5), one work group per 16-row group: wave w takes the 64-k
-// units w, w + WAVES, ...; lanes 0..31 build the 9-entry tables of the unit's 32 pairs for up to 8 tokens, and
-// lane (r, q) looks up the 8 pairs of its word (row r, k = 16 q .. 16 q + 15 of the unit).  LOSSY (TL1_0,
-// Sec. 3.2.1): each token's tables of a unit are quantised to int8 with the unit's power-of-two scale and the
-// unit's sum is scaled back.
+// The TL1 layout by table lookup (Algorithm TL1; Table 5), one work group per 16-row group: wave w takes the 256-k
+// blocks w, w + WAVES, ... (four 64-k units each, the last block possibly fewer); lane l builds the 9-entry tables
+// of pair l % 32 of units l / 32 and 2 + l / 32, for a chunk of up to two tokens at a time, and lane (r, q) looks
+// up the 8 pairs of each of its block's words (row r, k = 64 j + 16 q .. + 15 of unit j).  LOSSY (TL1_0, Sec. 3.2.1):
+// each token's tables of a unit are quantised to int8 with the unit's power-of-two scale and the unit's sum is
+// scaled back.
+constexpr int kTl1BlockStride = 128 * kSlot;                 // the 128 pair tables of a 256-k block per token
+
+// Largest value of each half-wave (lanes 0..31 and 32..63) of v, as scalars: DPP maxima inside each row of 16 lanes,
+// then the four row results read from lanes 0, 16, 32 and 48.
+__device__ __forceinline__ void half_wave_max(int v, int& lo, int& hi) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v = max(v, dpp_row_step(v, i));
+    lo = max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16));
+    hi = max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48));
+}
+
 template <int WAVES, int MT, bool LOSSY>
 __global__ __launch_bounds__(64 * WAVES) void tl1_elut_decode_kernel(
     const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
     const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     extern __shared__ __align__(16) uint8_t lds[];
+    constexpr int TC = tl2_elut_chunk(MT);      // tokens whose tables share LDS at a time
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = lane >> 4, r = lane & 15;
+    const int pr = lane & 31, hh = lane >> 5;  // this lane builds pair pr of units hh and 2 + hh
     const int rg = xcd_logical_id(blockIdx.x, gridDim.x);
     const int nsub = K / kSubK;
+    const int nkb = (nsub + 3) / 4;
     const uint8_t* rgbase = packed + (size_t)rg * 4 * K;
-    uint8_t* lut = lds + (size_t)wave * M * kTl1TokenStride;
+    uint8_t* lut = lds + (size_t)wave * TC * kTl1BlockStride;
 
     int acc[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) acc[m] = 0;
 
-    for (int u = wave; u < nsub; u += WAVES) {
-        // the lane's word of unit u: sub-tile j of block s, in the I2_S tiling
-        const int sb = u >> 2, j = u & 3;
-        const int T = min(4, nsub - 4 * sb);
-        const uint32_t word = *reinterpret_cast<const uint32_t*>(rgbase + (size_t)sb * 1024 + 4 * T * lane + 4 * j);
-        int shift[MT];
+    for (int sb = wave; sb < nkb; sb += WAVES) {
+        const int T = min(4, nsub - 4 * sb);   // units of this block
+        // the lane's word of unit j: word j of its 4 T bytes in the I2_S tiling (units past T repeat a real word)
+        uint32_t word[4];
 #pragma unroll
-        for (int m = 0; m < MT; ++m) shift[m] = 0;
+        for (int j = 0; j < 4; ++j)
+            word[j] = *reinterpret_cast<const uint32_t*>(rgbase + (size_t)sb * 1024 + 4 * T * lane + 4 * min(j, T - 1));
+        const bool ok0 = hh < T, ok1 = 2 + hh < T;
+        const int u0 = min(hh, T - 1), u1 = min(2 + hh, T - 1);
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-            if (m >= M) break;
-            const int8_t* b = xq + (size_t)m * K + kSubK * u + 2 * (lane & 31);
-            if constexpr (LOSSY) shift[m] = lossy_shift_of(wave_max_int(lane < 32 ? abs((int)b[0]) + abs((int)b[1]) : 0));
-            if (lane < 32) {
+        for (int c = 0; c < MT; c += TC) {
+            if (c >= M) break;
+            int sh[TC][4];
+#pragma unroll
+            for (int jj = 0; jj < TC; ++jj)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) sh[jj][j] = 0;
+#pragma unroll
+            for (int jj = 0; jj < TC; ++jj) {
+                const int m = c + jj;
+                if (m >= M) break;
+                const int8_t* xb = xq + (size_t)m * K + (size_t)sb * kI2sBlockK + 2 * pr;
+                const int a0 = xb[kSubK * u0], a1 = xb[kSubK * u0 + 1];
+                const int b0 = xb[kSubK * u1], b1 = xb[kSubK * u1 + 1];
+                if constexpr (LOSSY) {
+                    int lo0, hi0, lo1, hi1;
+                    half_wave_max(ok0 ? abs(a0) + abs(a1) : 0, lo0, hi0);
+                    half_wave_max(ok1 ? abs(b0) + abs(b1) : 0, lo1, hi1);
+                    sh[jj][0] = lossy_shift_of(lo0);
+                    sh[jj][1] = lossy_shift_of(hi0);
+                    sh[jj][2] = lossy_shift_of(lo1);
+                    sh[jj][3] = lossy_shift_of(hi1);
+                }
                 uint32_t w[8];
-                pair_table(b[0], b[1], w);
-                if constexpr (LOSSY) quantize_words(w, shift[m]);
-                store_table(lut + m * kTl1TokenStride + lane * kSlot, w);
+                uint8_t* tj = lut + jj * kTl1BlockStride;
+                if (ok0) {
+                    pair_table(a0, a1, w);
+                    if constexpr (LOSSY) quantize_words(w, hh ? sh[jj][1] : sh[jj][0]);
+                    store_table(tj + (32 * hh + pr) * kSlot, w);
+                }
+                if (ok1) {
+                    pair_table(b0, b1, w);
+                    if constexpr (LOSSY) quantize_words(w, hh ? sh[jj][3] : sh[jj][2]);
+                    store_table(tj + (64 + 32 * hh + pr) * kSlot, w);
+                }
             }
+            wave_lds_handoff();
+            // lookups: tokens past M read the chunk's first tables and are never stored
+            int usum[TC][4];
+#pragma unroll
+            for (int jj = 0; jj < TC; ++jj)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) usum[jj][j] = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (j >= T) break;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    // pair i of the word: byte i % 4, low nibble for i < 4; it is pair 8 q + i of unit j
+                    const int code = (int)((word[j] >> (8 * (i & 3) + 4 * (i >> 2))) & 15u);
+                    const uint8_t* e = lut + (32 * j + 8 * q + i) * kSlot + 2 * code;
+#pragma unroll
+                    for (int jj = 0; jj < TC; ++jj)
+                        usum[jj][j] += lds_i16(e + (c + jj < M ? jj : 0) * kTl1BlockStride);
+                }
+            }
+#pragma unroll
+            for (int jj = 0; jj < TC; ++jj)
+                if (c + jj < MT)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[c + jj] += usum[jj][j] << sh[jj][j];
+            wave_lds_handoff();
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-        int usum[MT];
-#pragma unroll
-        for (int m = 0; m < MT; ++m) usum[m] = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            // pair i of the word: byte i % 4, low nibble for i < 4; it is pair 8 q + i of the unit
-            const int code = (int)((word >> (8 * (i & 3) + 4 * (i >> 2))) & 15u);
-            const uint8_t* e = lut + (8 * q + i) * kSlot + 2 * code;
-#pragma unroll
-            for (int m = 0; m < MT; ++m) usum[m] += lds_i16(e + (m < M ? m : 0) * kTl1TokenStride);
-        }
-#pragma unroll
-        for (int m = 0; m < MT; ++m) acc[m] += usum[m] << shift[m];
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     }
 
     // Reduce: over the four q quarters (lanes r, r+16, r+32, r+48), then over waves.
@@ -1193,13 +1241,14 @@ hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, cons
 
 // TL1 layout by table lookup (Algorithm TL1): the 32 pair tables of a 64-k unit per wave, lossy or not.
 int tl1_elut_waves(int M) {
+    const int tc = tl2_elut_chunk(M);
     int w = 16;
-    while (w > 1 && (size_t)w * M * kTl1TokenStride > (size_t)kElutLdsBudget) w >>= 1;
+    while (w > 1 && (size_t)w * tc * kTl1BlockStride > (size_t)kElutLdsBudget) w >>= 1;
     return w;
 }
 
 size_t tl1_elut_lds_bytes(int M) {
-    const size_t tables = (size_t)tl1_elut_waves(M) * M * kTl1TokenStride;
+    const size_t tables = (size_t)tl1_elut_waves(M) * tl2_elut_chunk(M) * kTl1BlockStride;
     const size_t red = (size_t)tl1_elut_waves(M) * 16 * 16 * sizeof(int);
     return tables > red ? tables : red;
 }
