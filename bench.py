@@ -20,7 +20,8 @@ bound "hbm".  Prefill: `value` = int8 TOP/s of the step (2*M*N*K per linear), `r
 10th/50th/90th percentile of the per-step time over ten replays of the same graph (the first is the timed one).
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload, with every host thread and with one.
 `parity` checks the timed launches themselves (the first activation group's fused call, in the first, middle and
-last layer) on every output against the oracle.
+last layer) on every output against the oracle.  The default run also measures the 8B-class layer set at 2048 tokens
+(I2_S prefill) in a child process started first and adds it as `prefill_extra` (`--no-extra` skips it).
 """
 from __future__ import annotations
 
@@ -50,6 +51,8 @@ def parse():
     p.add_argument("--layout", default="i2s", choices=["i2s", "tl2", "tl1", "c4g2", "c5g2", "c3g5", "tl2_0", "tl1_0"])
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extra", action="store_true",
+                   help="skip the 2048-token prefill figure that the default run adds to its line")
     p.add_argument("--no-parity", action="store_true")
     p.add_argument("--replays", type=int, default=10, help="replays of the timed graph for the spread figure")
     return p.parse_args()
@@ -86,12 +89,42 @@ def activation_groups(by_name, inputs):
     return groups + [[n] for n in by_name if n not in listed]
 
 
+def prefill_extra(args):
+    """The default run also reports the 8B-class layer set at 2048 tokens (I2_S prefill), measured by this script in
+    a child process started before this one touches the GPU; None when skipped or when the child fails."""
+    if args.no_extra or args.workload != 4 or args.tokens is not None or args.layout != "i2s":
+        return None
+    import subprocess
+
+    log("prefill figure (8B-class layer set, 2048 tokens) in a child process")
+    cmd = [sys.executable, os.path.abspath(__file__), "--workload", "3", "--tokens", "2048", "--no-cpu-baseline",
+           "--no-extra"]
+    if args.no_parity:
+        cmd.append("--no-parity")
+    try:
+        res = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=600)
+        line = [ln for ln in res.stdout.splitlines() if ln.startswith("{")][-1] if res.returncode == 0 else None
+    except (subprocess.TimeoutExpired, IndexError):
+        line = None
+    if line is None:
+        log("prefill figure: child run failed; reported as null")
+        return None
+    d = json.loads(line)
+    r = d["roofline"]
+    return {"workload": d["config"]["workload"], "tokens": d["config"]["tokens"], "layout": d["config"]["layout"],
+            "value": d["value"], "unit": d["unit"], "ms_per_step": d["ms_per_step"],
+            "gemm_only_ms_per_step": d.get("gemm_only_ms_per_step"),
+            "roofline": {k: r.get(k) for k in ("bound", "kernel", "achieved", "peak", "unit", "frac", "traffic")},
+            "parity_pass": (d.get("parity") or {}).get("pass")}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+    extra = prefill_extra(args)
 
     import torch
 
@@ -336,6 +369,8 @@ def main():
         "cpu_baseline": cpu,
         "parity": parity,
     }
+    if extra is not None:
+        out["prefill_extra"] = extra
     print(json.dumps(out), flush=True)
 
 
