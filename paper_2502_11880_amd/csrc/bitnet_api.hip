@@ -248,8 +248,8 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
         return ok();
     }
     if (elut_layout(layout))   // table lookups of the integer-weight formats, any M (slices of 2 or 4 tokens)
-        return hip_status(bitnet::launch_elut_generic(elut_format(layout), packed, w_scale, xq, x_scale, (int)M, (int)N,
-                                                      (int)K, y, acc, s),
+        return hip_status(bitnet::launch_elut_generic(elut_format(layout), one_linear(packed, w_scale, N, y, acc), nullptr,
+                                                      xq, x_scale, (int)M, (int)K, nullptr, nullptr, nullptr, s),
                           "bitnet_mpgemm launch");
     if (i2s_tiled(layout) && (M <= kDecodeMaxTokens || bitnet::i2s_sliced_ok(M, K, x_rowsum != nullptr)))
         return hip_status(bitnet::launch_i2s_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, x_rowsum,
@@ -405,7 +405,33 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
 
     hipStream_t s = (hipStream_t)stream;
-    if (elut_layout(layout) || lossy_layout(layout)) {
+    if (elut_layout(layout)) {
+        // every weight of the group in one table-lookup launch; one token quantised inside it, else the quantiser
+        // first
+        bitnet::FusedLinears L{};
+        L.count = n_linears;
+        int64_t rgs = 0;
+        for (int i = 0; i < n_linears; ++i) {
+            L.packed[i] = static_cast<const uint8_t*>(packed[i]);
+            L.w_scale[i] = w_scale[i];
+            L.y[i] = y[i];
+            L.acc[i] = nullptr;
+            L.N[i] = (int)N[i];
+            rgs += N[i] / bitnet::kRowsPerGroup;
+        }
+        if (rgs > ((int64_t)1 << 26)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
+        bitnet::seal_fused(L);
+        const int fmt = elut_format(layout);
+        if (quantise && M == 1)
+            return hip_status(bitnet::launch_elut_generic(fmt, L, x, nullptr, nullptr, 1, (int)K, xq, x_scale, x_rowsum,
+                                                          s),
+                              "bitnet_mpgemm_fused launch");
+        hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
+        if (e == hipSuccess)
+            e = bitnet::launch_elut_generic(fmt, L, nullptr, xq, x_scale, (int)M, (int)K, nullptr, nullptr, nullptr, s);
+        return hip_status(e, "bitnet_mpgemm_fused launch");
+    }
+    if (lossy_layout(layout)) {
         // the quantiser once, then the table lookups of each weight
         hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
         if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm_fused launch");

@@ -267,12 +267,15 @@ hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_
                              int32_t* x_rowsum, hipStream_t stream);
 
 // ELUT for integer weights of other cardinalities: formats c4g2, c5g2 and c3g5 (table lookups, up to 4 tokens per
-// launch for the 2-weight groups and 2 for c3g5; the launcher slices M).
+// launch for the 2-weight groups and 2 for c3g5; the launcher slices M).  Every weight of L in one launch.  With x
+// (fp32, one token) the launch quantises the row itself and writes xq_out, s_out and rs_out as the quantiser would;
+// otherwise it reads xq and x_scale (M tokens).
 constexpr int kElutC4G2 = 0;
 constexpr int kElutC5G2 = 1;
 constexpr int kElutC3G5 = 2;
-hipError_t launch_elut_generic(int fmt, const void* packed, const float* w_scale, const int8_t* xq,
-                               const float* x_scale, int M, int N, int K, float* y, int32_t* acc, hipStream_t stream);
+hipError_t launch_elut_generic(int fmt, const FusedLinears& L, const float* x, const int8_t* xq,
+                               const float* x_scale, int M, int K, int8_t* xq_out, float* s_out, int32_t* rs_out,
+                               hipStream_t stream);
 hipError_t launch_pack_elut(int fmt, const int8_t* Wq, int N, int K, void* packed, hipStream_t stream);
 
 

@@ -72,47 +72,90 @@ struct DigitTable {
     }
 };
 
-template <int F, int RS, int MT>
-__global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* __restrict__ packed,
-                                                                 const float* __restrict__ w_scale,
+// One launch serves every weight of a fused group (rows concatenated, each row's weight found by a scalar compare
+// chain), since the tables depend only on the activation.  QX (one token): the work group quantises the fp32 row
+// itself (Sec. 2.1): the row's absmax first (a pass over the row, L2-resident after the first work groups), then
+// every block's codes from its fp32 values as the block is staged; work group 0 writes the codes, the scale and
+// their sum, as the quantiser would.
+template <int F, int RS, int MT, bool QX>
+__global__ __launch_bounds__(kEThreads) void elut_generic_kernel(FusedLinears L, const float* __restrict__ x,
                                                                  const int8_t* __restrict__ xq,
-                                                                 const float* __restrict__ x_scale, int M, int N,
-                                                                 int K, float* __restrict__ y,
-                                                                 int32_t* __restrict__ acc_out) {
+                                                                 const float* __restrict__ x_scale, int M, int K,
+                                                                 int8_t* __restrict__ xq_out, float* __restrict__ s_out,
+                                                                 int32_t* __restrict__ rs_out) {
     using T = ElutFmt<F>;
     constexpr int GB = 64 * T::GW;                // groups per block
     constexpr int KB = GB * T::G;                 // weights per block
     constexpr int kTab = MT * T::EP * GB;         // int16 entries
     constexpr int kXw = MT * (KB / 4);            // 32-bit words of activation codes per block
     static_assert(kXw <= kEThreads, "one word of codes per thread and block");
+    static_assert(!QX || MT == 1, "the fused quantiser takes one token");
     __shared__ int16_t tab[kTab];
     __shared__ __align__(16) int8_t xs[MT][KB];
+    __shared__ float redf[kEW];
+    __shared__ int redi[kEW];
     constexpr DigitTable<F> kDig{};
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int Gtot = K / T::G;                    // groups per row
     const int nblk = (Gtot + GB - 1) / GB;
+    const int rows = L.total * kRowsPerGroup;     // rows of all the launch's weights
     const int row0 = blockIdx.x * (kEW * RS) + wave * RS;
     const size_t row_bytes = T::GW == 8 ? (size_t)K / 4 : (size_t)K / 5;   // index plane (c4g2, c5g2) or bytes
-    const uint8_t* sign_plane = packed + (size_t)N * K / 4;                   // c5g2 only
+
+    // this wave's rows: weight, row within it, packed row and (c5g2) sign row; rows past the last are clamped
+    // to it and never stored
+    int rli[RS], rn[RS];
+    const uint8_t* rpk[RS];
+    const uint8_t* rsg[RS];
+#pragma unroll
+    for (int r = 0; r < RS; ++r) {
+        const int nc = min(row0 + r, rows - 1);
+        int li, rg;
+        locate(L, nc / kRowsPerGroup, li, rg);
+        rli[r] = li;
+        rn[r] = rg * kRowsPerGroup + nc % kRowsPerGroup;
+        const uint8_t* base = pick(L.packed, li);
+        rpk[r] = base + (size_t)rn[r] * row_bytes;
+        rsg[r] = base + (size_t)pick(L.N, li) * K / 4 + (size_t)rn[r] * (K / 16);   // c5g2 only
+    }
+
+    // QX: the row's scale (the quantiser's formula) before the first block
+    float sx = 1.0f;
+    int csum = 0;                                 // QX, work group 0: this thread's share of the code sum
+    if constexpr (QX) {
+        const float4* x4 = reinterpret_cast<const float4*>(x);
+        float amax = 0.0f;
+        for (int i = tid; i < K / 4; i += kEThreads) {
+            const float4 v = x4[i];
+            amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+        }
+        amax = wave_max_all(amax);
+        if (lane == 0) redf[wave] = amax;
+        __syncthreads();
+        amax = redf[0];
+#pragma unroll
+        for (int w = 1; w < kEW; ++w) amax = fmaxf(amax, redf[w]);
+        sx = 127.0f / fmaxf(amax, 1e-5f);
+    }
 
     // The loads of block kb: this wave's packed words (lane l: word l of each of its rows) and one word of the
-    // block's activation codes per thread (token tid / (KB/4)).  Addresses are clamped to real words and the
-    // values past the block, the rows or the tokens zeroed, so every load is unconditional.
-    auto load_block = [&](int kb, uint32_t (&wv)[RS], uint32_t (&sv)[RS], uint32_t& xv) {
+    // block's activation codes per thread (token tid / (KB/4)), or with QX the float4 it quantises.  Addresses are
+    // clamped to real words and the values past the block, the rows or the tokens zeroed, so every load is
+    // unconditional.
+    auto load_block = [&](int kb, uint32_t (&wv)[RS], uint32_t (&sv)[RS], uint32_t& xv, float4& xf) {
         const int gin = min(GB, Gtot - kb * GB);
         const int words = (gin + T::GW - 1) / T::GW;
         const int kin = gin * T::G;
         const int l = min(lane, words - 1);
 #pragma unroll
         for (int r = 0; r < RS; ++r) {
-            const int n = min(row0 + r, N - 1);
-            const bool ok = row0 + r < N && lane < words;
-            const uint32_t w = *reinterpret_cast<const uint32_t*>(packed + (size_t)n * row_bytes + (size_t)kb * 256 + 4 * l);
+            const bool ok = row0 + r < rows && lane < words;
+            const uint32_t w = *reinterpret_cast<const uint32_t*>(rpk[r] + (size_t)kb * 256 + 4 * l);
             wv[r] = ok ? w : 0u;
             if constexpr (F == kElutC5G2) {
-                const uint32_t sg = sign_plane[(size_t)n * (K / 16) + (size_t)kb * 64 + l];
+                const uint32_t sg = rsg[r][(size_t)kb * 64 + l];
                 sv[r] = ok ? sg : 0u;
             } else {
                 sv[r] = 0u;
@@ -120,9 +163,15 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
         }
         const int t = tid / (KB / 4), w = tid - t * (KB / 4);
         const bool xok = tid < kXw && t < M && 4 * w < kin;
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(xq + (size_t)min(t, M - 1) * K + (size_t)kb * KB +
-                                                              min(4 * w, kin - 4));
-        xv = xok ? v : 0u;
+        const size_t off = (size_t)kb * KB + min(4 * w, kin - 4);
+        if constexpr (QX) {
+            const float4 v = *reinterpret_cast<const float4*>(x + off);
+            xf = xok ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            xv = 0u;
+        } else {
+            const uint32_t v = *reinterpret_cast<const uint32_t*>(xq + (size_t)min(t, M - 1) * K + off);
+            xv = xok ? v : 0u;
+        }
     };
 
     int acc[RS][MT];
@@ -133,7 +182,8 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
 
     // Block kb + 1's loads are issued before block kb's tables are built, so they land during its arithmetic.
     uint32_t wn[RS], sn[RS], xn;
-    load_block(0, wn, sn, xn);
+    float4 xfn;
+    load_block(0, wn, sn, xn, xfn);
     for (int kb = 0; kb < nblk; ++kb) {
         uint32_t wv[RS], sv[RS];
 #pragma unroll
@@ -141,13 +191,24 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
             wv[r] = wn[r];
             sv[r] = sn[r];
         }
-        const uint32_t xv = xn;
+        uint32_t xv = xn;
+        if constexpr (QX) {
+            // the block's codes from its fp32 values (zeros past the block quantise to zero codes)
+            xv = quant4(xfn, sx);
+            if (blockIdx.x == 0 && tid < kXw) {
+                const int kin = min(GB, Gtot - kb * GB) * T::G;
+                if (4 * tid < kin) {
+                    reinterpret_cast<uint32_t*>(xq_out + (size_t)kb * KB)[tid] = xv;
+                    csum = byte_sum4(xv, csum);
+                }
+            }
+        }
         const int gin = min(GB, Gtot - kb * GB);             // groups in this block
         const int words = (gin + T::GW - 1) / T::GW;         // packed words per row in this block
         // 1. the block's activation codes into LDS (after every wave is done with the previous block's tables)
         __syncthreads();
         if (tid < kXw) reinterpret_cast<uint32_t*>(&xs[0][0])[tid] = xv;
-        load_block(min(kb + 1, nblk - 1), wn, sn, xn);
+        load_block(min(kb + 1, nblk - 1), wn, sn, xn, xfn);
         __syncthreads();
         // 2. the tables: one thread per token and group reads the group's codes once and writes all its entries,
         //    entry e = sum_j d_j(e) a_j with the digits as constants (groups past the block give zeros)
@@ -195,13 +256,30 @@ __global__ __launch_bounds__(kEThreads) void elut_generic_kernel(const uint8_t* 
     // 4. every row's sum over the lanes, then the epilogue
 #pragma unroll
     for (int r = 0; r < RS; ++r) {
-        const int n = row0 + r;
+        const int li = rli[r], n = rn[r], N = pick(L.N, li);
+        const float beta = *pick(L.w_scale, li);
+        float* y = pick(L.y, li);
+        int32_t* acc_out = pick(L.acc, li);
 #pragma unroll
         for (int t = 0; t < MT; ++t) {
             const int total = wave_sum_all(acc[r][t]);
-            if (lane == 0 && n < N && t < M) {
-                y[(size_t)t * N + n] = (float)total * (*w_scale / x_scale[t]);
+            if (lane == 0 && row0 + r < rows && t < M) {
+                y[(size_t)t * N + n] = (float)total * (beta / (QX ? sx : x_scale[t]));
                 if (acc_out) acc_out[(size_t)t * N + n] = total;
+            }
+        }
+    }
+    if constexpr (QX) {
+        if (blockIdx.x == 0) {
+            csum = wave_sum_all(csum);
+            if (lane == 0) redi[wave] = csum;
+            __syncthreads();
+            if (tid == 0) {
+                int tot = 0;
+#pragma unroll
+                for (int w = 0; w < kEW; ++w) tot += redi[w];
+                rs_out[0] = tot;
+                s_out[0] = sx;
             }
         }
     }
@@ -238,45 +316,54 @@ __global__ __launch_bounds__(256) void pack_elut_words(const int8_t* __restrict_
     if constexpr (F == kElutC5G2) packed[(size_t)N * K / 4 + n * (K / 16) + w] = (uint8_t)sign;
 }
 
-template <int F, int RS, int MT>
-hipError_t launch_elut_mt(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
-                          int N, int K, float* y, int32_t* acc, hipStream_t stream) {
-    const dim3 grid((unsigned)((N + kEW * RS - 1) / (kEW * RS))), block(kEThreads);
-    hipLaunchKernelGGL((elut_generic_kernel<F, RS, MT>), grid, block, 0, stream, static_cast<const uint8_t*>(packed),
-                       w_scale, xq, x_scale, M, N, K, y, acc);
+template <int F, int RS, int MT, bool QX>
+hipError_t launch_elut_mt(const FusedLinears& L, const float* x, const int8_t* xq, const float* x_scale, int M, int K,
+                          int8_t* xq_out, float* s_out, int32_t* rs_out, hipStream_t stream) {
+    const int64_t rows = (int64_t)L.total * kRowsPerGroup;
+    const dim3 grid((unsigned)((rows + kEW * RS - 1) / (kEW * RS))), block(kEThreads);
+    hipLaunchKernelGGL((elut_generic_kernel<F, RS, MT, QX>), grid, block, 0, stream, L, x, xq, x_scale, M, K, xq_out,
+                       s_out, rs_out);
     return hipGetLastError();
 }
 
 // Tokens in slices of up to T::MT per launch; the kernel instance builds tables for exactly the slice's tokens
-// (1, 2 or 4).
+// (1, 2 or 4).  With x given (one token) the launch quantises the row itself.
 template <int F, int RS>
-hipError_t launch_elut_rs(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
-                          int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+hipError_t launch_elut_rs(const FusedLinears& L, const float* x, const int8_t* xq, const float* x_scale, int M,
+                          int K, int8_t* xq_out, float* s_out, int32_t* rs_out, hipStream_t stream) {
     using T = ElutFmt<F>;
+    if (x) return launch_elut_mt<F, RS, 1, true>(L, x, nullptr, nullptr, 1, K, xq_out, s_out, rs_out, stream);
     for (int m0 = 0; m0 < M; m0 += T::MT) {
         const int mc = M - m0 < T::MT ? M - m0 : T::MT;
+        FusedLinears Ls = L;
+        for (int i = 0; i < L.count; ++i) {
+            Ls.y[i] = L.y[i] + (size_t)m0 * L.N[i];
+            Ls.acc[i] = L.acc[i] ? L.acc[i] + (size_t)m0 * L.N[i] : nullptr;
+        }
         const int8_t* xs = xq + (size_t)m0 * K;
-        float* ys = y + (size_t)m0 * N;
-        int32_t* as = acc ? acc + (size_t)m0 * N : nullptr;
         hipError_t e;
-        if (mc == 1) e = launch_elut_mt<F, RS, 1>(packed, w_scale, xs, x_scale + m0, mc, N, K, ys, as, stream);
-        else if (mc == 2 || T::MT < 4) e = launch_elut_mt<F, RS, 2>(packed, w_scale, xs, x_scale + m0, mc, N, K, ys, as, stream);
-        else e = launch_elut_mt<F, RS, (T::MT >= 4 ? 4 : 2)>(packed, w_scale, xs, x_scale + m0, mc, N, K, ys, as, stream);
+        if (mc == 1) e = launch_elut_mt<F, RS, 1, false>(Ls, nullptr, xs, x_scale + m0, mc, K, nullptr, nullptr, nullptr, stream);
+        else if (mc == 2 || T::MT < 4)
+            e = launch_elut_mt<F, RS, 2, false>(Ls, nullptr, xs, x_scale + m0, mc, K, nullptr, nullptr, nullptr, stream);
+        else
+            e = launch_elut_mt<F, RS, (T::MT >= 4 ? 4 : 2), false>(Ls, nullptr, xs, x_scale + m0, mc, K, nullptr, nullptr,
+                                                                   nullptr, stream);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
 template <int F>
-hipError_t launch_elut_fmt(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
-                           int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+hipError_t launch_elut_fmt(const FusedLinears& L, const float* x, const int8_t* xq, const float* x_scale, int M, int K,
+                           int8_t* xq_out, float* s_out, int32_t* rs_out, hipStream_t stream) {
     // rows per wave: as many work groups as CUs where the rows allow, up to 8 rows per wave
     const int cus = device_cus();
-    const int rs_need = (N + kEW * cus - 1) / (kEW * cus);
-    if (rs_need <= 1) return launch_elut_rs<F, 1>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (rs_need <= 2) return launch_elut_rs<F, 2>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (rs_need <= 4) return launch_elut_rs<F, 4>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    return launch_elut_rs<F, 8>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+    const int64_t rows = (int64_t)L.total * kRowsPerGroup;
+    const int64_t rs_need = (rows + kEW * cus - 1) / (kEW * cus);
+    if (rs_need <= 1) return launch_elut_rs<F, 1>(L, x, xq, x_scale, M, K, xq_out, s_out, rs_out, stream);
+    if (rs_need <= 2) return launch_elut_rs<F, 2>(L, x, xq, x_scale, M, K, xq_out, s_out, rs_out, stream);
+    if (rs_need <= 4) return launch_elut_rs<F, 4>(L, x, xq, x_scale, M, K, xq_out, s_out, rs_out, stream);
+    return launch_elut_rs<F, 8>(L, x, xq, x_scale, M, K, xq_out, s_out, rs_out, stream);
 }
 
 template <int F>
@@ -290,12 +377,13 @@ hipError_t launch_pack_fmt(const int8_t* Wq, int N, int K, void* packed, hipStre
 
 }  // namespace
 
-hipError_t launch_elut_generic(int fmt, const void* packed, const float* w_scale, const int8_t* xq,
-                               const float* x_scale, int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
+hipError_t launch_elut_generic(int fmt, const FusedLinears& L, const float* x, const int8_t* xq,
+                               const float* x_scale, int M, int K, int8_t* xq_out, float* s_out, int32_t* rs_out,
+                               hipStream_t stream) {
     switch (fmt) {
-        case kElutC4G2: return launch_elut_fmt<kElutC4G2>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-        case kElutC5G2: return launch_elut_fmt<kElutC5G2>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-        default: return launch_elut_fmt<kElutC3G5>(packed, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+        case kElutC4G2: return launch_elut_fmt<kElutC4G2>(L, x, xq, x_scale, M, K, xq_out, s_out, rs_out, stream);
+        case kElutC5G2: return launch_elut_fmt<kElutC5G2>(L, x, xq, x_scale, M, K, xq_out, s_out, rs_out, stream);
+        default: return launch_elut_fmt<kElutC3G5>(L, x, xq, x_scale, M, K, xq_out, s_out, rs_out, stream);
     }
 }
 

@@ -105,3 +105,34 @@ def test_elut_fused_and_noalloc(fmt):
         y2 = torch.empty((M, N), dtype=torch.float32, device=H.DEV)
         B.bitnet_mpgemm_noalloc(fmt, p, b, N, K, xq, s, y2)
         assert np.array_equal(H.to_np(y2), H.to_np(y))
+
+
+# The fused call: every weight of the group in one table-lookup launch (rows of several weights in one work group,
+# ragged row counts); at one token the launch also quantises the row (codes, scale and code sum bit-exact against
+# the oracle's quantiser), otherwise the quantiser runs first.  Outputs against the oracle and bit-identical to the
+# separate calls.
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("M,K,Ns", [(1, 3200, [3200, 3200, 3200]), (1, 640, [16, 48, 208]), (1, 8640, [3200]),
+                                    (1, 1280, [9600, 16]), (6, 640, [48, 16])])
+def test_elut_fused_groups(fmt, M, K, Ns):
+    _announce("elut fused groups", fmt, M, K, Ns)
+    C, g, mirror = O.ELUT_FORMATS[fmt]
+    ws_ = [inputs.int_weights(N, K, C, seed=inputs.seed_for(13, 500 + 7 * i + K)) for i, N in enumerate(Ns)]
+    x = inputs.activation_f32(M, K, seed=inputs.seed_for(13, 599 + K + M))
+    packs = [_pack(fmt, w) for w in ws_]
+    betas = [torch.tensor([0.013 * (i + 1)], dtype=torch.float32, device=H.DEV) for i in range(len(Ns))]
+    xq = torch.empty((M, K), dtype=torch.int8, device=H.DEV)
+    s = torch.empty(M, dtype=torch.float32, device=H.DEV)
+    rs = torch.empty(M, dtype=torch.int32, device=H.DEV)
+    ys = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
+    B.bitnet_mpgemm_fused(fmt, packs, betas, x.to(H.DEV), xq, s, rs, ys)
+    xq_ref, s_ref = O.quantize_act(x.numpy())
+    assert np.array_equal(H.to_np(xq), xq_ref)
+    assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
+    for w, b, y, p, N in zip(ws_, betas, ys, packs, Ns):
+        acc_ref = O.mad_gemm(xq_ref, w.numpy())
+        H.check_y(H.to_np(y), O.epilogue(acc_ref, float(H.to_np(b)[0]), s_ref), acc_ref)
+        y_sep, acc = H.mpgemm(fmt, p, b, N, K, xq, s)
+        assert np.array_equal(H.to_np(acc), acc_ref)
+        assert np.array_equal(H.to_np(y_sep), H.to_np(y))
