@@ -125,6 +125,9 @@ ONE_TOKEN_GROUPS = [
     (6144, [1024]),                  # <16, 2, 2>
     (28672, [1024]),                 # <16, 4, 8>, two batches per row group
     (40960, [512]),                  # <16, 4, 16>, three batches per row group
+    (61440, [32]),                   # the longest row one launch quantises itself (<16, 4, 16>, 4 batches)
+    (61504, [16]),                   # one 64-k unit longer: the quantiser, then the GEMV reading the codes
+    (132096, [16]),                  # the largest K
 ]
 
 

@@ -136,7 +136,8 @@ def _path_vs_oracle(M, N, K, seed, layout="i2s", repeat=True, rowsum=True):
 
 @pytest.mark.parametrize("M,N,K", [(1, 16, 64), (1, 32, 320), (2, 48, 832), (5, 64, 1536), (8, 208, 3200),
                                    (16, 96, 1024), (1, 1024, 4096), (3, 16, 8640), (1, 4096, 1536),
-                                   (17, 64, 576), (33, 48, 448)])
+                                   (17, 64, 576), (33, 48, 448), (1, 16, 132096), (4, 32, 65600),
+                                   (16, 16, 20480)])
 @pytest.mark.parametrize("rowsum", [True, False])
 def test_i2s_mpgemm_parity(M, N, K, rowsum):
     _announce("i2s mpgemm", M, N, K, rowsum)
