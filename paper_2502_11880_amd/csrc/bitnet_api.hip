@@ -90,6 +90,27 @@ bitnet::FusedLinears one_linear(const void* packed, const float* w_scale, int64_
     return L;
 }
 
+// The table lookups of TL2, TL1 (lossy or not) for M tokens of already quantised activations: launches of up to 8
+// tokens, each over every weight of L (outputs of later slices offset by the slice's first token).
+hipError_t lookup_sliced(bool tl1, bool lossy, const bitnet::FusedLinears& L, const int8_t* xq, const float* x_scale,
+                         int64_t M, int64_t K, hipStream_t s) {
+    for (int64_t m0 = 0; m0 < M; m0 += bitnet::kElutMaxTokens) {
+        const int mc = (int)((M - m0) < bitnet::kElutMaxTokens ? (M - m0) : bitnet::kElutMaxTokens);
+        bitnet::FusedLinears Ls = L;
+        for (int i = 0; i < L.count; ++i) {
+            Ls.y[i] = L.y[i] + m0 * L.N[i];
+            Ls.acc[i] = L.acc[i] ? L.acc[i] + m0 * L.N[i] : nullptr;
+        }
+        const hipError_t e =
+            tl1 ? bitnet::launch_tl1_elut_decode(Ls, nullptr, xq + m0 * K, x_scale + m0, mc, (int)K, nullptr, nullptr,
+                                                 nullptr, s, lossy)
+                : bitnet::launch_tl2_elut_decode(Ls, nullptr, xq + m0 * K, x_scale + m0, mc, (int)K, nullptr, nullptr,
+                                                 nullptr, s, lossy);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 // TL2 and TL1 at M > 16 run the I2_S prefill GEMM on their weights rewritten in the I2_S layout (in the workspace),
 // where the I2_S limits hold.
 bool tl2_via_i2s(int64_t M, int64_t N, int64_t K) {
@@ -233,20 +254,10 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
                          int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
                          float* y, int32_t* acc, void* ws, size_t ws_bytes, hipStream_t s) {
     (void)packed_bytes;
-    if (lossy_layout(layout)) {
-        // TL2_0 / TL1_0: table lookups on int8-quantised tables, slices of 8 tokens
-        for (int64_t m0 = 0; m0 < M; m0 += bitnet::kElutMaxTokens) {
-            const int mc = (int)((M - m0) < bitnet::kElutMaxTokens ? (M - m0) : bitnet::kElutMaxTokens);
-            const hipError_t e =
-                layout == BITNET_LAYOUT_TL2_0
-                    ? bitnet::launch_tl2_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
-                                                     y + m0 * N, acc ? acc + m0 * N : nullptr, s, true)
-                    : bitnet::launch_tl1_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
-                                                     y + m0 * N, acc ? acc + m0 * N : nullptr, s, true);
-            if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
-        }
-        return ok();
-    }
+    if (lossy_layout(layout))   // TL2_0 / TL1_0: table lookups on int8-quantised tables, slices of 8 tokens
+        return hip_status(lookup_sliced(layout == BITNET_LAYOUT_TL1_0, true, one_linear(packed, w_scale, N, y, acc),
+                                        xq, x_scale, M, K, s),
+                          "bitnet_mpgemm launch");
     if (elut_layout(layout))   // table lookups of the integer-weight formats, any M (slices of 2 or 4 tokens)
         return hip_status(bitnet::launch_elut_generic(elut_format(layout), one_linear(packed, w_scale, N, y, acc), nullptr,
                                                       xq, x_scale, (int)M, (int)K, nullptr, nullptr, nullptr, s),
@@ -289,14 +300,8 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
         return hip_status(bitnet::launch_tl2_mfma_decode(one_linear(packed, w_scale, N, y, acc), xq, x_scale, (int)M,
                                                          (int)K, s),
                           "bitnet_mpgemm launch");
-    const int64_t slice = bitnet::kElutMaxTokens;
-    for (int64_t m0 = 0; m0 < M; m0 += slice) {
-        const int mc = (int)((M - m0) < slice ? (M - m0) : slice);
-        hipError_t e = bitnet::launch_tl2_elut_decode(packed, w_scale, xq + m0 * K, x_scale + m0, mc, (int)N, (int)K,
-                                                      y + m0 * N, acc ? acc + m0 * N : nullptr, s);
-        if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm launch");
-    }
-    return ok();
+    return hip_status(lookup_sliced(false, false, one_linear(packed, w_scale, N, y, acc), xq, x_scale, M, K, s),
+                      "bitnet_mpgemm launch");
 }
 
 // Scratch of bitnet_mpgemm_noalloc: one copy of this array on every GPU the library runs on, held until the
@@ -405,9 +410,9 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
     if (!aligned(ws, 16)) return fail(BITNET_E_ALIGN, "ws needs 16-byte alignment");
 
     hipStream_t s = (hipStream_t)stream;
-    if (elut_layout(layout)) {
+    if (elut_layout(layout) || lossy_layout(layout)) {
         // every weight of the group in one table-lookup launch; one token quantised inside it, else the quantiser
-        // first
+        // first (TL2_0 and TL1_0: launches of up to 8 tokens)
         bitnet::FusedLinears L{};
         L.count = n_linears;
         int64_t rgs = 0;
@@ -421,26 +426,24 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
         }
         if (rgs > ((int64_t)1 << 26)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
         bitnet::seal_fused(L);
-        const int fmt = elut_format(layout);
-        if (quantise && M == 1)
-            return hip_status(bitnet::launch_elut_generic(fmt, L, x, nullptr, nullptr, 1, (int)K, xq, x_scale, x_rowsum,
-                                                          s),
-                              "bitnet_mpgemm_fused launch");
+        const bool tl1 = layout == BITNET_LAYOUT_TL1_0;
+        if (quantise && M == 1) {
+            const hipError_t e =
+                lossy_layout(layout)
+                    ? (tl1 ? bitnet::launch_tl1_elut_decode(L, x, nullptr, nullptr, 1, (int)K, xq, x_scale, x_rowsum, s,
+                                                            true)
+                           : bitnet::launch_tl2_elut_decode(L, x, nullptr, nullptr, 1, (int)K, xq, x_scale, x_rowsum, s,
+                                                            true))
+                    : bitnet::launch_elut_generic(elut_format(layout), L, x, nullptr, nullptr, 1, (int)K, xq, x_scale,
+                                                  x_rowsum, s);
+            return hip_status(e, "bitnet_mpgemm_fused launch");
+        }
         hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
         if (e == hipSuccess)
-            e = bitnet::launch_elut_generic(fmt, L, nullptr, xq, x_scale, (int)M, (int)K, nullptr, nullptr, nullptr, s);
+            e = lossy_layout(layout) ? lookup_sliced(tl1, true, L, xq, x_scale, M, K, s)
+                                     : bitnet::launch_elut_generic(elut_format(layout), L, nullptr, xq, x_scale, (int)M,
+                                                                   (int)K, nullptr, nullptr, nullptr, s);
         return hip_status(e, "bitnet_mpgemm_fused launch");
-    }
-    if (lossy_layout(layout)) {
-        // the quantiser once, then the table lookups of each weight
-        hipError_t e = quantise ? bitnet::launch_quantize_act(x, M, K, xq, x_scale, x_rowsum, s) : hipSuccess;
-        if (e != hipSuccess) return hip_status(e, "bitnet_mpgemm_fused launch");
-        for (int i = 0; i < n_linears; ++i) {
-            const bitnet_status st = mpgemm_run(layout, packed[i], packed_bytes[i], w_scale[i], N[i], K, xq, x_scale,
-                                                x_rowsum, M, y[i], nullptr, nullptr, 0, s);
-            if (st != BITNET_OK) return st;
-        }
-        return ok();
     }
     // the small-batch regime (17..128 tokens, K <= 16384): the decode GEMV in token slices, for I2_S and TL1
     const bool sliced = i2s_tiled(layout) && bitnet::i2s_sliced_ok(M, K, true);

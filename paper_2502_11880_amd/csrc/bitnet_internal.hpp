@@ -236,14 +236,17 @@ hipError_t launch_tl1_to_i2s(const void* const* packed, const int* N, void* cons
 constexpr int kElutMaxTokens = 8;     // tokens per ELUT launch
 int tl2_elut_waves(int M);
 size_t tl2_elut_lds_bytes(int M);
-// lossy: TL2_0 (Sec. 3.2.1), the tables quantised to int8 per token and block before the lookups
-hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, const int8_t* xq,
-                                  const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
-                                  hipStream_t stream, bool lossy = false);
-// The TL1 layout by table lookups (Algorithm TL1), up to 8 tokens per launch; lossy: TL1_0.
-hipError_t launch_tl1_elut_decode(const void* packed, const float* w_scale, const int8_t* xq,
-                                  const float* x_scale, int M, int N, int K, float* y, int32_t* acc,
-                                  hipStream_t stream, bool lossy);
+// The TL2 layout by table lookups, 1..8 tokens, every weight of L in one launch.  x NULL: xq and x_scale hold
+// the M tokens' codes and scales.  x set (M == 1): the fp32 row is quantised inside the launch, which writes its
+// codes, scale and code sum to xq_out, s_out and rs_out.  lossy: TL2_0 (Sec. 3.2.1), the tables quantised to int8
+// per token and block before the lookups.
+hipError_t launch_tl2_elut_decode(const FusedLinears& L, const float* x, const int8_t* xq, const float* x_scale,
+                                  int M, int K, int8_t* xq_out, float* s_out, int32_t* rs_out, hipStream_t stream,
+                                  bool lossy);
+// The TL1 layout by table lookups (Algorithm TL1), arguments as above; lossy: TL1_0.
+hipError_t launch_tl1_elut_decode(const FusedLinears& L, const float* x, const int8_t* xq, const float* x_scale,
+                                  int M, int K, int8_t* xq_out, float* s_out, int32_t* rs_out, hipStream_t stream,
+                                  bool lossy);
 hipError_t launch_elut_tables(const int8_t* xq, int M, int K, int16_t* lut, int16_t* lut1, hipStream_t stream);
 // One token, TL2, every weight of a group in one launch; x (fp32) is quantised inside, or, when x is NULL, xq is
 // read.  Only where the whole row's tables fit in LDS (tl2_stream_fits); the caller falls back otherwise.

@@ -97,20 +97,74 @@ __device__ __forceinline__ int wave_max_int(int v) {
     return (int)wave_max_all((float)v);
 }
 
-// LOSSY (TL2_0, Sec. 3.2.1): each token's tables of a block (128 triples, or the 32 pairs of a TL1 unit) are
-// quantised to int8 with the block's power-of-two scale before the lookups, and the block's sum is scaled back.
-template <int WAVES, int MT, bool LOSSY>
+// The int8 code of one activation (the quantiser's rounding: half to even, clamped to [-128, 127]).
+__device__ __forceinline__ int code_of(float v, float s) {
+    return (int)fminf(fmaxf(rintf(v * s), -128.0f), 127.0f);
+}
+
+// One token quantised inside a table-lookup launch (QX): the row's scale from its absmax (every work group reads the
+// whole fp32 row, L2-resident after the first), the quantiser's formula.
+template <int WAVES>
+__device__ __forceinline__ float row_scale(const float* __restrict__ x, int K, float* red) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    float amax = 0.0f;
+    for (int i = tid; i < K / 4; i += 64 * WAVES) {
+        const float4 v = x4[i];
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+    }
+    amax = wave_max_all(amax);
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    amax = red[0];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) amax = fmaxf(amax, red[w]);
+    return 127.0f / fmaxf(amax, 1e-5f);
+}
+
+// Work group 0 of a QX launch also writes the row's scale and code sum (its codes it stores as it makes them).
+template <int WAVES>
+__device__ __forceinline__ void write_row_sum(int csum, float sx, int* red, float* s_out, int32_t* rs_out) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    csum = wave_sum_all(csum);
+    __syncthreads();
+    if (lane == 0) red[wave] = csum;
+    __syncthreads();
+    if (tid == 0) {
+        int tot = 0;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) tot += red[w];
+        rs_out[0] = tot;
+        s_out[0] = sx;
+    }
+}
+
+// One work group per 16-row group of the launch's weights (rows of a fused group concatenated; the group's weight
+// is found by a scalar compare chain).  LOSSY (TL2_0, Sec. 3.2.1): each token's tables of a block (128 triples, or
+// the 32 pairs of a TL1 unit) are quantised to int8 with the block's power-of-two scale before the lookups, and the
+// block's sum is scaled back.  QX (one token): the work group quantises the fp32 row itself and work group 0 writes
+// the codes, the scale and their sum, as the quantiser would.
+template <int WAVES, int MT, bool LOSSY, bool QX>
 __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
-    const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
-    const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out) {
+    FusedLinears L, const float* __restrict__ x, const int8_t* __restrict__ xq, const float* __restrict__ x_scale,
+    int M, int K, int8_t* __restrict__ xq_out, float* __restrict__ s_out, int32_t* __restrict__ rs_out) {
     extern __shared__ __align__(16) uint8_t lds[];
+    __shared__ float redf[WAVES];
+    __shared__ int redi[WAVES];
+    static_assert(!QX || MT == 1, "the fused quantiser takes one token");
     constexpr int TC = tl2_elut_chunk(MT);      // tokens whose tables share LDS at a time
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = lane >> 4, r = lane & 15;
-    const int rg = xcd_logical_id(blockIdx.x, gridDim.x);
+    int li, rg;
+    locate(L, xcd_logical_id(blockIdx.x, gridDim.x), li, rg);
+    const int N = pick(L.N, li);
+    const uint8_t* packed = pick(L.packed, li);
     const int three = (K / kTl2BlockK) * kTl2BlockK;
     const int nblk = three / kTl2BlockK;
     const int units = (K - three) / kSubK;
+    const bool qw = QX && blockIdx.x == 0;      // this work group writes the codes
+    const float sx = QX ? row_scale<WAVES>(x, K, redf) : 1.0f;
+    int csum = 0;
     const uint8_t* idx_plane = packed;
     const uint8_t* sign_plane = packed + (size_t)N * (three / 6);
     const uint8_t* tail_plane = sign_plane + (size_t)N * (three / 24);
@@ -137,22 +191,37 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
             for (int j = 0; j < TC; ++j) {
                 const int m = c + j;
                 if (m >= M) break;
-                const int8_t* a = xq + (size_t)m * K + (size_t)blk * kTl2BlockK;
+                // the codes of triples lane and lane + 64
+                int cd[2][3];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int g = lane + 64 * h;
+                    const size_t k = (size_t)blk * kTl2BlockK + 3 * g;
+#pragma unroll
+                    for (int e = 0; e < 3; ++e) {
+                        if constexpr (QX) {
+                            cd[h][e] = code_of(x[k + e], sx);
+                            if (qw) {
+                                xq_out[k + e] = (int8_t)cd[h][e];
+                                csum += cd[h][e];
+                            }
+                        } else {
+                            cd[h][e] = xq[(size_t)m * K + k + e];
+                        }
+                    }
+                }
                 if constexpr (LOSSY) {
                     // the block's largest |entry| is the largest |a0| + |a1| + |a2| of its triples
                     int mx = 0;
 #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const int g = lane + 64 * h;
-                        mx = max(mx, abs((int)a[3 * g]) + abs((int)a[3 * g + 1]) + abs((int)a[3 * g + 2]));
-                    }
+                    for (int h = 0; h < 2; ++h) mx = max(mx, abs(cd[h][0]) + abs(cd[h][1]) + abs(cd[h][2]));
                     shift[j] = lossy_shift_of(wave_max_int(mx));
                 }
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     const int g = lane + 64 * h;
                     uint32_t w[8];
-                    triple_table(a[3 * g], a[3 * g + 1], a[3 * g + 2], w);
+                    triple_table(cd[h][0], cd[h][1], cd[h][2], w);
                     if constexpr (LOSSY) quantize_words(w, shift[j]);
                     store_table(lut + j * kTokenStride + skewed_slot(g) * kSlot, w);
                 }
@@ -196,12 +265,25 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
                 for (int j = 0; j < TC; ++j) {
                     const int m = c + j;
                     if (m >= M) break;
-                    const int8_t* b = xq + (size_t)m * K + three + kSubK * u + 2 * (lane & 31);
+                    const size_t k = (size_t)three + kSubK * u + 2 * (lane & 31);
+                    int b0, b1;
+                    if constexpr (QX) {
+                        b0 = code_of(x[k], sx);
+                        b1 = code_of(x[k + 1], sx);
+                        if (qw && lane < 32) {
+                            xq_out[k] = (int8_t)b0;
+                            xq_out[k + 1] = (int8_t)b1;
+                            csum += b0 + b1;
+                        }
+                    } else {
+                        b0 = xq[(size_t)m * K + k];
+                        b1 = xq[(size_t)m * K + k + 1];
+                    }
                     if constexpr (LOSSY)
-                        shift[j] = lossy_shift_of(wave_max_int(lane < 32 ? abs((int)b[0]) + abs((int)b[1]) : 0));
+                        shift[j] = lossy_shift_of(wave_max_int(lane < 32 ? abs(b0) + abs(b1) : 0));
                     if (lane < 32) {
                         uint32_t w[8];
-                        pair_table(b[0], b[1], w);
+                        pair_table(b0, b1, w);
                         if constexpr (LOSSY) quantize_words(w, shift[j]);
                         store_table(lut + j * kTokenStride + lane * kSlot, w);
                     }
@@ -233,6 +315,9 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
         v += __shfl_xor(v, 32, 64);
         acc[m] = v;
     }
+    if constexpr (QX) {
+        if (qw) write_row_sum<WAVES>(csum, sx, redi, s_out, rs_out);
+    }
     __syncthreads();   // every wave is done with its tables: reuse the LDS for the reduction
     int* red = reinterpret_cast<int*>(lds);
     if (lane < 16) {
@@ -242,12 +327,14 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
     }
     __syncthreads();
     if (wave != 0 || lane >= 16) return;
-    const float beta = *w_scale;
+    const float beta = *pick(L.w_scale, li);
+    float* y = pick(L.y, li);
+    int32_t* acc_out = pick(L.acc, li);
     const int n = rg * kRowsPerGroup + r;
     for (int m = 0; m < M; ++m) {
         int s = 0;
         for (int w = 0; w < WAVES; ++w) s += red[(w * 16 + m) * 16 + lane];
-        const float sc = beta / x_scale[m];
+        const float sc = beta / (QX ? sx : x_scale[m]);
         y[(size_t)m * N + n] = (float)s * sc;
         if (acc_out) acc_out[(size_t)m * N + n] = s;
     }
@@ -258,7 +345,7 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_elut_decode_kernel(
 // of pair l % 32 of units l / 32 and 2 + l / 32, for a chunk of up to two tokens at a time, and lane (r, q) looks
 // up the 8 pairs of each of its block's words (row r, k = 64 j + 16 q .. + 15 of unit j).  LOSSY (TL1_0, Sec. 3.2.1):
 // each token's tables of a unit are quantised to int8 with the unit's power-of-two scale and the unit's sum is
-// scaled back.
+// scaled back.  Fused weight groups and QX as for the TL2 kernel.
 constexpr int kTl1BlockStride = 128 * kSlot;                 // the 128 pair tables of a 256-k block per token
 
 // Largest value of each half-wave (lanes 0..31 and 32..63) of v, as scalars: DPP maxima inside each row of 16 lanes,
@@ -270,16 +357,25 @@ __device__ __forceinline__ void half_wave_max(int v, int& lo, int& hi) {
     hi = max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48));
 }
 
-template <int WAVES, int MT, bool LOSSY>
+template <int WAVES, int MT, bool LOSSY, bool QX>
 __global__ __launch_bounds__(64 * WAVES) void tl1_elut_decode_kernel(
-    const uint8_t* __restrict__ packed, const float* __restrict__ w_scale, const int8_t* __restrict__ xq,
-    const float* __restrict__ x_scale, int M, int N, int K, float* __restrict__ y, int32_t* __restrict__ acc_out) {
+    FusedLinears L, const float* __restrict__ x, const int8_t* __restrict__ xq, const float* __restrict__ x_scale,
+    int M, int K, int8_t* __restrict__ xq_out, float* __restrict__ s_out, int32_t* __restrict__ rs_out) {
     extern __shared__ __align__(16) uint8_t lds[];
+    __shared__ float redf[WAVES];
+    __shared__ int redi[WAVES];
+    static_assert(!QX || MT == 1, "the fused quantiser takes one token");
     constexpr int TC = tl2_elut_chunk(MT);      // tokens whose tables share LDS at a time
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = lane >> 4, r = lane & 15;
     const int pr = lane & 31, hh = lane >> 5;  // this lane builds pair pr of units hh and 2 + hh
-    const int rg = xcd_logical_id(blockIdx.x, gridDim.x);
+    int li, rg;
+    locate(L, xcd_logical_id(blockIdx.x, gridDim.x), li, rg);
+    const int N = pick(L.N, li);
+    const uint8_t* packed = pick(L.packed, li);
+    const bool qw = QX && blockIdx.x == 0;      // this work group writes the codes
+    const float sx = QX ? row_scale<WAVES>(x, K, redf) : 1.0f;
+    int csum = 0;
     const int nsub = K / kSubK;
     const int nkb = (nsub + 3) / 4;
     const uint8_t* rgbase = packed + (size_t)rg * 4 * K;
@@ -310,9 +406,32 @@ __global__ __launch_bounds__(64 * WAVES) void tl1_elut_decode_kernel(
             for (int jj = 0; jj < TC; ++jj) {
                 const int m = c + jj;
                 if (m >= M) break;
-                const int8_t* xb = xq + (size_t)m * K + (size_t)sb * kI2sBlockK + 2 * pr;
-                const int a0 = xb[kSubK * u0], a1 = xb[kSubK * u0 + 1];
-                const int b0 = xb[kSubK * u1], b1 = xb[kSubK * u1 + 1];
+                const size_t kb0 = (size_t)sb * kI2sBlockK + 2 * pr;
+                int a0, a1, b0, b1;
+                if constexpr (QX) {
+                    a0 = code_of(x[kb0 + kSubK * u0], sx);
+                    a1 = code_of(x[kb0 + kSubK * u0 + 1], sx);
+                    b0 = code_of(x[kb0 + kSubK * u1], sx);
+                    b1 = code_of(x[kb0 + kSubK * u1 + 1], sx);
+                    if (qw) {
+                        if (ok0) {
+                            xq_out[kb0 + kSubK * u0] = (int8_t)a0;
+                            xq_out[kb0 + kSubK * u0 + 1] = (int8_t)a1;
+                            csum += a0 + a1;
+                        }
+                        if (ok1) {
+                            xq_out[kb0 + kSubK * u1] = (int8_t)b0;
+                            xq_out[kb0 + kSubK * u1 + 1] = (int8_t)b1;
+                            csum += b0 + b1;
+                        }
+                    }
+                } else {
+                    const int8_t* xb = xq + (size_t)m * K + kb0;
+                    a0 = xb[kSubK * u0];
+                    a1 = xb[kSubK * u0 + 1];
+                    b0 = xb[kSubK * u1];
+                    b1 = xb[kSubK * u1 + 1];
+                }
                 if constexpr (LOSSY) {
                     int lo0, hi0, lo1, hi1;
                     half_wave_max(ok0 ? abs(a0) + abs(a1) : 0, lo0, hi0);
@@ -372,6 +491,9 @@ __global__ __launch_bounds__(64 * WAVES) void tl1_elut_decode_kernel(
         v += __shfl_xor(v, 32, 64);
         acc[m] = v;
     }
+    if constexpr (QX) {
+        if (qw) write_row_sum<WAVES>(csum, sx, redi, s_out, rs_out);
+    }
     __syncthreads();
     int* red = reinterpret_cast<int*>(lds);
     if (lane < 16) {
@@ -381,12 +503,14 @@ __global__ __launch_bounds__(64 * WAVES) void tl1_elut_decode_kernel(
     }
     __syncthreads();
     if (wave != 0 || lane >= 16) return;
-    const float beta = *w_scale;
+    const float beta = *pick(L.w_scale, li);
+    float* y = pick(L.y, li);
+    int32_t* acc_out = pick(L.acc, li);
     const int n = rg * kRowsPerGroup + r;
     for (int m = 0; m < M; ++m) {
         int s = 0;
         for (int w = 0; w < WAVES; ++w) s += red[(w * 16 + m) * 16 + lane];
-        y[(size_t)m * N + n] = (float)s * (beta / x_scale[m]);
+        y[(size_t)m * N + n] = (float)s * (beta / (QX ? sx : x_scale[m]));
         if (acc_out) acc_out[(size_t)m * N + n] = s;
     }
 }
@@ -1193,50 +1317,53 @@ size_t tl2_elut_lds_bytes(int M) {
     return tables > red ? tables : red;
 }
 
-template <int MT, bool LOSSY>
-hipError_t launch_elut_mt(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
-                          int N, int K, float* y, int32_t* acc, hipStream_t stream) {
-    const unsigned grid = (unsigned)(N / kRowsPerGroup);
-    const size_t lds = tl2_elut_lds_bytes(M);
-    switch (tl2_elut_waves(M)) {
-        case 16:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<16, MT, LOSSY>), dim3(grid), dim3(1024), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
-        case 8:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<8, MT, LOSSY>), dim3(grid), dim3(512), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
-        case 4:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<4, MT, LOSSY>), dim3(grid), dim3(256), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
-        case 2:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<2, MT, LOSSY>), dim3(grid), dim3(128), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
-        default:
-            hipLaunchKernelGGL((tl2_elut_decode_kernel<1, MT, LOSSY>), dim3(grid), dim3(64), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
+// Arguments of one table-lookup launch over a fused weight group; x set: one token quantised inside (QX).
+struct LookupArgs {
+    const FusedLinears* L;
+    const float* x;
+    const int8_t* xq;
+    const float* x_scale;
+    int M, K;
+    int8_t* xq_out;
+    float* s_out;
+    int32_t* rs_out;
+};
+
+template <int WAVES, int MT, bool LOSSY, bool QX>
+void launch_tl2_cfg(const LookupArgs& a, size_t lds, hipStream_t stream) {
+    hipLaunchKernelGGL((tl2_elut_decode_kernel<WAVES, MT, LOSSY, QX>), dim3((unsigned)a.L->total), dim3(64 * WAVES),
+                       lds, stream, *a.L, a.x, a.xq, a.x_scale, a.M, a.K, a.xq_out, a.s_out, a.rs_out);
+}
+
+template <int MT, bool LOSSY, bool QX>
+hipError_t launch_elut_mt(const LookupArgs& a, hipStream_t stream) {
+    const size_t lds = tl2_elut_lds_bytes(a.M);
+    switch (tl2_elut_waves(a.M)) {
+        case 16: launch_tl2_cfg<16, MT, LOSSY, QX>(a, lds, stream); break;
+        case 8: launch_tl2_cfg<8, MT, LOSSY, QX>(a, lds, stream); break;
+        case 4: launch_tl2_cfg<4, MT, LOSSY, QX>(a, lds, stream); break;
+        case 2: launch_tl2_cfg<2, MT, LOSSY, QX>(a, lds, stream); break;
+        default: launch_tl2_cfg<1, MT, LOSSY, QX>(a, lds, stream); break;
     }
     return hipGetLastError();
 }
 
 template <bool LOSSY>
-hipError_t launch_tl2_elut_lossy(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
-                                 int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
-    if (M <= 1) return launch_elut_mt<1, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (M <= 2) return launch_elut_mt<2, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (M <= 4) return launch_elut_mt<4, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    return launch_elut_mt<8, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+hipError_t launch_tl2_elut_lossy(const LookupArgs& a, hipStream_t stream) {
+    if (a.x) return launch_elut_mt<1, LOSSY, true>(a, stream);
+    if (a.M <= 1) return launch_elut_mt<1, LOSSY, false>(a, stream);
+    if (a.M <= 2) return launch_elut_mt<2, LOSSY, false>(a, stream);
+    if (a.M <= 4) return launch_elut_mt<4, LOSSY, false>(a, stream);
+    return launch_elut_mt<8, LOSSY, false>(a, stream);
 }
 
-hipError_t launch_tl2_elut_decode(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                                  int M, int N, int K, float* y, int32_t* acc, hipStream_t stream, bool lossy) {
-    const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    return lossy ? launch_tl2_elut_lossy<true>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream)
-                 : launch_tl2_elut_lossy<false>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+hipError_t launch_tl2_elut_decode(const FusedLinears& L, const float* x, const int8_t* xq, const float* x_scale,
+                                  int M, int K, int8_t* xq_out, float* s_out, int32_t* rs_out, hipStream_t stream,
+                                  bool lossy) {
+    if (L.total <= 0) return hipSuccess;
+    if (M < 1 || M > 8 || (x && M != 1)) return hipErrorInvalidValue;
+    const LookupArgs a{&L, x, xq, x_scale, M, K, xq_out, s_out, rs_out};
+    return lossy ? launch_tl2_elut_lossy<true>(a, stream) : launch_tl2_elut_lossy<false>(a, stream);
 }
 
 // TL1 layout by table lookup (Algorithm TL1): the 32 pair tables of a 64-k unit per wave, lossy or not.
@@ -1253,42 +1380,39 @@ size_t tl1_elut_lds_bytes(int M) {
     return tables > red ? tables : red;
 }
 
-template <int MT, bool LOSSY>
-hipError_t launch_tl1_mt(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale, int M,
-                         int N, int K, float* y, int32_t* acc, hipStream_t stream) {
-    const unsigned grid = (unsigned)(N / kRowsPerGroup);
-    const size_t lds = tl1_elut_lds_bytes(M);
-    switch (tl1_elut_waves(M)) {
-        case 16:
-            hipLaunchKernelGGL((tl1_elut_decode_kernel<16, MT, LOSSY>), dim3(grid), dim3(1024), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
-        case 8:
-            hipLaunchKernelGGL((tl1_elut_decode_kernel<8, MT, LOSSY>), dim3(grid), dim3(512), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
-        default:
-            hipLaunchKernelGGL((tl1_elut_decode_kernel<4, MT, LOSSY>), dim3(grid), dim3(256), lds, stream, pk,
-                               w_scale, xq, x_scale, M, N, K, y, acc);
-            break;
+template <int WAVES, int MT, bool LOSSY, bool QX>
+void launch_tl1_cfg(const LookupArgs& a, size_t lds, hipStream_t stream) {
+    hipLaunchKernelGGL((tl1_elut_decode_kernel<WAVES, MT, LOSSY, QX>), dim3((unsigned)a.L->total), dim3(64 * WAVES),
+                       lds, stream, *a.L, a.x, a.xq, a.x_scale, a.M, a.K, a.xq_out, a.s_out, a.rs_out);
+}
+
+template <int MT, bool LOSSY, bool QX>
+hipError_t launch_tl1_mt(const LookupArgs& a, hipStream_t stream) {
+    const size_t lds = tl1_elut_lds_bytes(a.M);
+    switch (tl1_elut_waves(a.M)) {
+        case 16: launch_tl1_cfg<16, MT, LOSSY, QX>(a, lds, stream); break;
+        case 8: launch_tl1_cfg<8, MT, LOSSY, QX>(a, lds, stream); break;
+        default: launch_tl1_cfg<4, MT, LOSSY, QX>(a, lds, stream); break;
     }
     return hipGetLastError();
 }
 
 template <bool LOSSY>
-hipError_t launch_tl1_elut_lossy(const uint8_t* pk, const float* w_scale, const int8_t* xq, const float* x_scale,
-                                 int M, int N, int K, float* y, int32_t* acc, hipStream_t stream) {
-    if (M <= 1) return launch_tl1_mt<1, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (M <= 2) return launch_tl1_mt<2, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    if (M <= 4) return launch_tl1_mt<4, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
-    return launch_tl1_mt<8, LOSSY>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+hipError_t launch_tl1_elut_lossy(const LookupArgs& a, hipStream_t stream) {
+    if (a.x) return launch_tl1_mt<1, LOSSY, true>(a, stream);
+    if (a.M <= 1) return launch_tl1_mt<1, LOSSY, false>(a, stream);
+    if (a.M <= 2) return launch_tl1_mt<2, LOSSY, false>(a, stream);
+    if (a.M <= 4) return launch_tl1_mt<4, LOSSY, false>(a, stream);
+    return launch_tl1_mt<8, LOSSY, false>(a, stream);
 }
 
-hipError_t launch_tl1_elut_decode(const void* packed, const float* w_scale, const int8_t* xq, const float* x_scale,
-                                  int M, int N, int K, float* y, int32_t* acc, hipStream_t stream, bool lossy) {
-    const uint8_t* pk = static_cast<const uint8_t*>(packed);
-    return lossy ? launch_tl1_elut_lossy<true>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream)
-                 : launch_tl1_elut_lossy<false>(pk, w_scale, xq, x_scale, M, N, K, y, acc, stream);
+hipError_t launch_tl1_elut_decode(const FusedLinears& L, const float* x, const int8_t* xq, const float* x_scale,
+                                  int M, int K, int8_t* xq_out, float* s_out, int32_t* rs_out, hipStream_t stream,
+                                  bool lossy) {
+    if (L.total <= 0) return hipSuccess;
+    if (M < 1 || M > 8 || (x && M != 1)) return hipErrorInvalidValue;
+    const LookupArgs a{&L, x, xq, x_scale, M, K, xq_out, s_out, rs_out};
+    return lossy ? launch_tl1_elut_lossy<true>(a, stream) : launch_tl1_elut_lossy<false>(a, stream);
 }
 
 size_t tl2_stream_lds_bytes(int K) {

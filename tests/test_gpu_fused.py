@@ -150,8 +150,9 @@ def test_fused_one_token_100b_groups(K, Ns):
 
 
 def _fused_case_lossy(layout, M=3, K=1600, Ns=(64, 208)):
-    """bitnet_mpgemm_fused on a lossy layout: the quantiser, then each weight's lookups; equal to the separate calls
-    and to the oracle's lossy route."""
+    """bitnet_mpgemm_fused on a lossy layout: one table-lookup launch per slice of up to 8 tokens over every weight
+    (one token quantised inside it, else the quantiser first); the codes, scales and sums bit-exact, the outputs
+    equal to the separate calls and to the oracle's lossy route."""
     Ws = [inputs.weight_f32(N, K, seed=inputs.seed_for(15, 500 + i)) for i, N in enumerate(Ns)]
     x = inputs.activation_f32(M, K, seed=inputs.seed_for(15, 599))
     packs = [H.pack(W, layout) for W in Ws]
@@ -161,6 +162,9 @@ def _fused_case_lossy(layout, M=3, K=1600, Ns=(64, 208)):
     ys = [torch.empty((M, N), dtype=torch.float32, device=H.DEV) for N in Ns]
     B.bitnet_mpgemm_fused(layout, [p for p, _ in packs], [b for _, b in packs], x.to(H.DEV), xq, s, rs, ys)
     xq_ref, s_ref = O.quantize_act(x.numpy())
+    assert np.array_equal(H.to_np(xq), xq_ref)
+    assert np.array_equal(H.to_np(s).view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
     route = O.elut_gemm_lossy if layout == "tl2_0" else O.elut_gemm_tl1_lossy
     pack = O.pack_tl2 if layout == "tl2_0" else O.pack_tl1
     for W, (p, b), y, N in zip(Ws, packs, ys, Ns):

@@ -58,7 +58,10 @@ def test_lossy_is_exact_when_tables_fit_int8(layout):
 
 
 @pytest.mark.parametrize("layout", ["tl2_0", "tl1_0"])
-def test_lossy_fused(layout):
-    _announce("lossy fused", layout)
+@pytest.mark.parametrize("M,K,Ns", [(3, 1600, (64, 208)), (1, 1600, (64, 208)), (1, 4096, (4096, 1024, 1024)),
+                                    (1, 8640, (3200,)), (1, 14336, (16, 32)), (1, 448, (16,)), (11, 832, (48, 16)),
+                                    (8, 3200, (208, 16, 32))])
+def test_lossy_fused(layout, M, K, Ns):
+    _announce("lossy fused", layout, M, K, Ns)
     from tests.test_gpu_fused import _fused_case_lossy
-    _fused_case_lossy(layout)
+    _fused_case_lossy(layout, M, K, Ns)
