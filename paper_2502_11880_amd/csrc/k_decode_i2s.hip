@@ -435,11 +435,11 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
         // every wave's row loads enter the memory pipeline before any weight load: without this barrier the last
         // waves' row loads queue behind the first waves' weight batches, and the quantisation waits for them
         __builtin_amdgcn_s_barrier();
-        // two batches in flight before the quantisation (steps 0 and 1), or one when there is only one step
+        // one batch in flight during the quantisation (step 0), the second (step 1) issued once the codes are made:
+        // a second or third batch ahead of the quantisation delays the row's arrival more than it saves later
         v4u wa[U], wb[U];
         float ba = 0.0f, bb = 0.0f;
         issue(wa, ba, 0);
-        if constexpr (kMulti) issue(wb, bb, 1);
         __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the quantisation arithmetic
 
         float amax = 0.0f;
@@ -475,6 +475,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
         // wave quantised exactly the blocks it multiplies, so only the lanes of one wave exchange codes (an
         // LDS hand-off inside the wave, no work-group barrier).  The waves' code sums meet in the first
         // epilogue, which follows a barrier.
+        if constexpr (kMulti) issue(wb, bb, 1);
         wave_lds_handoff();
         sum = wave_sum_all(sum);
         if (lane == 0) redi[wave] = sum;
@@ -611,6 +612,9 @@ hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t
     if (xv <= 2) return launch_stream<FMT, WAVES, U, 2>(L, x, K, xq, s, rs, stream);
     if (WAVES < 16 || xv <= 4) return launch_stream<FMT, WAVES, U, 4>(L, x, K, xq, s, rs, stream);
     if (xv <= 8) return launch_stream<FMT, WAVES, U, 8>(L, x, K, xq, s, rs, stream);
+    // rows just past 8 loads per thread (K = 33024: 9) load only what they need
+    if (xv <= 9) return launch_stream<FMT, WAVES, U, 9>(L, x, K, xq, s, rs, stream);
+    if (xv <= 12) return launch_stream<FMT, WAVES, U, 12>(L, x, K, xq, s, rs, stream);
     return launch_stream<FMT, WAVES, U, 16>(L, x, K, xq, s, rs, stream);
 }
 

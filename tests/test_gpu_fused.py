@@ -124,7 +124,7 @@ ONE_TOKEN_GROUPS = [
     (2560, [4096]),                  # <4, 3, 4>
     (6144, [1024]),                  # <16, 2, 2>
     (28672, [1024]),                 # <16, 4, 8>, two batches per row group
-    (40960, [512]),                  # <16, 4, 16>, three batches per row group
+    (40960, [512]),                  # <16, 4, 12>, three batches per row group
     (61440, [32]),                   # the longest row one launch quantises itself (<16, 4, 16>, 4 batches)
     (61504, [16]),                   # one 64-k unit longer: the quantiser, then the GEMV reading the codes
     (132096, [16]),                  # the largest K
@@ -139,7 +139,7 @@ def test_fused_one_token_workload_groups(K, Ns):
 
 # The 100B-class layer's groups at one token (the launches of the stack benchmark), every layout.  I2_S and TL1: q/k/v
 # (2304 row groups: 256 work groups of <16, 3, 4> walking nine row groups each), o and down (768 row groups:
-# three per work group; down <16, 3, 16> with three batches per row group), gate/up (4128 row groups).  TL2: every
+# three per work group; down <16, 3, 9> with three batches per row group), gate/up (4128 row groups).  TL2: every
 # group on the MFMA expansion, q/k/v, o and gate/up with the row quantised inside; down (K = 33024, 86 blocks) after
 # the quantiser, in two batches per row group.
 @pytest.mark.parametrize("K,Ns", [(12288, [12288, 12288, 12288]), (12288, [12288]), (12288, [33024, 33024]),
