@@ -590,11 +590,15 @@ hipError_t launch_stream(const FusedLinears& L, const float* x, int K, int8_t* x
                          hipStream_t stream) {
     auto kern = i2s_gemv1_stream_kernel<WAVES, U, XV, FMT>;
     const size_t lds = (size_t)K;
-    // as many work groups as fit on the chip at once, balanced so that every one walks the same number of
-    // row groups (to within one)
-    int occ = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, reinterpret_cast<const void*>(kern), 64 * WAVES, lds) !=
-            hipSuccess || occ <= 0)
+    // as many work groups as are resident at once, balanced so that every one walks the same number of row groups
+    // (to within one).  16-wave groups: one per CU (a second resident group per CU, which the register use of the
+    // one-batch start allows, measured slower on the 100B-class stack: 4.96 against 4.74 ms per step); 4-wave
+    // groups: as many as fit, every row group in flight at once
+    int occ = 1;
+    if (WAVES < 16 &&
+        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, reinterpret_cast<const void*>(kern), 64 * WAVES, lds) !=
+             hipSuccess ||
+         occ <= 0))
         occ = 1;
     const int total = L.total;
     const int64_t max_g = (int64_t)device_cus() * occ;
@@ -610,7 +614,7 @@ hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t
     const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
     if (xv <= 1) return launch_stream<FMT, WAVES, U, 1>(L, x, K, xq, s, rs, stream);
     if (xv <= 2) return launch_stream<FMT, WAVES, U, 2>(L, x, K, xq, s, rs, stream);
-    if (WAVES < 16 || xv <= 4) return launch_stream<FMT, WAVES, U, 4>(L, x, K, xq, s, rs, stream);
+    if (WAVES < 8 || xv <= 4) return launch_stream<FMT, WAVES, U, 4>(L, x, K, xq, s, rs, stream);
     if (xv <= 8) return launch_stream<FMT, WAVES, U, 8>(L, x, K, xq, s, rs, stream);
     // rows just past 8 loads per thread (K = 33024: 9) load only what they need
     if (xv <= 9) return launch_stream<FMT, WAVES, U, 9>(L, x, K, xq, s, rs, stream);
@@ -738,6 +742,16 @@ hipError_t launch_gemv1_fmt(const FusedLinears& L, const float* x, int K, int8_t
         if (u <= 2) return launch_stream_xv<FMT, 4, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
         if (u <= 3) return launch_stream_xv<FMT, 4, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
         return launch_stream_xv<FMT, 4, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
+    }
+    if (L.total <= cus && nkb > 32 && K <= 32768) {
+        // one row group per work group, long rows: 8-wave groups, so that a row group is at least two batches and
+        // only the first is in flight while the row is quantised (the 8B-class down projection, 14336 -> 4096:
+        // 16 waves 22.4 us per layer set, 8 waves 21.6 us)
+        constexpr int kW8 = 8;
+        const int nb8 = (nkb + 4 * kW8 - 1) / (4 * kW8);
+        const int u8 = (nkb + kW8 * nb8 - 1) / (kW8 * nb8);
+        if (u8 <= 3) return launch_stream_xv<FMT, kW8, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+        return launch_stream_xv<FMT, kW8, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
     }
     // 16-wave work groups, up to four 256-k blocks per wave per batch, the batches of a row group balanced;
     // past what fits on the chip at once the work groups stream

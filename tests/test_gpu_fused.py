@@ -119,11 +119,14 @@ ONE_TOKEN_GROUPS = [
     (4096, [4096, 1024, 1024]),      # 8B-class q/k/v: <4, 4, 4>
     (4096, [4096]),                  # 8B-class o: <4, 4, 4>
     (4096, [14336, 14336]),          # 8B-class gate/up: <4, 4, 4>
-    (14336, [4096]),                 # 8B-class down: <16, 4, 4>
+    (14336, [4096]),                 # 8B-class down: <8, 4, 8>, two batches per row group
+    (8640, [3200]),                  # 3B-class down: <8, 3, 8>, two batches per row group
     (1024, [4096]),                  # <4, 1, 1>
     (2560, [4096]),                  # <4, 3, 4>
     (6144, [1024]),                  # <16, 2, 2>
-    (28672, [1024]),                 # <16, 4, 8>, two batches per row group
+    (28672, [1024]),                 # <8, 4, 16>, four batches per row group
+    (32768, [48]),                   # <8, 4, 16>, the longest row on 8-wave groups
+    (33024, [16]),                   # one block longer: <16, 3, 9>, three batches per row group
     (40960, [512]),                  # <16, 4, 12>, three batches per row group
     (61440, [32]),                   # the longest row one launch quantises itself (<16, 4, 16>, 4 batches)
     (61504, [16]),                   # one 64-k unit longer: the quantiser, then the GEMV reading the codes
