@@ -1052,13 +1052,16 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_mfma_decode_kernel(FusedLinear
         // every wave's row (or code) loads enter the memory pipeline before any weight load, so that no wave's
         // activation waits behind the other waves' weight batches
         if constexpr (XV > 0 || kEarly) __builtin_amdgcn_s_barrier();
+        // two batches in flight from the start when the codes are given; one while the row is quantised (a second
+        // batch ahead of the quantisation delays the row's arrival more than it saves later), the second after it
         issue(iwa, swa, twa, ba, 0);
-        if constexpr (kMulti) issue(iwb, swb, twb, bb, 1);
+        if constexpr (kMulti && XV == 0) issue(iwb, swb, twb, bb, 1);
         __builtin_amdgcn_sched_barrier(0);   // keep the weight loads ahead of the tables and the conversion
         if constexpr (XV == 0 && !MB && !kEarly) load_codes();
         store_tables();
         if constexpr (XV > 0) {
             quantise_row();
+            if constexpr (kMulti) issue(iwb, swb, twb, bb, 1);
         } else if constexpr (MB) {
             // every token's codes, whole (16-byte chunks; K % 64 == 0)
             const int kc = K / 16;
