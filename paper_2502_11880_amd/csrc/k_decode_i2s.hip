@@ -364,9 +364,9 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
 
 // One token, streaming: each work group quantises the activation row once (Sec. 2.1), keeps its codes in LDS and
 // then walks the row groups g = blockIdx.x, blockIdx.x + gridDim.x, ... of the launch, one batch of WAVES * U
-// blocks at a time (a row group takes ceil(K / (256 WAVES U)) batches).  Two register sets of weight words
-// alternate: the loads of the next batch are issued before the current one is multiplied, so the weight stream
-// never waits for the arithmetic.  The last batch of a row group reduces the waves' partial sums through LDS
+// blocks at a time (a row group takes ceil(K / (256 WAVES U)) batches).  One batch is in flight while the row is
+// quantised; after that two register sets of weight words alternate: the loads of the next batch are issued before
+// the current one is multiplied, so the weight stream never waits for the arithmetic.  The last batch of a row group reduces the waves' partial sums through LDS
 // (double-buffered, one barrier) and applies the epilogue.  Every A row holds the token's codes (LDS broadcast
 // reads, no lane masking); D row 0 is the one stored.
 template <int WAVES, int U, int XV, int FMT>
