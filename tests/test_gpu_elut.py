@@ -66,11 +66,13 @@ def _vs_oracle(fmt, M, N, K, seed, extreme=False):
     return acc_ref
 
 
-# 1 to 17 tokens (slices of 4, or 2 for c3g5), partial last blocks (K = 640, 3200, 8640), one to several rows per
-# wave (N = 16 .. 9600), the 3B-class shapes.
+# 1 to 17 tokens (slices of 4, or 2 for c3g5), partial last blocks (K = 640, 3200, 8640), the 3B-class shapes, and
+# every rows-per-wave count the launcher picks (1 to 8: the fewest rows per wave that keep one work group per CU;
+# N = 12288 .. 30720 take 3, 4, 5, 6, 7 and 8 on 256 CUs).
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("M,N,K", [(1, 16, 640), (2, 48, 1280), (3, 208, 3200), (5, 64, 8640), (8, 3200, 3200),
-                                   (17, 96, 640), (1, 9600, 640), (1, 8640, 3200)])
+                                   (17, 96, 640), (1, 9600, 640), (1, 8640, 3200), (3, 12288, 640), (1, 16384, 640),
+                                   (1, 17280, 640), (2, 20496, 640), (1, 28672, 640), (1, 30720, 640)])
 def test_elut_mpgemm_parity(fmt, M, N, K):
     _announce("elut mpgemm", fmt, M, N, K)
     _vs_oracle(fmt, M, N, K, seed=inputs.seed_for(13, 100 + M * 31 + N + K))
@@ -113,7 +115,8 @@ def test_elut_fused_and_noalloc(fmt):
 # separate calls.
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("M,K,Ns", [(1, 3200, [3200, 3200, 3200]), (1, 640, [16, 48, 208]), (1, 8640, [3200]),
-                                    (1, 1280, [9600, 16]), (6, 640, [48, 16])])
+                                    (1, 1280, [9600, 16]), (6, 640, [48, 16]), (1, 640, [8640, 8640]),
+                                    (1, 640, [14336, 14336])])
 def test_elut_fused_groups(fmt, M, K, Ns):
     _announce("elut fused groups", fmt, M, K, Ns)
     C, g, mirror = O.ELUT_FORMATS[fmt]
