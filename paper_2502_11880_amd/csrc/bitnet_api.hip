@@ -254,10 +254,18 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
                          int64_t K, const int8_t* xq, const float* x_scale, const int32_t* x_rowsum, int64_t M,
                          float* y, int32_t* acc, void* ws, size_t ws_bytes, hipStream_t s) {
     (void)packed_bytes;
-    if (lossy_layout(layout))   // TL2_0 / TL1_0: table lookups on int8-quantised tables, slices of 8 tokens
+    if (lossy_layout(layout)) {
+        // TL2_0 / TL1_0: table lookups on int8-quantised tables; one TL2_0 token on the persistent table kernel
+        // (every work group builds the row's tables once), else slices of 8 tokens
+        if (layout == BITNET_LAYOUT_TL2_0 && M == 1 && bitnet::tl2_stream_fits((int)K))
+            return hip_status(bitnet::launch_tl2_stream(one_linear(packed, w_scale, N, y, acc), nullptr, (int)K,
+                                                        const_cast<int8_t*>(xq), const_cast<float*>(x_scale), nullptr,
+                                                        s, true),
+                              "bitnet_mpgemm launch");
         return hip_status(lookup_sliced(layout == BITNET_LAYOUT_TL1_0, true, one_linear(packed, w_scale, N, y, acc),
                                         xq, x_scale, M, K, s),
                           "bitnet_mpgemm launch");
+    }
     if (elut_layout(layout))   // table lookups of the integer-weight formats, any M (slices of 2 or 4 tokens)
         return hip_status(bitnet::launch_elut_generic(elut_format(layout), one_linear(packed, w_scale, N, y, acc), nullptr,
                                                       xq, x_scale, (int)M, (int)K, nullptr, nullptr, nullptr, s),
@@ -427,6 +435,11 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
         if (rgs > ((int64_t)1 << 26)) return fail(BITNET_E_SHAPE, "too many output rows in one launch");
         bitnet::seal_fused(L);
         const bool tl1 = layout == BITNET_LAYOUT_TL1_0;
+        if (layout == BITNET_LAYOUT_TL2_0 && M == 1 && bitnet::tl2_stream_fits((int)K))
+            // one token: the persistent table kernel (the row quantised inside when x is given)
+            return hip_status(bitnet::launch_tl2_stream(L, quantise ? x : nullptr, (int)K, xq, x_scale, x_rowsum, s,
+                                                        true),
+                              "bitnet_mpgemm_fused launch");
         if (quantise && M == 1) {
             const hipError_t e =
                 lossy_layout(layout)

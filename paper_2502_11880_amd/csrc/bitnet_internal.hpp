@@ -266,8 +266,9 @@ hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, i
 // i2s_out[i]), for the prefill GEMM; one launch.
 hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* const* i2s_out, int count, int K,
                              hipStream_t stream);
+// lossy: TL2_0 (Sec. 3.2.1), each block's tables quantised to int8 with its power-of-two scale.
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
-                             int32_t* x_rowsum, hipStream_t stream);
+                             int32_t* x_rowsum, hipStream_t stream, bool lossy = false);
 
 // ELUT for integer weights of other cardinalities: formats c4g2, c5g2 and c3g5 (table lookups, up to 4 tokens per
 // launch for the 2-weight groups and 2 for c3g5; the launcher slices M).  Every weight of L in one launch.  With x

@@ -530,7 +530,7 @@ __device__ __forceinline__ void store_words(uint8_t* slot, const uint32_t* w, in
     for (int i = 0; i < n; ++i) reinterpret_cast<uint32_t*>(slot)[i] = w[i];
 }
 
-template <int WAVES, int U, int XV, bool QUANT>
+template <int WAVES, int U, int XV, bool QUANT, bool LOSSY>
 __global__ __launch_bounds__(64 * WAVES) void tl2_stream_kernel(FusedLinears L, const float* __restrict__ x, int K,
                                                                 int8_t* __restrict__ xq, float* __restrict__ x_scale,
                                                                 int32_t* __restrict__ x_rowsum) {
@@ -636,27 +636,55 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_stream_kernel(FusedLinears L, 
             x_rowsum[0] = tot;
         }
 
-        // 2. this wave's tables, once: lane builds triples lane and lane + 64 of each of its blocks
+        // 2. this wave's tables, once: lane builds triples lane and lane + 64 of each of its blocks.  LOSSY (TL2_0,
+        //    Sec. 3.2.1): each block's tables (and each tail unit's pair tables) quantised to int8 with the block's
+        //    power-of-two scale; the wave that builds a block is the one that looks it up, so the shifts stay in its
+        //    registers
+        int bshift[U], tshift[kMaxUnits];
+#pragma unroll
+        for (int u = 0; u < U; ++u) bshift[u] = 0;
+#pragma unroll
+        for (int t = 0; t < kMaxUnits; ++t) tshift[t] = 0;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int blk = wave + WAVES * u;
             if (blk < nblk) {
+                const int8_t* a0 = reinterpret_cast<const int8_t*>(codes) + blk * kTl2BlockK + 3 * lane;
+                if constexpr (LOSSY) {
+                    // the block's largest |entry|: the largest |a0| + |a1| + |a2| of its triples
+                    int mx = 0;
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int8_t* a = a0 + 3 * 64 * h;
+                        mx = max(mx, abs((int)a[0]) + abs((int)a[1]) + abs((int)a[2]));
+                    }
+                    bshift[u] = lossy_shift_of(wave_max_int(mx));
+                }
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     const int g = lane + 64 * h;
-                    const int8_t* a = reinterpret_cast<const int8_t*>(codes) + blk * kTl2BlockK + 3 * g;
+                    const int8_t* a = a0 + 3 * 64 * h;
                     uint32_t w[8];
                     triple_table(a[0], a[1], a[2], w);
+                    if constexpr (LOSSY) quantize_words(w, bshift[u]);
                     store_words(tables + blk * kBlockBytes28 + skewed_slot(g) * kSlot28, w, 7);
                 }
             }
         }
-        if (wave == tail_wave && lane < 32) {
-            for (int t = 0; t < units; ++t) {
-                const int8_t* b = reinterpret_cast<const int8_t*>(codes) + three + kSubK * t + 2 * lane;
-                uint32_t w[8];
-                pair_table(b[0], b[1], w);
-                store_words(pairs + (t * 32 + lane) * kSlot28, w, 5);
+        if (wave == tail_wave) {
+#pragma unroll
+            for (int t = 0; t < kMaxUnits; ++t) {
+                if (t < units) {
+                    const int8_t* b = reinterpret_cast<const int8_t*>(codes) + three + kSubK * t + 2 * (lane & 31);
+                    if constexpr (LOSSY)
+                        tshift[t] = lossy_shift_of(wave_max_int(lane < 32 ? abs((int)b[0]) + abs((int)b[1]) : 0));
+                    if (lane < 32) {
+                        uint32_t w[8];
+                        pair_table(b[0], b[1], w);
+                        if constexpr (LOSSY) quantize_words(w, tshift[t]);
+                        store_words(pairs + (t * 32 + lane) * kSlot28, w, 5);
+                    }
+                }
             }
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -673,25 +701,29 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_stream_kernel(FusedLinears L, 
                 const int blk = wave + WAVES * u;
                 if (blk < nblk) {
                     const uint8_t* base = tables + blk * kBlockBytes28 + skewed_slot(32 * q) * kSlot28;
+                    int bsum = 0;
 #pragma unroll
                     for (int i = 0; i < 32; ++i) {
                         const uint32_t word = i < 8 ? iw[u].x : i < 16 ? iw[u].y : i < 24 ? iw[u].z : iw[u].w;
                         const int idx = (int)((word >> (4 * (i & 7))) & 15u);
                         const int msk = -(int)((sw[u] >> i) & 1u);
-                        acc += lds_i16(base + i * kSlot28 + 2 * idx) ^ msk;
+                        bsum += lds_i16(base + i * kSlot28 + 2 * idx) ^ msk;
                     }
-                    acc += __popc(sw[u]);
+                    bsum += __popc(sw[u]);
+                    acc += LOSSY ? bsum << bshift[u] : bsum;
                 }
             }
             if (wave == tail_wave) {
 #pragma unroll
                 for (int t = 0; t < kMaxUnits; ++t) {
                     if (t < units) {
+                        int usum = 0;
 #pragma unroll
                         for (int i = 0; i < 8; ++i) {
                             const int code = (int)((tw[t] >> (4 * i)) & 15u);
-                            acc += lds_i16(pairs + (t * 32 + 8 * q + i) * kSlot28 + 2 * code);
+                            usum += lds_i16(pairs + (t * 32 + 8 * q + i) * kSlot28 + 2 * code);
                         }
+                        acc += LOSSY ? usum << tshift[t] : usum;
                     }
                 }
             }
@@ -1428,43 +1460,52 @@ bool tl2_stream_fits(int K) {
     return K >= kTl2BlockK && tl2_stream_lds_bytes(K) + 2 * 16 * 16 * 4 + 256 <= 160 * 1024;
 }
 
-template <int WAVES, int U, int XV>
+template <int WAVES, int U, int XV, bool LOSSY>
 hipError_t launch_stream_cfg(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
                              hipStream_t stream) {
     const size_t lds = tl2_stream_lds_bytes(K);
-    const void* kern = x ? reinterpret_cast<const void*>(tl2_stream_kernel<WAVES, U, XV, true>)
-                         : reinterpret_cast<const void*>(tl2_stream_kernel<WAVES, U, XV, false>);
+    const void* kern = x ? reinterpret_cast<const void*>(tl2_stream_kernel<WAVES, U, XV, true, LOSSY>)
+                         : reinterpret_cast<const void*>(tl2_stream_kernel<WAVES, U, XV, false, LOSSY>);
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * WAVES, lds) != hipSuccess || occ <= 0) occ = 1;
     const int64_t max_g = (int64_t)device_cus() * occ;
     const int64_t rounds = (L.total + max_g - 1) / max_g;
     const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * WAVES);
     if (x)
-        hipLaunchKernelGGL((tl2_stream_kernel<WAVES, U, XV, true>), grid, block, lds, stream, L, x, K, xq, s, rs);
+        hipLaunchKernelGGL((tl2_stream_kernel<WAVES, U, XV, true, LOSSY>), grid, block, lds, stream, L, x, K, xq, s,
+                           rs);
     else
-        hipLaunchKernelGGL((tl2_stream_kernel<WAVES, U, XV, false>), grid, block, lds, stream, L, x, K, xq, s, rs);
+        hipLaunchKernelGGL((tl2_stream_kernel<WAVES, U, XV, false, LOSSY>), grid, block, lds, stream, L, x, K, xq, s,
+                           rs);
     return hipGetLastError();
 }
 
-template <int WAVES, int U>
+template <int WAVES, int U, bool LOSSY>
 hipError_t launch_stream_u(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
                            hipStream_t stream) {
     const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
-    if (xv <= 1) return launch_stream_cfg<WAVES, U, 1>(L, x, K, xq, s, rs, stream);
-    if (xv <= 2) return launch_stream_cfg<WAVES, U, 2>(L, x, K, xq, s, rs, stream);
-    if (xv <= 4) return launch_stream_cfg<WAVES, U, 4>(L, x, K, xq, s, rs, stream);
-    return launch_stream_cfg<WAVES, U, 8>(L, x, K, xq, s, rs, stream);
+    if (xv <= 1) return launch_stream_cfg<WAVES, U, 1, LOSSY>(L, x, K, xq, s, rs, stream);
+    if (xv <= 2) return launch_stream_cfg<WAVES, U, 2, LOSSY>(L, x, K, xq, s, rs, stream);
+    if (xv <= 4) return launch_stream_cfg<WAVES, U, 4, LOSSY>(L, x, K, xq, s, rs, stream);
+    return launch_stream_cfg<WAVES, U, 8, LOSSY>(L, x, K, xq, s, rs, stream);
+}
+
+template <bool LOSSY>
+hipError_t launch_tl2_stream_t(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                               int32_t* x_rowsum, hipStream_t stream) {
+    const int nblk = K / kTl2BlockK;
+    if (nblk <= 4) return launch_stream_u<4, 1, LOSSY>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nblk <= 8) return launch_stream_u<8, 1, LOSSY>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nblk <= 16) return launch_stream_u<8, 2, LOSSY>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nblk <= 32) return launch_stream_u<16, 2, LOSSY>(L, x, K, xq, x_scale, x_rowsum, stream);
+    return launch_stream_u<16, 3, LOSSY>(L, x, K, xq, x_scale, x_rowsum, stream);
 }
 
 // Waves and blocks per wave: every block of a row has its wave (at most three per wave).
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
-                             int32_t* x_rowsum, hipStream_t stream) {
-    const int nblk = K / kTl2BlockK;
-    if (nblk <= 4) return launch_stream_u<4, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
-    if (nblk <= 8) return launch_stream_u<8, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
-    if (nblk <= 16) return launch_stream_u<8, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
-    if (nblk <= 32) return launch_stream_u<16, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
-    return launch_stream_u<16, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+                             int32_t* x_rowsum, hipStream_t stream, bool lossy) {
+    return lossy ? launch_tl2_stream_t<true>(L, x, K, xq, x_scale, x_rowsum, stream)
+                 : launch_tl2_stream_t<false>(L, x, K, xq, x_scale, x_rowsum, stream);
 }
 
 size_t tl2_mfma_lds_bytes(int M, int K) { return (size_t)kTl2MfmaTables + (size_t)M * (K + 16); }

@@ -25,7 +25,8 @@ def _route(layout):
 
 @pytest.mark.parametrize("layout", ["tl2_0", "tl1_0"])
 @pytest.mark.parametrize("M,N,K", [(1, 16, 64), (1, 32, 448), (2, 48, 832), (3, 64, 1600), (8, 208, 3200),
-                                   (5, 64, 4096), (1, 3200, 8640), (11, 32, 14336), (17, 16, 384)])
+                                   (5, 64, 4096), (1, 3200, 8640), (11, 32, 14336), (17, 16, 384), (1, 48, 384),
+                                   (1, 1024, 4096), (1, 64, 14336), (1, 16, 12352)])
 def test_lossy_parity(layout, M, N, K):
     _announce("lossy", layout, M, N, K)
     pack_ref, gemm_ref = _route(layout)
@@ -43,9 +44,10 @@ def test_lossy_parity(layout, M, N, K):
 
 
 @pytest.mark.parametrize("layout", ["tl2_0", "tl1_0"])
-def test_lossy_is_exact_when_tables_fit_int8(layout):
-    _announce("lossy exact", layout)
-    N, K, M = 64, 832, 3
+@pytest.mark.parametrize("M", [1, 3])
+def test_lossy_is_exact_when_tables_fit_int8(layout, M):
+    _announce("lossy exact", layout, M)
+    N, K = 64, 832
     W = inputs.weight_f32(N, K, seed=inputs.seed_for(15, 900))
     packed, w_scale = H.pack(W, layout)
     rng = np.random.default_rng(4)
