@@ -255,12 +255,17 @@ bitnet_status mpgemm_run(int layout, const void* packed, size_t packed_bytes, co
                          float* y, int32_t* acc, void* ws, size_t ws_bytes, hipStream_t s) {
     (void)packed_bytes;
     if (lossy_layout(layout)) {
-        // TL2_0 / TL1_0: table lookups on int8-quantised tables; one TL2_0 token on the persistent table kernel
-        // (every work group builds the row's tables once), else slices of 8 tokens
+        // TL2_0 / TL1_0: table lookups on int8-quantised tables; one token on the persistent table kernels (every
+        // work group builds the row's tables once), else slices of 8 tokens
         if (layout == BITNET_LAYOUT_TL2_0 && M == 1 && bitnet::tl2_stream_fits((int)K))
             return hip_status(bitnet::launch_tl2_stream(one_linear(packed, w_scale, N, y, acc), nullptr, (int)K,
                                                         const_cast<int8_t*>(xq), const_cast<float*>(x_scale), nullptr,
                                                         s, true),
+                              "bitnet_mpgemm launch");
+        if (layout == BITNET_LAYOUT_TL1_0 && M == 1 && bitnet::tl1_stream_fits((int)K))
+            return hip_status(bitnet::launch_tl1_lossy_stream(one_linear(packed, w_scale, N, y, acc), nullptr, (int)K,
+                                                              const_cast<int8_t*>(xq), const_cast<float*>(x_scale),
+                                                              nullptr, s),
                               "bitnet_mpgemm launch");
         return hip_status(lookup_sliced(layout == BITNET_LAYOUT_TL1_0, true, one_linear(packed, w_scale, N, y, acc),
                                         xq, x_scale, M, K, s),
@@ -439,6 +444,10 @@ bitnet_status bitnet_mpgemm_fused(int layout, int n_linears, const void* const* 
             // one token: the persistent table kernel (the row quantised inside when x is given)
             return hip_status(bitnet::launch_tl2_stream(L, quantise ? x : nullptr, (int)K, xq, x_scale, x_rowsum, s,
                                                         true),
+                              "bitnet_mpgemm_fused launch");
+        if (layout == BITNET_LAYOUT_TL1_0 && M == 1 && bitnet::tl1_stream_fits((int)K))
+            return hip_status(bitnet::launch_tl1_lossy_stream(L, quantise ? x : nullptr, (int)K, xq, x_scale, x_rowsum,
+                                                              s),
                               "bitnet_mpgemm_fused launch");
         if (quantise && M == 1) {
             const hipError_t e =

@@ -266,6 +266,11 @@ hipError_t launch_tl2_mfma_quant(const FusedLinears& L, const float* x, int K, i
 // i2s_out[i]), for the prefill GEMM; one launch.
 hipError_t launch_tl2_to_i2s(const void* const* packed, const int* N, void* const* i2s_out, int count, int K,
                              hipStream_t stream);
+// One token, TL1_0, every weight of L in one launch: the whole row's int8 pair tables built once per work group
+// (x set: the row quantised inside, as launch_tl2_stream).  Only where tl1_stream_fits(K).
+bool tl1_stream_fits(int K);
+hipError_t launch_tl1_lossy_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                                   int32_t* x_rowsum, hipStream_t stream);
 // lossy: TL2_0 (Sec. 3.2.1), each block's tables quantised to int8 with its power-of-two scale.
 hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
                              int32_t* x_rowsum, hipStream_t stream, bool lossy = false);

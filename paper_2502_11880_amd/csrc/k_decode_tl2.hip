@@ -769,6 +769,216 @@ __global__ __launch_bounds__(64 * WAVES) void tl2_stream_kernel(FusedLinears L, 
     else run(std::true_type{});
 }
 
+// One token, TL1_0 (lossy TL1, Table 1; Sec. 3.2.1), persistent: each work group quantises the row (or copies the
+// given codes), builds the pair tables (Table 5, Algorithm TL1) of the whole row once, each unit's tables quantised
+// to int8 with the unit's power-of-two scale, and then walks the row groups g = blockIdx.x, blockIdx.x + gridDim.x,
+// ... of all the launch's weights with the next row group's words in flight.  Wave w builds and reads the tables of
+// blocks w, w + WAVES, ... (256 k each: 4 units of 32 pairs), so the unit shifts stay in its registers.
+constexpr int kSlot20 = 20;                                  // 10 int16 per pair table (9 used)
+constexpr int kTl1BlockBytes20 = 128 * kSlot20;               // the 128 pair tables of a 256-k block
+
+template <int WAVES, int U, int XV, bool QUANT>
+__global__ __launch_bounds__(64 * WAVES) void tl1_lossy_stream_kernel(FusedLinears L, const float* __restrict__ x,
+                                                                      int K, int8_t* __restrict__ xq,
+                                                                      float* __restrict__ x_scale,
+                                                                      int32_t* __restrict__ x_rowsum) {
+    extern __shared__ __align__(16) uint8_t lds[];    // codes | pair tables
+    __shared__ int part[2][WAVES][16];
+    __shared__ float redf[WAVES];
+    __shared__ int redi[WAVES];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int q = lane >> 4;
+    const int pr = lane & 31, hh = lane >> 5;                  // this lane builds pair pr of units hh and 2 + hh
+    const int G = gridDim.x, bid = blockIdx.x;
+    const int nsub = K / kSubK;
+    const int nkb = (nsub + 3) / 4;
+    uint8_t* codes = lds;
+    uint8_t* tables = lds + ((K + 15) & ~15);
+    const int S = (L.total - bid + G - 1) / G;                 // row groups of this work group (grid <= total)
+
+    // the loads of row group step st: word j of the lane's 4 T bytes of each of its blocks in the I2_S tiling (units
+    // past T, and blocks past nkb, repeat real words; all unconditional)
+    auto issue = [&](uint32_t (&wd)[U][4], float& bw, int st) {
+        int li, rg;
+        locate(L, bid + st * G, li, rg);
+        const uint8_t* rgbase = pick(L.packed, li) + (size_t)rg * 4 * K;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int blk = min(wave + WAVES * u, nkb - 1);
+            const int T = min(4, nsub - 4 * blk);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                wd[u][j] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(
+                    rgbase + (size_t)blk * 1024 + 4 * T * lane + 4 * min(j, T - 1)));
+        }
+        bw = *pick(L.w_scale, li);
+    };
+
+    auto run = [&](auto multi) {
+        constexpr bool kMulti = decltype(multi)::value;
+        // 1. the activation row, the first row group's words, then the quantisation (or the given codes)
+        const float4* x4 = reinterpret_cast<const float4*>(x);
+        const int K4 = K >> 2;
+        float4 xv[XV];
+        if (QUANT) {
+#pragma unroll
+            for (int i = 0; i < XV; ++i) {
+                const int e = tid + i * 64 * WAVES;
+                const float4 v = x4[e < K4 ? e : K4 - 1];
+                xv[i] = e < K4 ? v : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+        }
+        uint32_t wa[U][4], wb[U][4];
+        float ba = 0.0f, bb = 0.0f;
+        issue(wa, ba, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        float sx;
+        if (QUANT) {
+            float amax = 0.0f;
+#pragma unroll
+            for (int i = 0; i < XV; ++i)
+                amax = fmaxf(amax, fmaxf(fmaxf(fabsf(xv[i].x), fabsf(xv[i].y)), fmaxf(fabsf(xv[i].z), fabsf(xv[i].w))));
+            amax = wave_max_all(amax);
+            if (lane == 0) redf[wave] = amax;
+            __syncthreads();
+            amax = redf[0];
+#pragma unroll
+            for (int w = 1; w < WAVES; ++w) amax = fmaxf(amax, redf[w]);
+            sx = 127.0f / fmaxf(amax, 1e-5f);
+            int sum = 0;
+#pragma unroll
+            for (int i = 0; i < XV; ++i) {
+                const int e = tid + i * 64 * WAVES;
+                if (e < K4) {
+                    const uint32_t c = quant4(xv[i], sx);
+                    sum = byte_sum4(c, sum);
+                    reinterpret_cast<uint32_t*>(codes)[e] = c;
+                    if (bid == 0) reinterpret_cast<uint32_t*>(xq)[e] = c;
+                }
+            }
+            sum = wave_sum_all(sum);
+            if (lane == 0) redi[wave] = sum;
+        } else {
+            for (int e = tid; e < K4; e += 64 * WAVES)
+                reinterpret_cast<uint32_t*>(codes)[e] = reinterpret_cast<const uint32_t*>(xq)[e];
+            sx = x_scale[0];
+        }
+        if constexpr (kMulti) issue(wb, bb, 1);
+        __syncthreads();                                   // every code (and every wave's code sum) is in LDS
+        if (QUANT && bid == 0 && tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < WAVES; ++w) tot += redi[w];
+            x_scale[0] = sx;
+            x_rowsum[0] = tot;
+        }
+
+        // 2. this wave's tables, once, and the shift of each of their units
+        int bsh[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bsh[u][j] = 0;
+            const int blk = wave + WAVES * u;
+            if (blk < nkb) {
+                const int T = min(4, nsub - 4 * blk);
+                const bool ok0 = hh < T, ok1 = 2 + hh < T;
+                const int u0 = min(hh, T - 1), u1 = min(2 + hh, T - 1);
+                const int8_t* cb = reinterpret_cast<const int8_t*>(codes) + blk * kI2sBlockK + 2 * pr;
+                const int a0 = cb[kSubK * u0], a1 = cb[kSubK * u0 + 1];
+                const int b0 = cb[kSubK * u1], b1 = cb[kSubK * u1 + 1];
+                int lo0, hi0, lo1, hi1;
+                half_wave_max(ok0 ? abs(a0) + abs(a1) : 0, lo0, hi0);
+                half_wave_max(ok1 ? abs(b0) + abs(b1) : 0, lo1, hi1);
+                bsh[u][0] = lossy_shift_of(lo0);
+                bsh[u][1] = lossy_shift_of(hi0);
+                bsh[u][2] = lossy_shift_of(lo1);
+                bsh[u][3] = lossy_shift_of(hi1);
+                uint8_t* tb = tables + (size_t)blk * kTl1BlockBytes20;
+                uint32_t w[8];
+                if (ok0) {
+                    pair_table(a0, a1, w);
+                    quantize_words(w, hh ? bsh[u][1] : bsh[u][0]);
+                    store_words(tb + (32 * hh + pr) * kSlot20, w, 5);
+                }
+                if (ok1) {
+                    pair_table(b0, b1, w);
+                    quantize_words(w, hh ? bsh[u][3] : bsh[u][2]);
+                    store_words(tb + (64 + 32 * hh + pr) * kSlot20, w, 5);
+                }
+            }
+        }
+        // the tables a lane wrote are read by the other lanes of its wave only
+        wave_lds_handoff();
+
+        // 3. the stream
+        int par = 0;
+        auto compute = [&](const uint32_t (&wd)[U][4], float bw, int st) {
+            int acc = 0;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int blk = wave + WAVES * u;
+                if (blk < nkb) {
+                    const int T = min(4, nsub - 4 * blk);
+                    const uint8_t* tb = tables + (size_t)blk * kTl1BlockBytes20;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        if (j < T) {
+                            int us = 0;
+#pragma unroll
+                            for (int i = 0; i < 8; ++i) {
+                                // pair i of the word: byte i % 4, low nibble for i < 4; pair 8 q + i of unit j
+                                const int code = (int)((wd[u][j] >> (8 * (i & 3) + 4 * (i >> 2))) & 15u);
+                                us += lds_i16(tb + (32 * j + 8 * q + i) * kSlot20 + 2 * code);
+                            }
+                            acc += us << bsh[u][j];
+                        }
+                    }
+                }
+            }
+            acc += __shfl_xor(acc, 16, 64);
+            acc += __shfl_xor(acc, 32, 64);
+            if (lane < 16) part[par][wave][lane] = acc;
+            __syncthreads();
+            if (wave == 0 && lane < 16) {
+                int v = 0;
+#pragma unroll
+                for (int w = 0; w < WAVES; ++w) v += part[par][w][lane];
+                int li, rg;
+                locate(L, bid + st * G, li, rg);
+                const int n = rg * kRowsPerGroup + lane;
+                pick(L.y, li)[n] = (float)v * (bw / sx);
+                int32_t* acc_out = pick(L.acc, li);
+                if (acc_out) acc_out[n] = v;
+            }
+            par ^= 1;
+        };
+        if constexpr (!kMulti) {
+            compute(wa, ba, 0);
+            return;
+        }
+        int st = 0;
+        for (; st + 3 < S; st += 2) {
+            compute(wa, ba, st);
+            issue(wa, ba, st + 2);
+            compute(wb, bb, st + 1);
+            issue(wb, bb, st + 3);
+        }
+        if (st + 2 < S) {
+            compute(wa, ba, st);
+            issue(wa, ba, st + 2);
+            compute(wb, bb, st + 1);
+            compute(wa, ba, st + 2);
+        } else {
+            compute(wa, ba, st);
+            compute(wb, bb, st + 1);
+        }
+    };
+    if (S == 1) run(std::false_type{});
+    else run(std::true_type{});
+}
+
 // Several tokens (up to 16 per launch), TL2 on int8 MFMA.  Table lookups cost one LDS read per token and triple,
 // so past one token the packed triples are instead expanded to int8 weights in registers and multiplied on
 // v_mfma_i32_16x16x64_i8, the same contraction the I2_S kernels run; the expansion is shared by every token.
@@ -1506,6 +1716,57 @@ hipError_t launch_tl2_stream(const FusedLinears& L, const float* x, int K, int8_
                              int32_t* x_rowsum, hipStream_t stream, bool lossy) {
     return lossy ? launch_tl2_stream_t<true>(L, x, K, xq, x_scale, x_rowsum, stream)
                  : launch_tl2_stream_t<false>(L, x, K, xq, x_scale, x_rowsum, stream);
+}
+
+size_t tl1_stream_lds_bytes(int K) {
+    return (size_t)((K + 15) & ~15) + (size_t)((K / kSubK + 3) / 4) * kTl1BlockBytes20;
+}
+
+bool tl1_stream_fits(int K) {
+    const int nkb = (K / kSubK + 3) / 4;
+    return K >= kSubK && nkb <= 64 && tl1_stream_lds_bytes(K) + 2 * 16 * 16 * 4 + 256 <= 160 * 1024;
+}
+
+template <int WAVES, int U, int XV>
+hipError_t launch_tl1_stream_cfg(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
+                                 hipStream_t stream) {
+    const size_t lds = tl1_stream_lds_bytes(K);
+    const void* kern = x ? reinterpret_cast<const void*>(tl1_lossy_stream_kernel<WAVES, U, XV, true>)
+                         : reinterpret_cast<const void*>(tl1_lossy_stream_kernel<WAVES, U, XV, false>);
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 64 * WAVES, lds) != hipSuccess || occ <= 0) occ = 1;
+    const int64_t max_g = (int64_t)device_cus() * occ;
+    const int64_t rounds = (L.total + max_g - 1) / max_g;
+    const dim3 grid((unsigned)((L.total + rounds - 1) / rounds)), block(64 * WAVES);
+    if (x)
+        hipLaunchKernelGGL((tl1_lossy_stream_kernel<WAVES, U, XV, true>), grid, block, lds, stream, L, x, K, xq, s, rs);
+    else
+        hipLaunchKernelGGL((tl1_lossy_stream_kernel<WAVES, U, XV, false>), grid, block, lds, stream, L, x, K, xq, s,
+                           rs);
+    return hipGetLastError();
+}
+
+template <int WAVES, int U>
+hipError_t launch_tl1_stream_u(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
+                               hipStream_t stream) {
+    const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
+    if (xv <= 1) return launch_tl1_stream_cfg<WAVES, U, 1>(L, x, K, xq, s, rs, stream);
+    if (xv <= 2) return launch_tl1_stream_cfg<WAVES, U, 2>(L, x, K, xq, s, rs, stream);
+    if (xv <= 4) return launch_tl1_stream_cfg<WAVES, U, 4>(L, x, K, xq, s, rs, stream);
+    return launch_tl1_stream_cfg<WAVES, U, 8>(L, x, K, xq, s, rs, stream);
+}
+
+// Waves and blocks per wave: every 256-k block of the row has its wave (at most four per wave).
+hipError_t launch_tl1_lossy_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* x_scale,
+                                   int32_t* x_rowsum, hipStream_t stream) {
+    if (!tl1_stream_fits(K)) return hipErrorInvalidValue;
+    const int nkb = (K / kSubK + 3) / 4;
+    if (nkb <= 4) return launch_tl1_stream_u<4, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nkb <= 8) return launch_tl1_stream_u<8, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nkb <= 16) return launch_tl1_stream_u<16, 1>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nkb <= 32) return launch_tl1_stream_u<16, 2>(L, x, K, xq, x_scale, x_rowsum, stream);
+    if (nkb <= 48) return launch_tl1_stream_u<16, 3>(L, x, K, xq, x_scale, x_rowsum, stream);
+    return launch_tl1_stream_u<16, 4>(L, x, K, xq, x_scale, x_rowsum, stream);
 }
 
 size_t tl2_mfma_lds_bytes(int M, int K) { return (size_t)kTl2MfmaTables + (size_t)M * (K + 16); }
