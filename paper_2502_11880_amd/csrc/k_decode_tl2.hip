@@ -1784,10 +1784,11 @@ int tl2_mfma_max_tokens(int K) {
 }
 
 bool tl2_mfma_quant_fits(int K) {
-    // one token quantised inside: the fp32 row in registers, at most 8 float4 per thread of 16 waves (16 float4
-    // beside two batches of weight words need a stack frame, and that kernel ran 2.5x slower than the quantiser
-    // followed by the kernel that reads the codes)
-    return tl2_mfma_max_tokens(K) >= 1 && K / 4 <= 8 * 64 * 16;
+    // one token quantised inside: the fp32 row in registers, at most 9 float4 per thread of 16 waves (K <= 36864,
+    // the 100B-class down projection's 33024 included: 106 registers, no stack; 16 float4 beside two batches of
+    // weight words need a stack frame, and that kernel ran 2.5x slower than the quantiser followed by the kernel
+    // that reads the codes)
+    return tl2_mfma_max_tokens(K) >= 1 && K / 4 <= 9 * 64 * 16;
 }
 
 template <int WAVES, int U, int CH, int XV, bool MB = false>
@@ -1826,10 +1827,11 @@ hipError_t launch_mfma_quant(const FusedLinears& L, const float* x, int8_t* xq, 
     return launch_mfma_kernel<WAVES, U, 1, 8>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
 }
 
-// One token quantised inside, row groups in several batches (K past 48 blocks, K / 4 <= 8192).
+// One token quantised inside, row groups in several batches (K past 48 blocks, K / 4 <= 9216).
 hipError_t launch_mfma_quant_mb(const FusedLinears& L, const float* x, int8_t* xq, float* x_scale,
                                 int32_t* x_rowsum, int K, hipStream_t stream) {
-    return launch_mfma_kernel<16, 3, 1, 8, true>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
+    if (K / 4 <= 8 * 64 * 16) return launch_mfma_kernel<16, 3, 1, 8, true>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
+    return launch_mfma_kernel<16, 3, 1, 9, true>(L, x, xq, x_scale, x_rowsum, 1, K, stream);
 }
 
 // One token, quantised inside (tl2_mfma_quant_fits(K)).

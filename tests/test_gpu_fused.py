@@ -143,8 +143,8 @@ def test_fused_one_token_workload_groups(K, Ns):
 # The 100B-class layer's groups at one token (the launches of the stack benchmark), every layout.  I2_S and TL1: q/k/v
 # (2304 row groups: 256 work groups of <16, 3, 4> walking nine row groups each), o and down (768 row groups:
 # three per work group; down <16, 3, 9> with three batches per row group), gate/up (4128 row groups).  TL2: every
-# group on the MFMA expansion, q/k/v, o and gate/up with the row quantised inside; down (K = 33024, 86 blocks) after
-# the quantiser, in two batches per row group.
+# group on the MFMA expansion with the row quantised inside; down (K = 33024, 86 blocks: 9 float4 of the row per
+# thread) in two batches per row group.
 @pytest.mark.parametrize("K,Ns", [(12288, [12288, 12288, 12288]), (12288, [12288]), (12288, [33024, 33024]),
                                   (33024, [12288])])
 def test_fused_one_token_100b_groups(K, Ns):

@@ -123,12 +123,13 @@ def test_tl2_stream_one_token(N, K):
 # One token as one launch for several weights that share the activation, quantised inside the launch (the MFMA
 # kernel with the row converted in each work group): every wave configuration, 1 to 8 float4 of the row per
 # thread (K = 16512: five, rounded up to eight), with and without a TL1 tail; past 48 blocks, row groups in two or
-# three batches with 8 float4 per thread (K = 19264 with a 1-unit tail; K = 32768, the longest such row), and past
-# 8 float4 per thread the quantiser followed by the multi-batch kernel (K = 33024; K = 65472 with a 3-unit tail).
+# three batches with 8 float4 per thread (K = 19264 with a 1-unit tail; K = 32768) or 9 (K = 33024, the 100B-class
+# down projection; K = 36864, the longest such row), and past 9 float4 per thread the quantiser followed by the
+# multi-batch kernel (K = 36928; K = 65472 with a 3-unit tail).
 @pytest.mark.parametrize("K,Ns", [(3200, [3200, 3200, 3200]), (4096, [4096, 1024, 1024]), (8640, [3200, 16]),
                                   (14336, [4096]), (1536, [64, 48]), (16512, [32]), (448, [2400]),
                                   (2304, [48]), (4480, [64, 32]), (19264, [48]), (32768, [64, 16]),
-                                  (33024, [64, 16]), (65472, [32])])
+                                  (33024, [64, 16]), (36864, [32]), (36928, [16]), (65472, [32])])
 def test_tl2_one_token_fused(K, Ns):
     _announce("tl2 one token fused", K, Ns)
     from tests.test_gpu_fused import _fused_case
