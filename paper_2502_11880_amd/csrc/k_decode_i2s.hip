@@ -29,16 +29,6 @@
 namespace bitnet {
 namespace {
 
-__device__ __forceinline__ int q8(float v, float s) {
-    return (int)fminf(fmaxf(rintf(v * s), -128.0f), 127.0f);
-}
-
-__device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
-
 // Words per lane of block kb: 4 for a full 256-k block, (K mod 256) / 64 for a short last one.
 __device__ __forceinline__ int block_T(int kb, int nfull, int Tlast) { return kb < nfull ? 4 : Tlast; }
 

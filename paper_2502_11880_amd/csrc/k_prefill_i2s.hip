@@ -421,7 +421,7 @@ struct FinishLinears {
 };
 
 __global__ __launch_bounds__(256) void prefill_splitk_finish(FinishLinears F, const int32_t* __restrict__ part,
-                                                             int64_t slice, int splits, int M,
+                                                             int64_t slice, int splits,
                                                              const int32_t* __restrict__ x_rowsum,
                                                              const float* __restrict__ x_scale) {
     const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -567,7 +567,7 @@ hipError_t launch_i2s_prefill(const FusedLinears& L, const int8_t* xq, const flo
         }
         F.total4 = q4;
         hipLaunchKernelGGL(prefill_splitk_finish, dim3((unsigned)((q4 + 255) / 256)), dim3(256), 0, stream, F, part,
-                           (int64_t)M * ntot, splits, M, x_rowsum, x_scale);
+                           (int64_t)M * ntot, splits, x_rowsum, x_scale);
     }
     return hipGetLastError();
 }
