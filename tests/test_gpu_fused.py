@@ -85,6 +85,17 @@ def test_fused_i2s_streaming_tokens(M, K, Ns):
     _fused_case("i2s", M, K, Ns, seed=inputs.seed_for(2, 700 + M + K))
 
 
+# 2..12 tokens through the fused call, both word formats: 1, 2 and 3 token groups of the multi-token stream,
+# K = 4160 (a 64-k last block), K = 4032 (a 192-k last block), K = 8192, several row groups per work group
+# (2900 row groups) and a single row group.
+@pytest.mark.parametrize("M,K,Ns", [(4, 4096, [1024, 2048]), (12, 4096, [4096, 1024]), (7, 4032, [640, 16]),
+                                    (3, 4160, [512]), (4, 8192, [2048, 2048]), (2, 8192, [16]),
+                                    (9, 1088, [16000, 16000, 14400])])
+def test_fused_few_tokens(M, K, Ns):
+    _announce("fused few tokens", M, K, Ns)
+    _fused_case(("i2s", "tl1"), M, K, Ns, seed=inputs.seed_for(17, M * 13 + K + len(Ns)))
+
+
 # More than 16 tokens: one prefill launch over the weights' concatenated row tiles; with a workspace from
 # bitnet_mpgemm_fused_workspace_bytes small grids also split K over all the weights.
 @pytest.mark.parametrize("M,K,Ns", [(40, 832, [48, 16, 64]), (300, 3200, [3200, 3200, 3200]),
