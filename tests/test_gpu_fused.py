@@ -163,10 +163,12 @@ def test_fused_one_token_100b_groups(K, Ns):
     _fused_case(("i2s", "tl2", "tl1"), 1, K, Ns, seed=inputs.seed_for(4, 10 * len(Ns) + K % 7))
 
 
-def _fused_case_lossy(layout, M=3, K=1600, Ns=(64, 208)):
+def _fused_case_lossy(layout, M=3, K=1600, Ns=(64, 208), sample_groups=None):
     """bitnet_mpgemm_fused on a lossy layout: one table-lookup launch per slice of up to 8 tokens over every weight
     (one token quantised inside it, else the quantiser first); the codes, scales and sums bit-exact, the outputs
-    equal to the separate calls and to the oracle's lossy route."""
+    equal to the separate calls and to the oracle's lossy route.  sample_groups: the oracle route runs on the first,
+    the last and that many seeded random 16-row groups of each weight (rows are independent in the packing and in
+    the route, so packing only those rows gives their exact values); the separate calls are compared everywhere."""
     Ws = [inputs.weight_f32(N, K, seed=inputs.seed_for(15, 500 + i)) for i, N in enumerate(Ns)]
     x = inputs.activation_f32(M, K, seed=inputs.seed_for(15, 599))
     packs = [H.pack(W, layout) for W in Ws]
@@ -181,9 +183,17 @@ def _fused_case_lossy(layout, M=3, K=1600, Ns=(64, 208)):
     assert np.array_equal(H.to_np(rs), xq_ref.astype(np.int64).sum(1))
     route = O.elut_gemm_lossy if layout == "tl2_0" else O.elut_gemm_tl1_lossy
     pack = O.pack_tl2 if layout == "tl2_0" else O.pack_tl1
-    for W, (p, b), y, N in zip(Ws, packs, ys, Ns):
+    for i, (W, (p, b), y, N) in enumerate(zip(Ws, packs, ys, Ns)):
         t_ref, beta = O.ternarize(W.numpy())
-        acc_ref = route(xq_ref, pack(t_ref), N, K)
-        H.check_y(H.to_np(y), O.epilogue(acc_ref, beta, s_ref), acc_ref)
+        if sample_groups is None:
+            rows = np.arange(N)
+        else:
+            groups = N // 16
+            pick = np.random.default_rng(inputs.seed_for(15, 700 + i)).choice(groups, size=sample_groups,
+                                                                                 replace=False)
+            groups_sel = np.unique(np.concatenate([[0, groups - 1], pick]))
+            rows = (groups_sel[:, None] * 16 + np.arange(16)[None, :]).ravel()
+        acc_ref = route(xq_ref, pack(np.ascontiguousarray(t_ref[rows])), len(rows), K)
+        H.check_y(H.to_np(y)[:, rows], O.epilogue(acc_ref, beta, s_ref), acc_ref)
         y_sep, _ = H.mpgemm(layout, p, b, N, K, xq, s)
         assert np.array_equal(H.to_np(y), H.to_np(y_sep))

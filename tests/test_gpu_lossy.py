@@ -67,3 +67,14 @@ def test_lossy_fused(layout, M, K, Ns):
     _announce("lossy fused", layout, M, K, Ns)
     from tests.test_gpu_fused import _fused_case_lossy
     _fused_case_lossy(layout, M, K, Ns)
+
+
+# The 100B-class groups at one token, as the stack benchmark runs them on the lossy layouts: q/k/v (2304 row groups)
+# and o (768) on the persistent kernels (the whole row's tables in LDS), down (K = 33024) on the lookup kernels with
+# the row quantised inside.  The oracle's lossy route runs on sampled row groups.
+@pytest.mark.parametrize("layout", ["tl2_0", "tl1_0"])
+@pytest.mark.parametrize("K,Ns", [(12288, (12288, 12288, 12288)), (12288, (12288,)), (33024, (12288,))])
+def test_lossy_fused_100b_groups(layout, K, Ns):
+    _announce("lossy fused 100B-class", layout, K, Ns)
+    from tests.test_gpu_fused import _fused_case_lossy
+    _fused_case_lossy(layout, 1, K, Ns, sample_groups=6)
