@@ -119,6 +119,10 @@ def test_elut_fused_and_noalloc(fmt):
                                     (1, 640, [14336, 14336])])
 def test_elut_fused_groups(fmt, M, K, Ns):
     _announce("elut fused groups", fmt, M, K, Ns)
+    _elut_fused(fmt, M, K, Ns)
+
+
+def _elut_fused(fmt, M, K, Ns):
     C, g, mirror = O.ELUT_FORMATS[fmt]
     ws_ = [inputs.int_weights(N, K, C, seed=inputs.seed_for(13, 500 + 7 * i + K)) for i, N in enumerate(Ns)]
     x = inputs.activation_f32(M, K, seed=inputs.seed_for(13, 599 + K + M))
@@ -139,3 +143,18 @@ def test_elut_fused_groups(fmt, M, K, Ns):
         y_sep, acc = H.mpgemm(fmt, p, b, N, K, xq, s)
         assert np.array_equal(H.to_np(acc), acc_ref)
         assert np.array_equal(H.to_np(y_sep), H.to_np(y))
+
+
+# The exact groups the benchmark times on the integer-weight layouts: the 3B-class layer set at one token (every
+# format) and the 8B-class layer set at one and eight tokens (C4G2 and C5G2; C3G5 needs K % 320 == 0).
+ELUT_WORKLOAD_GROUPS = (
+    [(fmt, 1, K, Ns) for fmt in FMTS
+     for K, Ns in [(3200, [3200, 3200, 3200]), (3200, [3200]), (3200, [8640, 8640]), (8640, [3200])]] +
+    [(fmt, M, K, Ns) for fmt in ("c4g2", "c5g2") for M in (1, 8)
+     for K, Ns in [(4096, [4096, 1024, 1024]), (4096, [4096]), (4096, [14336, 14336]), (14336, [4096])]])
+
+
+@pytest.mark.parametrize("fmt,M,K,Ns", ELUT_WORKLOAD_GROUPS)
+def test_elut_fused_workload_groups(fmt, M, K, Ns):
+    _announce("elut fused workload group", fmt, M, K, Ns)
+    _elut_fused(fmt, M, K, Ns)
