@@ -85,6 +85,26 @@ def test_fused_i2s_streaming_tokens(M, K, Ns):
     _fused_case("i2s", M, K, Ns, seed=inputs.seed_for(2, 700 + M + K))
 
 
+# The 8B-class layer groups at the token counts the benchmark times, every output against the oracle: 8 and 16 tokens
+# (the multi-token stream for I2_S and TL1, the TL2 MFMA expansion on codes given) and the small-batch regime
+# (32, 64 and 112 tokens: token slices of the stream for I2_S and TL1).
+GROUPS_8B = [(4096, [4096, 1024, 1024]), (4096, [4096]), (4096, [14336, 14336]), (14336, [4096])]
+
+
+@pytest.mark.parametrize("M", [8, 16])
+@pytest.mark.parametrize("K,Ns", GROUPS_8B)
+def test_fused_few_tokens_8b_groups(M, K, Ns):
+    _announce("fused 8B-class group", M, K, Ns)
+    _fused_case(("i2s", "tl2", "tl1"), M, K, Ns, seed=inputs.seed_for(18, M * 31 + K + len(Ns)))
+
+
+@pytest.mark.parametrize("M", [32, 64, 112])
+@pytest.mark.parametrize("K,Ns", GROUPS_8B)
+def test_fused_small_batch_8b_groups(M, K, Ns):
+    _announce("fused 8B-class group, small batch", M, K, Ns)
+    _fused_case(("i2s", "tl1"), M, K, Ns, seed=inputs.seed_for(19, M * 31 + K + len(Ns)))
+
+
 # 2..12 tokens through the fused call, both word formats: 1, 2 and 3 token groups of the multi-token stream,
 # K = 4160 (a 64-k last block), K = 4032 (a 192-k last block), K = 8192, several row groups per work group
 # (2900 row groups) and a single row group.
