@@ -78,3 +78,15 @@ def test_lossy_fused_100b_groups(layout, K, Ns):
     _announce("lossy fused 100B-class", layout, K, Ns)
     from tests.test_gpu_fused import _fused_case_lossy
     _fused_case_lossy(layout, 1, K, Ns, sample_groups=6)
+
+
+# The 8B-class layer groups at one and eight tokens, as the benchmark runs them on the lossy layouts (one token: the
+# persistent kernels; eight: the quantiser, then the lookup kernels); the oracle's lossy route on sampled row groups.
+@pytest.mark.parametrize("layout", ["tl2_0", "tl1_0"])
+@pytest.mark.parametrize("M", [1, 8])
+@pytest.mark.parametrize("K,Ns", [(4096, (4096, 1024, 1024)), (4096, (4096,)), (4096, (14336, 14336)),
+                                  (14336, (4096,))])
+def test_lossy_fused_8b_groups(layout, M, K, Ns):
+    _announce("lossy fused 8B-class", layout, M, K, Ns)
+    from tests.test_gpu_fused import _fused_case_lossy
+    _fused_case_lossy(layout, M, K, Ns, sample_groups=6)
