@@ -358,8 +358,9 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_decode_stream_kernel(FusedLine
 // quantised; after that two register sets of weight words alternate: the loads of the next batch are issued before
 // the current one is multiplied, so the weight stream never waits for the arithmetic.  The last batch of a row group reduces the waves' partial sums through LDS
 // (double-buffered, one barrier) and applies the epilogue.  Every A row holds the token's codes (LDS broadcast
-// reads, no lane masking); D row 0 is the one stored.
-template <int WAVES, int U, int XV, int FMT>
+// reads, no lane masking); D row 0 is the one stored.  AREG (one batch per row group): every step multiplies the
+// same blocks of the wave, so their A operands are read from LDS once and kept in registers.
+template <int WAVES, int U, int XV, int FMT, bool AREG>
 __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinears L, const float* __restrict__ x,
                                                                       int K, int8_t* __restrict__ xq_out,
                                                                       float* __restrict__ s_out,
@@ -476,6 +477,17 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
         // 2. the stream
         const v4i zero = {0, 0, 0, 0};
         const int8_t* arow = xs + 16 * q;
+        v4i areg[AREG ? U : 1][4];
+        if constexpr (AREG) {
+    #pragma unroll
+            for (int u = 0; u < U; ++u)
+    #pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    // k past a short block or past K: any real k (never multiplied)
+                    const int k = min((wave + WAVES * u) * kI2sBlockK + kSubK * j, K - kSubK);
+                    areg[u][j] = *reinterpret_cast<const v4i*>(arow + k);
+                }
+        }
         v4i acc = zero;
         int par = 0;
         auto compute = [&](const v4u (&w)[U], float bw, int st) {
@@ -489,7 +501,7 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
                 if (kb < nfull) {
     #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j),
+                        acc = mfma16x16x64(AREG ? areg[AREG ? u : 0][j] : *reinterpret_cast<const v4i*>(ab + kSubK * j),
                                            decode_b<FMT>(word_of(w[u], j)), acc);
                 } else if (kb < nkb) {
     #pragma unroll
@@ -497,7 +509,8 @@ __global__ __launch_bounds__(64 * WAVES) void i2s_gemv1_stream_kernel(FusedLinea
                         if (j < Tlast) {
                             const int i = j + sh_tail;
                             const uint32_t wd = i == 0 ? w[u].x : i == 1 ? w[u].y : i == 2 ? w[u].z : w[u].w;
-                            acc = mfma16x16x64(*reinterpret_cast<const v4i*>(ab + kSubK * j), decode_b<FMT>(wd), acc);
+                            acc = mfma16x16x64(AREG ? areg[AREG ? u : 0][j] : *reinterpret_cast<const v4i*>(ab + kSubK * j),
+                                               decode_b<FMT>(wd), acc);
                         }
                     }
                 }
@@ -575,10 +588,10 @@ void launch_plain_u(int U, const FusedLinears& L, const int8_t* xq, const float*
 
 constexpr int64_t kDecodeStageBytes = 128 * 1024;   // LDS for the tokens' codes in the multi-token stream
 
-template <int FMT, int WAVES, int U, int XV>
+template <int FMT, int WAVES, int U, int XV, bool AREG = false>
 hipError_t launch_stream(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
                          hipStream_t stream) {
-    auto kern = i2s_gemv1_stream_kernel<WAVES, U, XV, FMT>;
+    auto kern = i2s_gemv1_stream_kernel<WAVES, U, XV, FMT, AREG>;
     const size_t lds = (size_t)K;
     // as many work groups as are resident at once, balanced so that every one walks the same number of row groups
     // (to within one).  16-wave groups: one per CU (a second resident group per CU, which the register use of the
@@ -602,6 +615,14 @@ template <int FMT, int WAVES, int U>
 hipError_t launch_stream_xv(const FusedLinears& L, const float* x, int K, int8_t* xq, float* s, int32_t* rs,
                             hipStream_t stream) {
     const int xv = (K / 4 + 64 * WAVES - 1) / (64 * WAVES);
+    if constexpr (WAVES == 16 && U <= 3) {
+        // one batch per row group: the A operands stay in registers (16 U of them; at U = 4 the kernel spills)
+        if ((K + kI2sBlockK - 1) / kI2sBlockK <= WAVES * U) {
+            if (xv <= 1) return launch_stream<FMT, WAVES, U, 1, true>(L, x, K, xq, s, rs, stream);
+            if (xv <= 2) return launch_stream<FMT, WAVES, U, 2, true>(L, x, K, xq, s, rs, stream);
+            if (xv <= 4) return launch_stream<FMT, WAVES, U, 4, true>(L, x, K, xq, s, rs, stream);
+        }
+    }
     if (xv <= 1) return launch_stream<FMT, WAVES, U, 1>(L, x, K, xq, s, rs, stream);
     if (xv <= 2) return launch_stream<FMT, WAVES, U, 2>(L, x, K, xq, s, rs, stream);
     if (WAVES < 8 || xv <= 4) return launch_stream<FMT, WAVES, U, 4>(L, x, K, xq, s, rs, stream);
