@@ -105,6 +105,14 @@ def test_fused_small_batch_8b_groups(M, K, Ns):
     _fused_case(("i2s", "tl1"), M, K, Ns, seed=inputs.seed_for(19, M * 31 + K + len(Ns)))
 
 
+# The same groups at 512 tokens (the prefill GEMM; split-K over the workspace where a launch has fewer tiles than
+# CUs), every output against the oracle, for the three layouts.
+@pytest.mark.parametrize("K,Ns", GROUPS_8B)
+def test_fused_prefill_512_8b_groups(K, Ns):
+    _announce("fused 8B-class group, 512 tokens", K, Ns)
+    _fused_case(("i2s", "tl2", "tl1"), 512, K, Ns, seed=inputs.seed_for(20, K + len(Ns)), split_ws=True)
+
+
 # 2..12 tokens through the fused call, both word formats: 1, 2 and 3 token groups of the multi-token stream,
 # K = 4160 (a 64-k last block), K = 4032 (a 192-k last block), K = 8192, several row groups per work group
 # (2900 row groups) and a single row group.
